@@ -1,0 +1,36 @@
+"""CPU oracle for shared-prefix continuous-sampling decode.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check in
+``__graft_entry__`` and the CPU-baseline leg of ``bench.py`` may import or run
+anything in this package.  The GPU library never calls it, and it shares no
+code with the GPU library: the two meet only at the seeded input generator in
+``workload/``.
+
+Two parts, both plain and slow on purpose:
+
+* ``attention`` -- float64 softmax attention of a decode query over the
+  concatenation of the shared prompt KV and the sample's own response KV
+  (Sections 2.1, 3.1 and 3.2 of the paper: one prompt KV cache shared by the
+  whole group, one private response buffer per active sample).
+* ``simulator`` -- the step-by-step slot / refill process of naive micro
+  sampling groups (Section 3.1), fixed-slot continuous sampling (Section 3.2)
+  and continuous refill in FIFO or shortest-job-first order (Algorithms 1
+  and 3).
+
+Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
+a library routine, brute force and a hand-derived worked example.
+"""
+
+from .attention import attend, attend_slot, attention_weights, default_scale
+from .simulator import POLICIES, SimResult, simulate, simulate_group
+
+__all__ = [
+    "attend",
+    "attend_slot",
+    "attention_weights",
+    "default_scale",
+    "POLICIES",
+    "SimResult",
+    "simulate",
+    "simulate_group",
+]

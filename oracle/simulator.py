@@ -1,0 +1,140 @@
+"""Step-by-step slot / refill simulator.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+The process follows the paper's decode loop (Algorithm 1, phase 2): at every
+running step each active slot decodes one token of its sample (a running step
+is one token-generation round over the g slots, Section 5.1); a sample that
+has produced its last token releases its slot, and the slot receives the next
+sample, which decodes its first token at the following step (Section 3.2).
+
+Refill policies:
+
+* ``naive``     -- micro sampling groups decoded one after another
+                   (Section 3.1): slots are refilled only once every slot is
+                   empty, with the next m sample ids in order.
+* ``fixed_row`` -- fixed-slot continuous sampling (Section 3.2, mode 1): slot
+                   s runs samples s, s+m, s+2m, ... back to back.
+* ``fifo``      -- continuous refill from the pending pool, lowest sample id
+                   first.
+* ``sjf``       -- shortest-job-first refill (Algorithm 3): the pending sample
+                   with the smallest predicted length, ties to the lowest id.
+
+Readings where the paper is silent: a sample of length L holds its slot for
+exactly L steps; when several slots free up in one step they are refilled in
+ascending slot order; the initial fill uses the same policy as every refill;
+Algorithm 3's candidate set is the samples neither finished nor already
+dispatched (its ``mask`` being the runtime dispatch record).
+"""
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Tuple
+
+import numpy as np
+
+POLICIES = ("naive", "fixed_row", "fifo", "sjf")
+
+
+@dataclass
+class SimResult:
+    steps: int
+    # log[k][s] = (sample, t) for slot s at step k+1 (t = tokens after this step), or None
+    log: List[Tuple[Optional[Tuple[int, int]], ...]]
+    tokens: np.ndarray                       # tokens decoded per sample
+    dispatch: List[Tuple[int, int, int]]     # (steps completed before, slot, sample)
+    finish_step: np.ndarray                  # step at which each sample produced its last token
+
+
+def simulate(L, m: int, policy: str, pred=None) -> SimResult:
+    """Simulate one prompt's group of G = len(L) samples on m slots."""
+    L = [int(x) for x in L]
+    G = len(L)
+    if m < 1:
+        raise ValueError("m must be >= 1")
+    if any(x < 1 for x in L):
+        raise ValueError("every sample has at least one token")
+    if policy not in POLICIES:
+        raise ValueError(f"unknown policy {policy!r}")
+    if policy == "sjf":
+        if pred is None:
+            raise ValueError("sjf needs predicted lengths")
+        pred = [float(x) for x in pred]
+
+    slot_sample = [None] * m      # sample id held by each slot, or None
+    slot_len = [0] * m            # tokens generated so far by that sample
+    pending = set(range(G))       # not yet dispatched
+    row_next = list(range(m))     # fixed_row: next sample id of each slot
+    naive_next = 0                # naive: first id of the next micro group
+    tokens = np.zeros(G, dtype=np.int64)
+    finish = np.full(G, -1, dtype=np.int64)
+    log = []
+    dispatch = []
+    step = 0
+
+    def fill():
+        nonlocal naive_next
+        if policy == "naive":
+            if any(x is not None for x in slot_sample) or naive_next >= G:
+                return
+            for s in range(m):
+                if naive_next < G:
+                    give(s, naive_next)
+                    naive_next += 1
+            return
+        for s in range(m):
+            if slot_sample[s] is not None:
+                continue
+            if policy == "fixed_row":
+                j = row_next[s]
+                if j >= G:
+                    continue
+                row_next[s] = j + m
+            elif policy == "fifo":
+                if not pending:
+                    return
+                j = min(pending)
+            else:  # sjf
+                if not pending:
+                    return
+                j = min(pending, key=lambda i: (pred[i], i))
+            give(s, j)
+
+    def give(s, j):
+        pending.discard(j)
+        slot_sample[s] = j
+        slot_len[s] = 0
+        dispatch.append((step, s, j))
+
+    fill()
+    while any(x is not None for x in slot_sample):
+        step += 1
+        row = []
+        for s in range(m):
+            j = slot_sample[s]
+            if j is None:
+                row.append(None)
+                continue
+            slot_len[s] += 1
+            tokens[j] += 1
+            row.append((j, slot_len[s]))
+        log.append(tuple(row))
+        for s in range(m):
+            j = slot_sample[s]
+            if j is not None and slot_len[s] == L[j]:
+                finish[j] = step
+                slot_sample[s] = None
+        fill()
+    return SimResult(steps=step, log=log, tokens=tokens, dispatch=dispatch, finish_step=finish)
+
+
+def simulate_group(L, m: int, policy: str, pred=None):
+    """Several prompts decoded in one batch, each with its own m slots and
+    pending pool.  A step advances every prompt; the batch ends when the last
+    prompt's group is done.  Returns (total steps, per-prompt SimResults)."""
+    L = np.asarray(L)
+    if L.ndim == 1:
+        L = L[None, :]
+    if pred is not None:
+        pred = np.asarray(pred).reshape(L.shape)
+    res = [simulate(L[p], m, policy, None if pred is None else pred[p]) for p in range(L.shape[0])]
+    return max(r.steps for r in res), res
