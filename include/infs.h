@@ -1,0 +1,211 @@
+/*
+ * infs -- shared-prefix continuous-sampling decode attention for one MI355X
+ * (gfx950).  C ABI: plain pointers and sizes only.
+ *
+ * The operations follow the problem statement of "Infinite Sampling"
+ * (arXiv 2506.22950):
+ *   - the G completions of a prompt share one prefill KV cache, kept for the
+ *     whole group (Section 3.1, "KV Cache Pooling"; Section 3.2, "Shared
+ *     Prompt KV and Sample-Level Cache Lifecycle")          -> infs_prefill_shared
+ *   - a fixed pool holds the response KV of the m live slots; every running
+ *     step decodes one token for each live slot, through every layer
+ *     (Section 2.1; Section 5.1, definition of a running step)
+ *                                                          -> infs_decode_step, infs_end_step
+ *   - a finished sample releases its slot and buffer, and the slot is refilled
+ *     at once with a pending sample that starts at the next step
+ *     (Section 3.2; Algorithm 1, phase 2)                  -> infs_retire_slot, infs_refill_slot
+ *   - the refill order: naive micro groups (Section 3.1), fixed-slot rows
+ *     (Section 3.2), FIFO, or shortest-job-first on predicted lengths
+ *     (Algorithm 3)                                         -> infs_sched_*
+ *
+ * Attention computed by infs_decode_step, per live slot s holding sample i of
+ * prompt p with t generated tokens (the token of this step included), per
+ * query head h:
+ *     g   = h / (Hq / Hkv)                       (grouped-query KV head)
+ *     K   = [ prefix_p K[0:P_p, g] ; response_(p,i) K[0:t, g] ]   (V alike)
+ *     o_h = softmax(scale * K q_h) V,  scale = 1/sqrt(head_dim) unless set.
+ *
+ * Conventions for every call:
+ *   - Every function returns an infs_status; nothing throws or aborts across
+ *     the ABI.  infs_last_error() gives the message of the last failure.
+ *   - Arguments and state are validated on the host before anything is
+ *     enqueued, so argument and state errors are synchronous and leave the
+ *     context unchanged.  A failed HIP call or kernel launch makes the
+ *     context return INFS_E_DEVICE from then on.
+ *   - Device work is enqueued on the HIP stream given to infs_create; no call
+ *     synchronises except infs_sync, infs_sample_tokens and infs_timing_end.
+ *   - "_dev" pointers are device (HBM) pointers owned by the caller; they
+ *     must stay valid until the stream work that reads or writes them is
+ *     done.  Host pointers are read or written before the call returns.
+ *   - Element type of Q/K/V buffers is the context dtype (fp32, or bf16 as
+ *     raw 16-bit patterns); O is always fp32.
+ *   - A context must be used from one host thread at a time.
+ */
+#ifndef INFS_H
+#define INFS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define INFS_ABI_VERSION 1
+
+typedef enum infs_status {
+    INFS_OK = 0,
+    INFS_E_ARG = -1,       /* invalid argument (shape, index, null pointer, unsupported shape) */
+    INFS_E_STATE = -2,     /* call not allowed in the current slot / step state */
+    INFS_E_CAPACITY = -3,  /* a response would exceed max_suffix_len, or the page pool is full */
+    INFS_E_DUP = -4,       /* the sample id was already dispatched in this group */
+    INFS_E_NOMEM = -5,     /* device allocation failed */
+    INFS_E_DEVICE = -6     /* a HIP call failed; sticky for the context */
+} infs_status;
+
+typedef enum infs_dtype { INFS_F32 = 0, INFS_BF16 = 1 } infs_dtype;
+
+/* Refill policies of the host scheduler. */
+typedef enum infs_policy {
+    INFS_NAIVE = 0,      /* micro groups one after another: refill only when all m slots are empty,
+                            with the next m sample ids (Section 3.1) */
+    INFS_FIXED_ROW = 1,  /* fixed-slot continuous sampling: slot s runs s, s+m, s+2m, ... (Section 3.2) */
+    INFS_FIFO = 2,       /* continuous refill with the lowest pending sample id */
+    INFS_SJF = 3         /* continuous refill with the smallest predicted length, ties to the
+                            lowest id (Algorithm 3) */
+} infs_policy;
+
+/* Bookkeeping only: no device memory, no kernels, pointers are not read.
+   Lets the slot / page / step state machine run on a host without a GPU. */
+#define INFS_FLAG_DRY_RUN 1u
+
+typedef struct infs_config {
+    int32_t num_layers;          /* >= 1 */
+    int32_t num_q_heads;         /* Hq, a multiple of num_kv_heads */
+    int32_t num_kv_heads;        /* Hkv */
+    int32_t head_dim;            /* d: 64 or 128 */
+    int32_t num_prompts;         /* prompts decoded in one batch, 1..16 */
+    int32_t slots_per_prompt;    /* m live slots per prompt; slot s serves prompt s / m */
+    int32_t samples_per_prompt;  /* G: sample ids of a prompt are 0..G-1 */
+    int32_t max_prompt_len;      /* capacity of the shared prefix per prompt, >= 0 */
+    int32_t max_suffix_len;      /* capacity of one response, >= 1 */
+    int32_t page_tokens;         /* tokens per response page; 0 or 16 */
+    int32_t num_pages;           /* response page pool size; 0: enough for every slot at capacity */
+    int32_t split_tokens;        /* split-K chunk length in tokens; 0: 256; a multiple of 128 */
+    int32_t dtype;               /* infs_dtype of Q, K, V */
+    float scale;                 /* softmax scale; 0: 1/sqrt(head_dim) */
+    uint32_t flags;              /* INFS_FLAG_* */
+} infs_config;
+
+typedef struct infs_ctx infs_ctx;
+
+/* Totals since creation or the last infs_reset (host-side counts). */
+typedef struct infs_stats {
+    int64_t steps;               /* infs_end_step calls */
+    int64_t launches;            /* attention kernel launches (one per decode_step) */
+    int64_t tokens;              /* tokens generated (live slots summed over steps) */
+    double alg_bytes;            /* algorithmic HBM bytes of all decode_step launches: prefix K/V
+                                    once per prompt with a live slot, each live slot's response K/V,
+                                    new K/V read and append write, Q read, O write */
+    double alg_flops;            /* 4 * Hq * d * (P + t) per live slot and layer */
+} infs_stats;
+
+int32_t infs_abi_version(void);
+
+/* Create a context: validates cfg, allocates the prefix store, the response page pool, the slot
+   table and the split-K workspace on the current HIP device (all zero-initialised), and records
+   `hip_stream` (a hipStream_t; NULL = default stream) for all later work.  On failure *out is NULL
+   and infs_last_error(NULL) describes why. */
+infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out);
+
+/* Free everything infs_create allocated.  Waits for the context's stream first.  NULL is a no-op. */
+void infs_destroy(infs_ctx* ctx);
+
+/* Return to the just-created state (no prefix prefilled, every slot empty, no sample dispatched,
+   token counters zero, stats zero), keeping allocations.  Enqueues a clear of the device counters. */
+infs_status infs_reset(infs_ctx* ctx);
+
+/* Copy one prompt's prefill K and V for one layer into the shared-prefix store (Section 3.1:
+   the prompt's KV cache is kept and shared by every micro group).
+   k_dev, v_dev: [prompt_len, Hkv, head_dim] row-major, context dtype.  prompt_len in
+   [0, max_prompt_len]; every layer of a prompt must use the same prompt_len.  Not allowed while
+   a step is open (between the first decode_step of a step and end_step). */
+infs_status infs_prefill_shared(infs_ctx* ctx, int32_t prompt, int32_t layer, int32_t prompt_len,
+                                const void* k_dev, const void* v_dev);
+
+/* Give empty slot `slot` the sample `sample_id` of `prompt` (which must be slot / m).  The sample
+   starts with an empty response and decodes its first token at the next decode step.
+   E_STATE: slot is live, or a step is open.  E_DUP: sample_id already dispatched for this prompt. */
+infs_status infs_refill_slot(infs_ctx* ctx, int32_t slot, int32_t prompt, int64_t sample_id);
+
+/* Release a live slot: its response pages return to the pool (the sample's buffer is recycled on
+   completion, Section 3.2).  E_STATE: slot is empty, or a step is open. */
+infs_status infs_retire_slot(infs_ctx* ctx, int32_t slot);
+
+/* One layer of one running step for every slot:
+   live slots append this step's K/V (position = current length) to their response, then attend
+   over [prefix ; response]; idle slots' rows are ignored and their O rows are written as 0.
+   q_dev: [S, Hq, d]; k_new_dev, v_new_dev: [S, Hkv, d] (context dtype); o_dev: [S, Hq, d] fp32,
+   with S = num_prompts * slots_per_prompt, slot-major.  Each layer must be decoded exactly once
+   per step.  E_STATE: layer already decoded in this step, or a live slot's prompt has no prefix
+   for this layer.  E_CAPACITY: a response would pass max_suffix_len or the page pool is empty. */
+infs_status infs_decode_step(infs_ctx* ctx, int32_t layer, const void* q_dev, const void* k_new_dev,
+                             const void* v_new_dev, float* o_dev);
+
+/* Close the step: every live slot's length grows by one.  E_STATE unless every layer was decoded
+   exactly once since the previous end_step (a step with no live slot needs no decode). */
+infs_status infs_end_step(infs_ctx* ctx);
+
+/* Host mirror of a slot: *sample_id = -1 and *len = 0 when empty. */
+infs_status infs_slot_state(const infs_ctx* ctx, int32_t slot, int64_t* sample_id, int32_t* len);
+
+/* Synchronise and copy the device per-sample token counters of `prompt` (tokens appended at layer
+   0, counted on the GPU) into counts_host[0..n).  n must equal samples_per_prompt. */
+infs_status infs_sample_tokens(infs_ctx* ctx, int32_t prompt, int32_t* counts_host, int32_t n);
+
+/* Wait for all work enqueued by the context. */
+infs_status infs_sync(infs_ctx* ctx);
+
+infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
+
+/* Kernel timing: between begin and end every decode_step launch is bracketed by HIP events on
+   the context's stream.  infs_timing_end synchronises and returns the summed kernel time (ms) and
+   the number of timed launches. */
+infs_status infs_timing_begin(infs_ctx* ctx);
+infs_status infs_timing_end(infs_ctx* ctx, double* kernel_ms, int64_t* launches);
+
+/* Message of the last failed call on ctx (NULL ctx: last failed infs_create / infs_sched_create
+   of this thread).  Never NULL. */
+const char* infs_last_error(const infs_ctx* ctx);
+
+/* ---------------------------------------------------------------------------------------------
+ * Host scheduler (CPU only, no device): chooses which sample a freed slot receives.
+ * One scheduler serves one prompt's m slots (local slot ids 0..m-1) and G samples.
+ * Use: after the retirements of a step, call infs_sched_next for every empty slot in ascending
+ * slot order; a returned id is dispatched (pass it to infs_refill_slot).  Call infs_sched_done
+ * when a slot's sample finishes.
+ * ------------------------------------------------------------------------------------------- */
+typedef struct infs_sched infs_sched;
+
+/* pred_len: G predicted lengths (float64), required for INFS_SJF, ignored otherwise (may be NULL).
+   The array is copied. */
+infs_status infs_sched_create(int32_t G, int32_t m, int32_t policy, const double* pred_len,
+                              infs_sched** out);
+
+/* Next sample for empty slot `slot`: *sample_out = id, or -1 when the policy dispatches nothing
+   now (naive: some slot of the current micro group still runs; every policy: no candidate left).
+   E_STATE if the slot already holds a sample. */
+infs_status infs_sched_next(infs_sched* s, int32_t slot, int64_t* sample_out);
+
+/* The sample in `slot` finished; the slot becomes empty.  E_STATE if the slot is empty. */
+infs_status infs_sched_done(infs_sched* s, int32_t slot);
+
+/* Samples not yet dispatched. */
+int32_t infs_sched_pending(const infs_sched* s);
+
+void infs_sched_destroy(infs_sched* s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INFS_H */

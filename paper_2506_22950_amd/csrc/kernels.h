@@ -1,0 +1,36 @@
+// Launch entry points of the HIP kernels (host side).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "plan.h"
+
+namespace infs {
+
+// Which instantiation of the decode kernel serves a context.
+struct KernelKey {
+  int bf16;        // 0: fp32 Q/K/V, 1: bf16
+  int head_dim;    // 64 or 128
+  int hpk;         // query heads per KV head
+  int mfma;        // 1: prefix rows go through MFMA tiles, 0: wavefront reductions
+  int prefix_rows; // rows of one prompt's prefix work item, padded (wave: 8/16; MFMA: 16/32/64)
+};
+
+// Resolve the padded prefix row count and path for a shape; false if no
+// instantiation exists.
+bool select_kernel(int bf16, int head_dim, int hpk, int prefix_rows_real, KernelKey* key);
+
+// Record layout of the split-K workspace for a key.
+int64_t workspace_records(const KernelKey& key, int num_prompts, int hkv, int prefix_chunks_max,
+                          int num_slots, int suffix_chunks_max);
+
+// Prefix store elements per (prompt, kv head) for a key and capacity.
+int64_t prefix_elems_per_head(const KernelKey& key, int max_prompt_len_padded);
+
+hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream);
+
+// Copy one prompt's K/V [plen, Hkv, D] into the shared-prefix store (layout chosen by key).
+hipError_t launch_prefill(const KernelKey& key, void* prefix_layer, const void* k, const void* v,
+                          int prompt, int plen, int hkv, int max_prompt_len_padded, hipStream_t stream);
+
+}  // namespace infs

@@ -1,0 +1,793 @@
+// HIP kernels for gfx950 (CDNA4): shared-prefix continuous-sampling decode.
+//
+// One launch per layer-step does all the device work of that layer:
+//   * append: each live slot's new K/V row goes into its response pages;
+//   * split-K attention over the shared prefix: one work-group per
+//     (prompt, KV head, chunk of `split` prefix tokens).  Every K/V byte of the
+//     chunk is read from HBM once and used by all m * hpk query rows of that
+//     KV head -- the rows of every live slot of the prompt.  With >= 16 rows
+//     the two contractions run on MFMA tiles (v_mfma_f32_16x16x32_bf16);
+//     below that, on wavefront dot products;
+//   * split-K attention over each live slot's private response (hpk rows per
+//     KV byte, wavefront dot products);
+//   * log-sum-exp merge: the last work-group to finish for a (slot, KV head)
+//     combines the partial softmaxes of all its chunks and writes O.
+// Idle slots get O = 0.
+//
+// A partial over a key set J is (M, L, O) with scores in log2 units
+// (s_j = scale * log2(e) * q.k_j): M = max_j s_j, L = sum_j 2^(s_j - M),
+// O = sum_j 2^(s_j - M) v_j.  Two partials combine exactly as
+// M = max(M1, M2), L = 2^(M1-M) L1 + 2^(M2-M) L2, O likewise, and the result
+// is O / L.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace infs {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
+#define NEG_INF (-__builtin_huge_valf())
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Lane permutations inside 16-lane DPP rows (row_mask = bank_mask = all).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over each aligned group of N consecutive lanes; every lane gets its group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(N == 2 || N == 4 || N == 8 || N == 16 || N == 32 || N == 64, "group size");
+  x += dpp<0xB1>(x);                       // quad_perm [1,0,3,2]: lane ^ 1
+  if constexpr (N >= 4) x += dpp<0x4E>(x); // quad_perm [2,3,0,1]: lane ^ 2
+  if constexpr (N == 8) x += dpp<0x141>(x);  // row_half_mirror: quad 0 <-> quad 1
+  if constexpr (N >= 16) {
+    x += dpp<0x124>(x);                    // row_ror:4
+    x += dpp<0x128>(x);                    // row_ror:8
+  }
+  if constexpr (N >= 32) x += __shfl_xor(x, 16);
+  if constexpr (N >= 64) x += __shfl_xor(x, 32);
+  return x;
+}
+
+// Combine partial (m2, l2) into (m, l); returns the weights of the old and new parts.
+__device__ __forceinline__ void lse_combine(float& m, float& l, float m2, float l2, float& a, float& b) {
+  const float mn = fmaxf(m, m2);
+  const float mu = (mn == NEG_INF) ? 0.f : mn;
+  a = exp2_fast(m - mu);
+  b = exp2_fast(m2 - mu);
+  l = l * a + l2 * b;
+  m = mn;
+}
+
+// 16-byte chunk helpers: 8 bf16 or 4 fp32 elements.
+template <bool BF>
+__device__ __forceinline__ float dot16B(const u32x4& k, const u32x4& q) {
+  if constexpr (BF) {
+    // Pairs are taken with shufflevector from a whole-vector cast: casting the
+    // individual 32-bit lanes to bf16x2 is mis-lowered by this compiler (all
+    // four dots read the same dword).
+    const bf16x8 kv = __builtin_bit_cast(bf16x8, k), qv = __builtin_bit_cast(bf16x8, q);
+    float s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 0, 1), __builtin_shufflevector(qv, qv, 0, 1), 0.f, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 2, 3), __builtin_shufflevector(qv, qv, 2, 3), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 4, 5), __builtin_shufflevector(qv, qv, 4, 5), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 6, 7), __builtin_shufflevector(qv, qv, 6, 7), s, false);
+    return s;
+  } else {
+    float s = __uint_as_float(k.x) * __uint_as_float(q.x);
+    s = fmaf(__uint_as_float(k.y), __uint_as_float(q.y), s);
+    s = fmaf(__uint_as_float(k.z), __uint_as_float(q.z), s);
+    s = fmaf(__uint_as_float(k.w), __uint_as_float(q.w), s);
+    return s;
+  }
+}
+
+template <bool BF>
+__device__ __forceinline__ void axpy16B(float* o, float p, const u32x4& v) {
+  if constexpr (BF) {
+    o[0] = fmaf(p, bf_lo(v.x), o[0]); o[1] = fmaf(p, bf_hi(v.x), o[1]);
+    o[2] = fmaf(p, bf_lo(v.y), o[2]); o[3] = fmaf(p, bf_hi(v.y), o[3]);
+    o[4] = fmaf(p, bf_lo(v.z), o[4]); o[5] = fmaf(p, bf_hi(v.z), o[5]);
+    o[6] = fmaf(p, bf_lo(v.w), o[6]); o[7] = fmaf(p, bf_hi(v.w), o[7]);
+  } else {
+    o[0] = fmaf(p, __uint_as_float(v.x), o[0]); o[1] = fmaf(p, __uint_as_float(v.y), o[1]);
+    o[2] = fmaf(p, __uint_as_float(v.z), o[2]); o[3] = fmaf(p, __uint_as_float(v.w), o[3]);
+  }
+}
+
+// Compile-time shape of one kernel instantiation.
+template <bool BF_, int D_, int HPK_, bool MFMA_, int PR_>
+struct Shape {
+  static constexpr bool BF = BF_;
+  static constexpr int D = D_;
+  static constexpr int HPK = HPK_;
+  static constexpr bool MFMA = MFMA_;
+  static constexpr int PR = PR_;                  // prefix rows per record group (padded)
+  static constexpr int ES = BF ? 2 : 4;            // element bytes
+  static constexpr int EPL = 16 / ES;              // elements per lane chunk
+  static constexpr int ROWB = D * ES;              // bytes of one K or V row of one head
+  static constexpr int LPT = ROWB / 16;            // lanes per token (wavefront path)
+  static constexpr int TPI = 64 / LPT;             // tokens per load instruction
+  static constexpr int U = (32 / TPI) < 8 ? (32 / TPI) : 8;  // unrolled loads per iteration
+  static constexpr int PAGEB = kPageTokens * ROWB; // bytes of one page of one head, K or V
+  static constexpr int NB = PR / 16;               // MFMA row blocks
+  static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
+  static constexpr int DB = D / 16;                // MFMA 16-wide head_dim blocks
+  static constexpr int WAVE_NR = (!MFMA && PR > HPK) ? PR : HPK;
+  static constexpr int WAVE_SMEM = 4 * WAVE_NR * (D + 2);
+  static constexpr int MFMA_SLOT = MFMA ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
+  static constexpr int MFMA_SMEM = 2 * MFMA_SLOT;
+  static constexpr int SMEM = WAVE_SMEM > MFMA_SMEM ? WAVE_SMEM : MFMA_SMEM;
+  static_assert(LPT >= 2 && LPT <= 64, "row size");
+  static_assert(!MFMA || BF, "MFMA path is bf16");
+  static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
+};
+
+// ----------------------------------------------------------------------------
+// Wavefront path: NR query rows, token range [t0, t1) of one KV head.
+// Lane layout: LPT consecutive lanes hold one token's row (16 B each); a load
+// instruction covers TPI tokens.  Each token group keeps its own running
+// (m, l, o) and the groups are combined at the end.
+// ----------------------------------------------------------------------------
+template <class SH, int NR, class Addr>
+__device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, const u32x4 (&q)[NR], float sl2,
+                                             float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
+  constexpr int LPT = SH::LPT, TPI = SH::TPI, U = SH::U, EPL = SH::EPL;
+  const int lane = threadIdx.x & 63, ts = lane / LPT, ch = lane % LPT;
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    m[r] = NEG_INF;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
+  }
+  for (int base = t0; base < t1; base += U * TPI) {
+    u32x4 kk[U], vv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int tok = base + u * TPI + ts;
+      if (tok < t1) {
+        kk[u] = *ad.k(tok, ch);
+        vv[u] = *ad.v(tok, ch);
+      } else {
+        kk[u] = u32x4{0, 0, 0, 0};
+        vv[u] = u32x4{0, 0, 0, 0};
+      }
+    }
+    float s[U][NR];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool ok = base + u * TPI + ts < t1;
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const float x = group_sum<LPT>(dot16B<SH::BF>(kk[u], q[r])) * sl2;
+        s[u][r] = ok ? x : NEG_INF;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      float mb = s[0][r];
+#pragma unroll
+      for (int u = 1; u < U; ++u) mb = fmaxf(mb, s[u][r]);
+      const float mn = fmaxf(m[r], mb);
+      const float mu = (mn == NEG_INF) ? 0.f : mn;
+      const float corr = exp2_fast(m[r] - mu);
+      m[r] = mn;
+      l[r] *= corr;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[r][e] *= corr;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const float p = exp2_fast(s[u][r] - mu);
+        l[r] += p;
+        axpy16B<SH::BF>(o[r], p, vv[u]);
+      }
+    }
+  }
+  // Combine the TPI token groups of this wavefront (lanes ch, ch+LPT, ...).
+#pragma unroll
+  for (int mask = LPT; mask < 64; mask <<= 1) {
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const float m2 = __shfl_xor(m[r], mask);
+      const float l2 = __shfl_xor(l[r], mask);
+      float a, b;
+      lse_combine(m[r], l[r], m2, l2, a, b);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) o[r][e] = o[r][e] * a + __shfl_xor(o[r][e], mask) * b;
+    }
+  }
+}
+
+// Combine the four wavefronts' partials through LDS and store the block's
+// partial rows [0, NR) at records rec0 + r.
+template <class SH, int NR>
+__device__ __forceinline__ void block_store_partial(float* smem, const float (&m)[NR], const float (&l)[NR],
+                                                    const float (&o)[NR][SH::EPL], float* ws_o, float* ws_ml,
+                                                    int64_t rec0) {
+  constexpr int D = SH::D, EPL = SH::EPL;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  float* so = smem;                   // [4][NR][D]
+  float* sml = smem + 4 * NR * D;     // [4][NR][2]
+  if (lane < SH::LPT) {
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) so[(w * NR + r) * D + lane * EPL + e] = o[r][e];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      sml[(w * NR + r) * 2 + 0] = m[r];
+      sml[(w * NR + r) * 2 + 1] = l[r];
+    }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < NR * D; idx += kBlockThreads) {
+    const int r = idx / D, d = idx - r * D;
+    float M = NEG_INF;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, sml[(v * NR + r) * 2]);
+    const float Mu = (M == NEG_INF) ? 0.f : M;
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float wgt = exp2_fast(sml[(v * NR + r) * 2] - Mu);
+      L += wgt * sml[(v * NR + r) * 2 + 1];
+      O += wgt * so[(v * NR + r) * D + d];
+    }
+    ws_o[(rec0 + r) * D + d] = O;
+    if (d == 0) {
+      ws_ml[(rec0 + r) * 2 + 0] = M;
+      ws_ml[(rec0 + r) * 2 + 1] = L;
+    }
+  }
+}
+
+// Addressing of the plain prefix store: [prompt][kv][K|V][max_prompt_len][D].
+template <class SH>
+struct PrefixAddr {
+  const char* kb;
+  const char* vb;
+  __device__ const u32x4* k(int tok, int ch) const { return (const u32x4*)(kb + (int64_t)tok * SH::ROWB) + ch; }
+  __device__ const u32x4* v(int tok, int ch) const { return (const u32x4*)(vb + (int64_t)tok * SH::ROWB) + ch; }
+};
+
+// Addressing of a slot's response: pages [page][kv][K|V][16][D]; the token of
+// this step (position len-1) is read from the caller's new K/V rows.
+template <class SH>
+struct SuffixAddr {
+  const char* pool;
+  const int32_t* pt;   // this slot's page table
+  const char* knew;    // this slot's new K row for this KV head
+  const char* vnew;
+  int last;
+  int hkv, g;
+  __device__ const char* page(int tok, int kind) const {
+    const int pg = pt[tok >> 4];
+    return pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tok & 15) * SH::ROWB;
+  }
+  __device__ const u32x4* k(int tok, int ch) const {
+    return (tok == last) ? (const u32x4*)knew + ch : (const u32x4*)page(tok, 0) + ch;
+  }
+  __device__ const u32x4* v(int tok, int ch) const {
+    return (tok == last) ? (const u32x4*)vnew + ch : (const u32x4*)page(tok, 1) + ch;
+  }
+};
+
+__device__ __forceinline__ int64_t prefix_records(const StepArgs& a, int pr) {
+  return (int64_t)a.num_prompts * a.prefix_chunks_max * a.Hkv * pr;
+}
+
+// ----------------------------------------------------------------------------
+// Prefix chunk, wavefront path (fewer than 16 rows): rows r = slot_in_prompt * hpk + j.
+// ----------------------------------------------------------------------------
+template <class SH>
+__device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem) {
+  constexpr int PR = SH::PR, HPK = SH::HPK;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
+  const int plen = a.prompt[p].plen;
+  const int t0 = c * a.split, t1 = min(t0 + a.split, plen);
+  const int sub = a.split / 4;
+  const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
+  u32x4 q[PR];
+#pragma unroll
+  for (int r = 0; r < PR; ++r) {
+    const int si = r / HPK, j = r - si * HPK, s = p * a.m + min(si, a.m - 1);
+    if (r < a.prefix_rows && a.slot[s].len > 0)
+      q[r] = *((const u32x4*)((const char*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * SH::ROWB) + ch);
+    else
+      q[r] = u32x4{0, 0, 0, 0};
+  }
+  const int64_t head = ((int64_t)p * a.Hkv + g) * 2;
+  PrefixAddr<SH> ad{(const char*)a.prefix + head * a.max_prompt_len * SH::ROWB,
+                    (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::ROWB};
+  float m[PR], l[PR], o[PR][SH::EPL];
+  wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
+  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * PR;
+  block_store_partial<SH, PR>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
+}
+
+// ----------------------------------------------------------------------------
+// Prefix chunk, MFMA path (R = NB*16 rows).  Per 32-token block:
+//   S^T[tok][row] = K[tok][:] . Q[row][:]     (A = K block, B = Q^T; 2 x NB tiles of 16x16)
+//   O^T[d][row]  += V^T[d][tok] P^T[tok][row] (A = V^T, B = P^T; NB x DB tiles)
+// With S^T, O^T and the running (m, l) all indexed by row = lane % 16, the
+// online-softmax rescale needs no cross-lane transpose.  The P^T operand takes
+// the 8 probabilities a lane already holds; the contraction index (token) is
+// the same permutation on both operands, and the prefix store keeps V in that
+// order (see prefill_mfma_kernel).
+// ----------------------------------------------------------------------------
+template <class SH>
+__device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
+  constexpr int D = SH::D, NB = SH::NB, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
+  const int plen = a.prompt[p].plen;
+  const int t0 = c * a.split, t1 = min(t0 + a.split, plen);
+  const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
+  const int bpw = a.split / kMfmaBlock / 4;
+  const int b0 = w * bpw, b1 = min(b0 + bpw, nblk);
+  const float sl2 = a.scale_log2;
+
+  bf16x8 bq[NB][KB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int row = nb * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
+    const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
+    const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      if (ok)
+        bq[nb][kb] = *(const bf16x8*)(qr + kb * 32 + q4 * 8);
+      else
+        bq[nb][kb] = bf16x8{};
+    }
+  }
+
+  f32x4 acc[NB][DB];
+  float mrow[NB], lrow[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    mrow[nb] = NEG_INF;
+    lrow[nb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const uint16_t* head = (const uint16_t*)a.prefix +
+                         ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D);
+  for (int b = b0; b < b1; ++b) {
+    const int tb = t0 + b * kMfmaBlock;
+    const uint16_t* kblk = head + (int64_t)(tb / kMfmaBlock) * (2 * kMfmaBlock * D);
+    const uint16_t* vblk = kblk + kMfmaBlock * D;
+    bf16x8 ka[2][KB], va[DB];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = *(const bf16x8*)(kblk + ((mb * KB + kb) * 64 + lane) * 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
+
+    f32x4 st[2][NB];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mb][kb], bq[nb][kb], t, 0, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int tok = tb + mb * 16 + q4 * 4 + e;
+          t[e] = (tok < t1) ? t[e] * sl2 : NEG_INF;
+        }
+        st[mb][nb] = t;
+      }
+
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float mb_ = fmaxf(fmaxf(fmaxf(st[0][nb][0], st[0][nb][1]), fmaxf(st[0][nb][2], st[0][nb][3])),
+                        fmaxf(fmaxf(st[1][nb][0], st[1][nb][1]), fmaxf(st[1][nb][2], st[1][nb][3])));
+      mb_ = fmaxf(mb_, __shfl_xor(mb_, 16));
+      mb_ = fmaxf(mb_, __shfl_xor(mb_, 32));
+      const float mn = fmaxf(mrow[nb], mb_);
+      const float mu = (mn == NEG_INF) ? 0.f : mn;
+      const float corr = exp2_fast(mrow[nb] - mu);
+      mrow[nb] = mn;
+      lrow[nb] *= corr;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[nb][db] *= corr;
+      bf16x8 pb;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const __bf16 h = (__bf16)exp2_fast(st[mb][nb][e] - mu);
+          pb[mb * 4 + e] = h;
+          lrow[nb] += (float)h;
+        }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[db], pb, acc[nb][db], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    lrow[nb] += __shfl_xor(lrow[nb], 16);
+    lrow[nb] += __shfl_xor(lrow[nb], 32);
+  }
+
+  // Tree-combine the four wavefronts through two LDS slots (lane-major fragments).
+  constexpr int OFL = NB * DB * 64 * 4;
+  auto put = [&](float* sl) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
+      sl[OFL + nb * 64 + lane] = mrow[nb];
+      sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
+    }
+  };
+  auto take = [&](const float* sl) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      float a, b;
+      lse_combine(mrow[nb], lrow[nb], sl[OFL + nb * 64 + lane], sl[OFL + NB * 64 + nb * 64 + lane], a, b);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) acc[nb][db] = acc[nb][db] * a + *(const f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) * b;
+    }
+  };
+  if (w >= 2) put(smem + (w - 2) * SH::MFMA_SLOT);
+  __syncthreads();
+  if (w < 2) take(smem + w * SH::MFMA_SLOT);
+  __syncthreads();
+  if (w == 1) put(smem);
+  __syncthreads();
+  if (w == 0) {
+    take(smem);
+    const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int64_t rec = rec0 + nb * 16 + r16;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *(f32x4*)(a.ws_o + rec * D + db * 16 + q4 * 4) = acc[nb][db];
+      if (q4 == 0) {
+        a.ws_ml[rec * 2 + 0] = mrow[nb];
+        a.ws_ml[rec * 2 + 1] = lrow[nb];
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Response chunk of one live slot (hpk rows), plus the append of this step's
+// K/V when the chunk holds the newest position.
+// ----------------------------------------------------------------------------
+template <class SH>
+__device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem) {
+  constexpr int HPK = SH::HPK;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
+  const SlotPlan& sp = a.slot[s];
+  const int len = sp.len;
+  const int t0 = c * a.split, t1 = min(t0 + a.split, len);
+  const int sub = a.split / 4;
+  const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
+  u32x4 q[HPK];
+#pragma unroll
+  for (int r = 0; r < HPK; ++r)
+    q[r] = *((const u32x4*)((const char*)a.q + ((int64_t)s * a.Hq + g * HPK + r) * SH::ROWB) + ch);
+  const int64_t newrow = ((int64_t)s * a.Hkv + g) * SH::ROWB;
+  SuffixAddr<SH> ad{(const char*)a.pool, a.page_table + (int64_t)s * a.pages_per_slot,
+                    (const char*)a.knew + newrow, (const char*)a.vnew + newrow, len - 1, a.Hkv, g};
+  float m[HPK], l[HPK], o[HPK][SH::EPL];
+  wave_partial<SH, HPK>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
+  const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.suffix_chunks_max + c) * a.Hkv + g) * HPK;
+  block_store_partial<SH, HPK>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
+
+  if (t1 == len) {  // append this step's K/V at position len-1
+    const int pos = len - 1;
+    const int tid = threadIdx.x;
+    if (tid < 2 * SH::LPT) {
+      const int kind = tid / SH::LPT, cc = tid % SH::LPT;
+      const u32x4* src = (const u32x4*)((const char*)(kind ? a.vnew : a.knew) + newrow) + cc;
+      char* dst = (char*)a.pool + ((int64_t)(sp.cur_page * a.Hkv + g) * 2 + kind) * SH::PAGEB + (pos & 15) * SH::ROWB;
+      *((u32x4*)dst + cc) = *src;
+    }
+    if (g == 0 && tid == 0) {
+      a.page_table[(int64_t)s * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
+      if (a.count_tokens) {
+        const int p = s / a.m;
+        a.tokens[p * a.G + sp.sample] += 1;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. g*hpk+hpk-1.
+// ----------------------------------------------------------------------------
+template <class SH>
+__device__ void merge_slot(const StepArgs& a, int s, int g) {
+  constexpr int D = SH::D, HPK = SH::HPK;
+  const int p = s / a.m, si = s - p * a.m;
+  const int nP = a.prompt[p].nchunks;
+  const int nS = (a.slot[s].len + a.split - 1) / a.split;
+  const int64_t pbase = ((int64_t)p * a.prefix_chunks_max * a.Hkv + g) * SH::PR;  // + c*Hkv*PR + row
+  const int64_t pstride = (int64_t)a.Hkv * SH::PR;
+  const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
+  const int64_t sstride = (int64_t)a.Hkv * HPK;
+  for (int idx = threadIdx.x; idx < HPK * D; idx += kBlockThreads) {
+    const int j = idx / D, d = idx - j * D;
+    const int64_t prow = pbase + si * HPK + j, srow = sbase + j;
+    float M = NEG_INF;
+    for (int c = 0; c < nP; ++c) M = fmaxf(M, a.ws_ml[(prow + c * pstride) * 2]);
+    for (int c = 0; c < nS; ++c) M = fmaxf(M, a.ws_ml[(srow + c * sstride) * 2]);
+    float L = 0.f, O = 0.f;
+    for (int c = 0; c < nP; ++c) {
+      const int64_t rec = prow + c * pstride;
+      const float wgt = exp2_fast(a.ws_ml[rec * 2] - M);
+      L += wgt * a.ws_ml[rec * 2 + 1];
+      O += wgt * a.ws_o[rec * D + d];
+    }
+    for (int c = 0; c < nS; ++c) {
+      const int64_t rec = srow + c * sstride;
+      const float wgt = exp2_fast(a.ws_ml[rec * 2] - M);
+      L += wgt * a.ws_ml[rec * 2 + 1];
+      O += wgt * a.ws_o[rec * D + d];
+    }
+    a.o[((int64_t)s * a.Hq + g * HPK + j) * D + d] = O / L;
+  }
+}
+
+// Count this block's arrival at each listed live slot (first_slot .. +nslots-1)
+// for KV head g; the block that completes a slot's set of partials merges it.
+template <class SH>
+__device__ void arrive_and_merge(const StepArgs& a, int g, int first_slot, int nslots, unsigned long long* flag) {
+  __threadfence();  // release this block's partials
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    bool last = false;
+    if (lane < nslots) {
+      const int s = first_slot + lane;
+      const int len = a.slot[s].len;
+      if (len > 0) {
+        const int old = atomicAdd(&a.counters[s * a.Hkv + g], 1);
+        last = (old == a.slot[s].n_expect - 1);
+      }
+    }
+    const unsigned long long mk = __ballot(last);
+    if (lane == 0) *flag = mk;
+  }
+  __syncthreads();
+  unsigned long long mk = *flag;
+  if (mk) {
+    __threadfence();  // acquire the other blocks' partials
+    while (mk) {
+      const int b = __ffsll((long long)mk) - 1;
+      mk &= mk - 1;
+      const int s = first_slot + b;
+      merge_slot<SH>(a, s, g);
+      if (threadIdx.x == 0) a.counters[s * a.Hkv + g] = 0;
+    }
+  }
+}
+
+template <class SH>
+__global__ __launch_bounds__(kBlockThreads) void decode_kernel(const StepArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[SH::SMEM];
+  __shared__ unsigned long long flag;
+  const int item = blockIdx.x / a.Hkv;
+  const int g = blockIdx.x - item * a.Hkv;
+  if (item < a.n_prefix_items) {
+    int p = 0;
+    while (p < a.num_prompts - 1 && !(a.prompt[p].nchunks > 0 && item < a.prompt[p].item_begin + a.prompt[p].nchunks))
+      ++p;
+    const int c = item - a.prompt[p].item_begin;
+    if constexpr (SH::MFMA)
+      prefix_mfma<SH>(a, p, c, g, smem);
+    else
+      prefix_wave<SH>(a, p, c, g, smem);
+    arrive_and_merge<SH>(a, g, p * a.m, a.m, &flag);
+    return;
+  }
+  const int it = item - a.n_prefix_items;
+  if (it < a.n_suffix_items) {
+    const int lane = threadIdx.x & 63;
+    bool hit = false;
+    if (lane < a.S) {
+      const int len = a.slot[lane].len, b = a.slot[lane].item_begin;
+      hit = len > 0 && it >= b && it < b + (len + a.split - 1) / a.split;
+    }
+    const int s = __ffsll((long long)__ballot(hit)) - 1;
+    if (s < 0) return;  // unreachable with a consistent plan
+    const int c = it - a.slot[s].item_begin;
+    suffix_chunk<SH>(a, s, c, g, smem);
+    arrive_and_merge<SH>(a, g, s, 1, &flag);
+    return;
+  }
+  const int z = it - a.n_suffix_items;
+  const int s = a.zero_slot[z];
+  float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
+  for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = 0.f;
+}
+
+// ----------------------------------------------------------------------------
+// Prefill: [plen, Hkv, D] -> prefix store.  One thread per 16-byte unit.
+// ----------------------------------------------------------------------------
+template <class SH>
+__global__ __launch_bounds__(256) void prefill_plain_kernel(char* store, const char* k, const char* v, int prompt,
+                                                           int plen, int hkv, int pmax) {
+  const int64_t units = (int64_t)hkv * 2 * plen * SH::LPT;
+  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < units; u += (int64_t)gridDim.x * blockDim.x) {
+    const int ch = u % SH::LPT;
+    const int64_t r = u / SH::LPT;
+    const int j = r % plen;
+    const int kind = (r / plen) % 2;
+    const int g = r / (2 * plen);
+    const u32x4* src = (const u32x4*)((kind ? v : k) + ((int64_t)j * hkv + g) * SH::ROWB) + ch;
+    char* dst = store + (((int64_t)prompt * hkv + g) * 2 + kind) * pmax * SH::ROWB + (int64_t)j * SH::ROWB;
+    *((u32x4*)dst + ch) = *src;
+  }
+}
+
+// MFMA layout per (prompt, kv head), per 32-token block: a K block of
+// [2 token halves][KB][64 lanes][8] and a V block of [DB][64 lanes][8].
+// K unit (mb, kb, lane): tokens mb*16 + lane%16, dims kb*32 + 8*(lane/16) + e.
+// V unit (db, lane): dim db*16 + lane%16, tokens tau(8*(lane/16) + e) where
+// tau(8q+e) = 4q+e for e < 4 and 16+4q+(e-4) otherwise -- the order in which
+// a lane holds probabilities after the S^T tiles.  Padding tokens are zero.
+template <class SH>
+__global__ __launch_bounds__(256) void prefill_mfma_kernel(uint16_t* store, const uint16_t* k, const uint16_t* v,
+                                                          int prompt, int plen, int hkv, int pmax) {
+  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB;
+  constexpr int KU = 2 * KB * 64, VU = DB * 64, BU = KU + VU;
+  const int nblk = (plen + kMfmaBlock - 1) / kMfmaBlock;
+  const int64_t units = (int64_t)hkv * nblk * BU;
+  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < units; u += (int64_t)gridDim.x * blockDim.x) {
+    const int g = u / ((int64_t)nblk * BU);
+    const int rem = u - (int64_t)g * nblk * BU;
+    const int b = rem / BU;
+    int x = rem - b * BU;
+    uint16_t* blk = store + (((int64_t)prompt * hkv + g) * (pmax / kMfmaBlock) + b) * (2 * kMfmaBlock * D);
+    uint16_t vals[8];
+    if (x < KU) {
+      const int lane = x & 63, sub = x >> 6, mb = sub / KB, kb = sub - mb * KB;
+      const int tok = b * kMfmaBlock + mb * 16 + (lane & 15);
+      const int d0 = kb * 32 + (lane >> 4) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vals[e] = tok < plen ? k[((int64_t)tok * hkv + g) * D + d0 + e] : 0;
+      uint16_t* dst = blk + (int64_t)x * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dst[e] = vals[e];
+    } else {
+      x -= KU;
+      const int lane = x & 63, db = x >> 6, qq = lane >> 4;
+      const int d = db * 16 + (lane & 15);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int tok = b * kMfmaBlock + (e < 4 ? 4 * qq + e : 16 + 4 * qq + (e - 4));
+        vals[e] = tok < plen ? v[((int64_t)tok * hkv + g) * D + d] : 0;
+      }
+      uint16_t* dst = blk + kMfmaBlock * D + (int64_t)x * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) dst[e] = vals[e];
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Instantiation table.
+// ----------------------------------------------------------------------------
+struct Entry {
+  KernelKey key;
+  void (*decode)(const StepArgs);
+  int smem_floats;
+};
+
+#define INFS_KERNELS(X)      \
+  X(false, 64, 1, false, 8)  \
+  X(false, 64, 2, false, 8)  \
+  X(false, 64, 2, false, 16) \
+  X(false, 64, 4, false, 16) \
+  X(false, 128, 1, false, 8) \
+  X(false, 128, 2, false, 8) \
+  X(false, 128, 2, false, 16) \
+  X(false, 128, 4, false, 16) \
+  X(true, 64, 2, false, 8)   \
+  X(true, 64, 2, true, 16)   \
+  X(true, 64, 2, true, 32)   \
+  X(true, 128, 1, false, 8)  \
+  X(true, 128, 1, true, 16)  \
+  X(true, 128, 2, false, 8)  \
+  X(true, 128, 2, false, 16) \
+  X(true, 128, 2, true, 16)  \
+  X(true, 128, 2, true, 32)  \
+  X(true, 128, 2, true, 64)  \
+  X(true, 128, 4, false, 16) \
+  X(true, 128, 4, true, 16)  \
+  X(true, 128, 4, true, 32)  \
+  X(true, 128, 4, true, 64)  \
+  X(true, 128, 8, true, 64)
+
+#define INFS_ENTRY(bf, d, hpk, mf, pr) \
+  {{bf, d, hpk, mf, pr}, decode_kernel<Shape<bf, d, hpk, mf, pr>>, Shape<bf, d, hpk, mf, pr>::SMEM},
+
+const Entry kTable[] = {INFS_KERNELS(INFS_ENTRY)};
+
+const Entry* find_entry(const KernelKey& k) {
+  for (const Entry& e : kTable)
+    if (e.key.bf16 == k.bf16 && e.key.head_dim == k.head_dim && e.key.hpk == k.hpk && e.key.mfma == k.mfma &&
+        e.key.prefix_rows == k.prefix_rows)
+      return &e;
+  return nullptr;
+}
+
+}  // namespace
+
+bool select_kernel(int bf16, int head_dim, int hpk, int rows, KernelKey* key) {
+  KernelKey k{bf16, head_dim, hpk, 0, 0};
+  if (bf16 && rows >= 16) {
+    k.mfma = 1;
+    k.prefix_rows = rows <= 16 ? 16 : rows <= 32 ? 32 : rows <= 64 ? 64 : 0;
+  } else {
+    k.prefix_rows = rows <= 8 ? 8 : rows <= 16 ? 16 : 0;
+  }
+  if (k.prefix_rows == 0 || !find_entry(k)) return false;
+  *key = k;
+  return true;
+}
+
+int64_t workspace_records(const KernelKey& key, int num_prompts, int hkv, int prefix_chunks_max, int num_slots,
+                          int suffix_chunks_max) {
+  return (int64_t)num_prompts * prefix_chunks_max * hkv * key.prefix_rows +
+         (int64_t)num_slots * suffix_chunks_max * hkv * key.hpk;
+}
+
+int64_t prefix_elems_per_head(const KernelKey& key, int pmax_padded) {
+  return (int64_t)2 * pmax_padded * key.head_dim;
+}
+
+hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream) {
+  const Entry* e = find_entry(key);
+  if (!e) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(e->decode, dim3(grid), dim3(kBlockThreads), 0, stream, args);
+  return hipGetLastError();
+}
+
+#define INFS_PREFILL_CASE(bf, d, mf)                                                                    \
+  if (key.bf16 == bf && key.head_dim == d && key.mfma == mf) {                                         \
+    using SH = Shape<bf, d, 1, mf, mf ? 16 : 8>;                                                       \
+    if constexpr (mf)                                                                                  \
+      hipLaunchKernelGGL(prefill_mfma_kernel<SH>, dim3(grid), dim3(256), 0, stream, (uint16_t*)store,  \
+                         (const uint16_t*)k, (const uint16_t*)v, prompt, plen, hkv, pmax);             \
+    else                                                                                               \
+      hipLaunchKernelGGL(prefill_plain_kernel<SH>, dim3(grid), dim3(256), 0, stream, (char*)store,     \
+                         (const char*)k, (const char*)v, prompt, plen, hkv, pmax);                     \
+    return hipGetLastError();                                                                          \
+  }
+
+hipError_t launch_prefill(const KernelKey& key, void* store, const void* k, const void* v, int prompt, int plen,
+                          int hkv, int pmax, hipStream_t stream) {
+  if (plen == 0) return hipSuccess;
+  const int64_t units = (int64_t)hkv * 2 * ((plen + 31) / 32) * 32 * key.head_dim;
+  const int grid = (int)((units / 8 + 255) / 256 < 4096 ? (units / 8 + 255) / 256 : 4096);
+  INFS_PREFILL_CASE(false, 64, 0)
+  INFS_PREFILL_CASE(false, 128, 0)
+  INFS_PREFILL_CASE(true, 64, 0)
+  INFS_PREFILL_CASE(true, 128, 0)
+  INFS_PREFILL_CASE(true, 64, 1)
+  INFS_PREFILL_CASE(true, 128, 1)
+  return hipErrorInvalidValue;
+}
+
+}  // namespace infs

@@ -1,0 +1,547 @@
+// Host runtime of the C ABI: context, validation, slot table, response page
+// allocator, per-step split-K plan, kernel launches, statistics and timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <functional>
+#include <new>
+#include <queue>
+#include <string>
+#include <vector>
+
+#include "infs.h"
+#include "kernels.h"
+#include "plan.h"
+
+using infs::KernelKey;
+using infs::StepArgs;
+
+static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must fit 4 KiB");
+
+namespace {
+thread_local std::string g_thread_error = "no error";
+
+struct Timing {
+  bool on = false;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<bool> pending;
+  size_t next = 0;
+  double ms = 0.0;
+  int64_t launches = 0;
+};
+}  // namespace
+
+struct infs_ctx {
+  infs_config cfg{};
+  bool dry = false;
+  hipStream_t stream = nullptr;
+  KernelKey key{};
+  int S = 0, m = 0, G = 0, hpk = 0, D = 0, Hkv = 0, Hq = 0, L = 0, NP = 0;
+  int pmax_pad = 0, split = 0, pages_per_slot = 0, num_pages = 0, pcmax = 0, scmax = 0;
+  size_t es = 0;
+  size_t prefix_layer_bytes = 0, pool_layer_bytes = 0;
+  int64_t ws_records = 0;
+  // device memory
+  char* prefix = nullptr;
+  char* pool = nullptr;
+  int32_t* page_table = nullptr;
+  float* ws_o = nullptr;
+  float* ws_ml = nullptr;
+  int32_t* counters = nullptr;
+  int32_t* tokens = nullptr;
+  // host state
+  std::vector<int32_t> plen;                       // per prompt, -1 before its first prefill
+  std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
+  std::vector<int64_t> slot_sample;                // -1: empty
+  std::vector<int32_t> slot_len;
+  std::vector<std::vector<int32_t>> slot_pages;    // host copy of each slot's page list
+  std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_pages;
+  std::vector<std::vector<uint8_t>> dispatched;    // [prompt][G]
+  bool step_open = false;
+  std::vector<uint8_t> layer_done;
+  int layers_done = 0;
+  StepArgs plan{};
+  int grid = 0;
+  double step_bytes = 0, step_flops = 0;
+  infs_stats stats{};
+  bool dead = false;
+  std::string err = "no error";
+  Timing timing;
+};
+
+namespace {
+
+infs_status fail(infs_ctx* c, infs_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (c)
+    c->err = buf;
+  else
+    g_thread_error = buf;
+  return st;
+}
+
+infs_status device_fail(infs_ctx* c, hipError_t e, const char* what) {
+  if (c) c->dead = true;
+  return fail(c, e == hipErrorOutOfMemory ? INFS_E_NOMEM : INFS_E_DEVICE, "%s failed: %s", what,
+              hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, expr)                                  \
+  do {                                                      \
+    hipError_t e_ = (expr);                                 \
+    if (e_ != hipSuccess) return device_fail(ctx, e_, #expr); \
+  } while (0)
+
+#define CHECK_CTX(c)                                                                  \
+  do {                                                                                \
+    if (!(c)) return fail(nullptr, INFS_E_ARG, "null context");                      \
+    if ((c)->dead) return fail(c, INFS_E_DEVICE, "context unusable after a device error: %s", (c)->err.c_str()); \
+  } while (0)
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+void free_device(infs_ctx* c) {
+  if (c->dry) return;
+  hipFree(c->prefix);
+  hipFree(c->pool);
+  hipFree(c->page_table);
+  hipFree(c->ws_o);
+  hipFree(c->ws_ml);
+  hipFree(c->counters);
+  hipFree(c->tokens);
+}
+
+void reset_host(infs_ctx* c) {
+  c->plen.assign(c->NP, -1);
+  c->prefilled.assign(c->NP, std::vector<uint8_t>(c->L, 0));
+  c->slot_sample.assign(c->S, -1);
+  c->slot_len.assign(c->S, 0);
+  c->slot_pages.assign(c->S, {});
+  c->free_pages = {};
+  for (int i = 0; i < c->num_pages; ++i) c->free_pages.push(i);
+  c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
+  c->step_open = false;
+  c->layer_done.assign(c->L, 0);
+  c->layers_done = 0;
+  c->stats = infs_stats{};
+}
+
+// Build the plan of the step that is about to open: lengths after the append,
+// pages, chunk items.  Validates before changing anything.
+infs_status open_step(infs_ctx* c) {
+  int need_pages = 0;
+  for (int s = 0; s < c->S; ++s) {
+    if (c->slot_sample[s] < 0) continue;
+    if (c->slot_len[s] + 1 > c->cfg.max_suffix_len)
+      return fail(c, INFS_E_CAPACITY, "slot %d: response would exceed max_suffix_len=%d", s, c->cfg.max_suffix_len);
+    if (c->slot_len[s] % infs::kPageTokens == 0) ++need_pages;
+  }
+  if ((size_t)need_pages > c->free_pages.size())
+    return fail(c, INFS_E_CAPACITY, "page pool exhausted: need %d pages, %zu free", need_pages, c->free_pages.size());
+
+  StepArgs& a = c->plan;
+  int items = 0;
+  std::vector<int> live(c->NP, 0);
+  for (int s = 0; s < c->S; ++s)
+    if (c->slot_sample[s] >= 0) ++live[s / c->m];
+  for (int p = 0; p < c->NP; ++p) {
+    if (live[p] > 0 && c->plen[p] < 0)
+      return fail(c, INFS_E_STATE, "prompt %d has live slots but no prefilled prefix", p);
+  }
+  double bytes = 0, flops = 0;
+  const double kvrow = (double)c->Hkv * c->D * c->es;
+  for (int p = 0; p < c->NP; ++p) {
+    infs::PromptPlan& pp = a.prompt[p];
+    pp.plen = std::max(c->plen[p], 0);
+    pp.nchunks = live[p] > 0 ? ceil_div(pp.plen, c->split) : 0;
+    pp.item_begin = items;
+    items += pp.nchunks;
+    if (live[p] > 0) bytes += 2.0 * pp.plen * kvrow;
+  }
+  a.n_prefix_items = items;
+  items = 0;
+  int zeros = 0;
+  for (int s = 0; s < c->S; ++s) {
+    infs::SlotPlan& sp = a.slot[s];
+    sp = infs::SlotPlan{};
+    if (c->slot_sample[s] < 0) {
+      sp.item_begin = items;
+      a.zero_slot[zeros++] = (int8_t)s;
+      continue;
+    }
+    const int len = c->slot_len[s] + 1;
+    const int pos = len - 1;
+    if (pos % infs::kPageTokens == 0) {
+      c->slot_pages[s].push_back(c->free_pages.top());
+      c->free_pages.pop();
+    }
+    sp.len = len;
+    sp.item_begin = items;
+    sp.cur_page = c->slot_pages[s][pos / infs::kPageTokens];
+    sp.sample = (int32_t)c->slot_sample[s];
+    const int nch = ceil_div(len, c->split);
+    sp.n_expect = a.prompt[s / c->m].nchunks + nch;
+    items += nch;
+    const int P = a.prompt[s / c->m].plen;
+    bytes += 2.0 * len * kvrow + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
+    flops += 4.0 * c->Hq * c->D * (double)(P + len);
+  }
+  a.n_suffix_items = items;
+  a.n_zero_items = zeros;
+  c->grid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items) * c->Hkv;
+  c->step_bytes = bytes;
+  c->step_flops = flops;
+  c->step_open = true;
+  std::fill(c->layer_done.begin(), c->layer_done.end(), 0);
+  c->layers_done = 0;
+  return INFS_OK;
+}
+
+infs_status timed_launch(infs_ctx* c) {
+  Timing& t = c->timing;
+  size_t slot = 0;
+  if (t.on) {
+    slot = t.next;
+    t.next = (t.next + 1) % t.start.size();
+    if (t.pending[slot]) {
+      HIP_TRY(c, hipEventSynchronize(t.stop[slot]));
+      float ms = 0.f;
+      HIP_TRY(c, hipEventElapsedTime(&ms, t.start[slot], t.stop[slot]));
+      t.ms += ms;
+      ++t.launches;
+      t.pending[slot] = false;
+    }
+    HIP_TRY(c, hipEventRecord(t.start[slot], c->stream));
+  }
+  HIP_TRY(c, infs::launch_decode(c->key, c->plan, c->grid, c->stream));
+  if (t.on) {
+    HIP_TRY(c, hipEventRecord(t.stop[slot], c->stream));
+    t.pending[slot] = true;
+  }
+  return INFS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t infs_abi_version(void) { return INFS_ABI_VERSION; }
+
+const char* infs_last_error(const infs_ctx* ctx) { return ctx ? ctx->err.c_str() : g_thread_error.c_str(); }
+
+infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out) {
+  if (!out) return fail(nullptr, INFS_E_ARG, "out is null");
+  *out = nullptr;
+  if (!cfg) return fail(nullptr, INFS_E_ARG, "cfg is null");
+  const infs_config& k = *cfg;
+  if (k.num_layers < 1 || k.num_layers > 4096) return fail(nullptr, INFS_E_ARG, "num_layers must be in [1, 4096]");
+  if (k.num_kv_heads < 1 || k.num_q_heads < 1 || k.num_q_heads % k.num_kv_heads)
+    return fail(nullptr, INFS_E_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (k.head_dim != 64 && k.head_dim != 128) return fail(nullptr, INFS_E_ARG, "head_dim must be 64 or 128");
+  if (k.num_prompts < 1 || k.num_prompts > infs::kMaxPrompts)
+    return fail(nullptr, INFS_E_ARG, "num_prompts must be in [1, %d]", infs::kMaxPrompts);
+  if (k.slots_per_prompt < 1 || (int64_t)k.num_prompts * k.slots_per_prompt > infs::kMaxSlots)
+    return fail(nullptr, INFS_E_ARG, "num_prompts * slots_per_prompt must be in [1, %d]", infs::kMaxSlots);
+  if (k.samples_per_prompt < 1 || k.samples_per_prompt > (1 << 24))
+    return fail(nullptr, INFS_E_ARG, "samples_per_prompt must be in [1, 2^24]");
+  if (k.max_prompt_len < 0 || k.max_prompt_len > (1 << 20))
+    return fail(nullptr, INFS_E_ARG, "max_prompt_len must be in [0, 2^20]");
+  if (k.max_suffix_len < 1 || k.max_suffix_len > (1 << 20))
+    return fail(nullptr, INFS_E_ARG, "max_suffix_len must be in [1, 2^20]");
+  if (k.page_tokens != 0 && k.page_tokens != infs::kPageTokens)
+    return fail(nullptr, INFS_E_ARG, "page_tokens must be 0 or %d", infs::kPageTokens);
+  if (k.split_tokens < 0 || k.split_tokens % 128 || k.split_tokens > (1 << 16))
+    return fail(nullptr, INFS_E_ARG, "split_tokens must be 0 or a multiple of 128 up to 65536");
+  if (k.num_pages < 0) return fail(nullptr, INFS_E_ARG, "num_pages must be >= 0");
+  if (k.dtype != INFS_F32 && k.dtype != INFS_BF16) return fail(nullptr, INFS_E_ARG, "dtype must be INFS_F32 or INFS_BF16");
+  if (!(k.scale >= 0.f) || !std::isfinite(k.scale)) return fail(nullptr, INFS_E_ARG, "scale must be finite and >= 0");
+  if (k.flags & ~INFS_FLAG_DRY_RUN) return fail(nullptr, INFS_E_ARG, "unknown flags");
+
+  const int hpk = k.num_q_heads / k.num_kv_heads;
+  KernelKey key{};
+  if (!infs::select_kernel(k.dtype == INFS_BF16, k.head_dim, hpk, k.slots_per_prompt * hpk, &key))
+    return fail(nullptr, INFS_E_ARG,
+                "no kernel for dtype=%s head_dim=%d heads_per_kv=%d prefix rows=%d (bf16 supports up to 64 rows, "
+                "fp32 up to 16)",
+                k.dtype == INFS_BF16 ? "bf16" : "f32", k.head_dim, hpk, k.slots_per_prompt * hpk);
+
+  infs_ctx* c = new (std::nothrow) infs_ctx;
+  if (!c) return fail(nullptr, INFS_E_NOMEM, "host allocation failed");
+  c->cfg = k;
+  c->dry = (k.flags & INFS_FLAG_DRY_RUN) != 0;
+  c->stream = (hipStream_t)hip_stream;
+  c->key = key;
+  c->NP = k.num_prompts;
+  c->m = k.slots_per_prompt;
+  c->S = c->NP * c->m;
+  c->G = k.samples_per_prompt;
+  c->hpk = hpk;
+  c->D = k.head_dim;
+  c->Hkv = k.num_kv_heads;
+  c->Hq = k.num_q_heads;
+  c->L = k.num_layers;
+  c->es = k.dtype == INFS_BF16 ? 2 : 4;
+  c->split = k.split_tokens ? k.split_tokens : 256;
+  c->pmax_pad = std::max(32, (k.max_prompt_len + 31) / 32 * 32);
+  c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);
+  c->num_pages = k.num_pages ? k.num_pages : c->S * c->pages_per_slot;
+  c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->split));
+  c->scmax = ceil_div(k.max_suffix_len, c->split);
+  c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->es;
+  c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->es;
+  c->ws_records = infs::workspace_records(key, c->NP, c->Hkv, c->pcmax, c->S, c->scmax);
+  reset_host(c);
+
+  StepArgs& a = c->plan;
+  a.S = c->S;
+  a.m = c->m;
+  a.G = c->G;
+  a.Hq = c->Hq;
+  a.Hkv = c->Hkv;
+  a.prefix_rows = c->m * hpk;
+  a.max_prompt_len = c->pmax_pad;
+  a.pages_per_slot = c->pages_per_slot;
+  a.split = c->split;
+  a.prefix_chunks_max = c->pcmax;
+  a.suffix_chunks_max = c->scmax;
+  a.num_prompts = c->NP;
+  const float scale = k.scale > 0.f ? k.scale : 1.0f / std::sqrt((float)k.head_dim);
+  a.scale_log2 = scale * 1.4426950408889634f;
+
+  if (!c->dry) {
+    auto alloc = [&](void** p, size_t bytes, const char* what) -> infs_status {
+      hipError_t e = hipMalloc(p, std::max<size_t>(bytes, 256));
+      if (e != hipSuccess) {
+        return fail(nullptr, e == hipErrorOutOfMemory ? INFS_E_NOMEM : INFS_E_DEVICE, "hipMalloc(%s, %zu bytes): %s",
+                    what, bytes, hipGetErrorString(e));
+      }
+      e = hipMemset(*p, 0, std::max<size_t>(bytes, 256));
+      if (e != hipSuccess) return fail(nullptr, INFS_E_DEVICE, "hipMemset(%s): %s", what, hipGetErrorString(e));
+      return INFS_OK;
+    };
+    infs_status st = INFS_OK;
+    if (st == INFS_OK) st = alloc((void**)&c->prefix, c->prefix_layer_bytes * c->L, "prefix store");
+    if (st == INFS_OK) st = alloc((void**)&c->pool, c->pool_layer_bytes * c->L, "page pool");
+    if (st == INFS_OK) st = alloc((void**)&c->page_table, sizeof(int32_t) * c->S * c->pages_per_slot, "page table");
+    if (st == INFS_OK) st = alloc((void**)&c->ws_o, sizeof(float) * c->ws_records * c->D, "workspace");
+    if (st == INFS_OK) st = alloc((void**)&c->ws_ml, sizeof(float) * c->ws_records * 2, "workspace");
+    if (st == INFS_OK) st = alloc((void**)&c->counters, sizeof(int32_t) * c->S * c->Hkv, "counters");
+    if (st == INFS_OK) st = alloc((void**)&c->tokens, sizeof(int32_t) * c->NP * c->G, "token counters");
+    if (st != INFS_OK) {
+      free_device(c);
+      delete c;
+      return st;
+    }
+    a.page_table = c->page_table;
+    a.ws_o = c->ws_o;
+    a.ws_ml = c->ws_ml;
+    a.counters = c->counters;
+    a.tokens = c->tokens;
+  }
+  *out = c;
+  return INFS_OK;
+}
+
+void infs_destroy(infs_ctx* c) {
+  if (!c) return;
+  if (!c->dry) {
+    hipStreamSynchronize(c->stream);
+    for (auto e : c->timing.start) hipEventDestroy(e);
+    for (auto e : c->timing.stop) hipEventDestroy(e);
+    free_device(c);
+  }
+  delete c;
+}
+
+infs_status infs_reset(infs_ctx* c) {
+  CHECK_CTX(c);
+  reset_host(c);
+  if (!c->dry) {
+    HIP_TRY(c, hipMemsetAsync(c->tokens, 0, sizeof(int32_t) * c->NP * c->G, c->stream));
+    HIP_TRY(c, hipMemsetAsync(c->counters, 0, sizeof(int32_t) * c->S * c->Hkv, c->stream));
+  }
+  return INFS_OK;
+}
+
+infs_status infs_prefill_shared(infs_ctx* c, int32_t prompt, int32_t layer, int32_t prompt_len, const void* k_dev,
+                                const void* v_dev) {
+  CHECK_CTX(c);
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range [0, %d)", prompt, c->NP);
+  if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (prompt_len < 0 || prompt_len > c->cfg.max_prompt_len)
+    return fail(c, INFS_E_ARG, "prompt_len %d out of range [0, %d]", prompt_len, c->cfg.max_prompt_len);
+  if (c->plen[prompt] >= 0 && c->plen[prompt] != prompt_len)
+    return fail(c, INFS_E_ARG, "prompt %d was prefilled with %d tokens in another layer", prompt, c->plen[prompt]);
+  if (c->step_open) return fail(c, INFS_E_STATE, "prefill while a step is open");
+  if (!c->dry && prompt_len > 0 && (!k_dev || !v_dev)) return fail(c, INFS_E_ARG, "null K/V pointer");
+  if (!c->dry) {
+    HIP_TRY(c, infs::launch_prefill(c->key, c->prefix + c->prefix_layer_bytes * layer, k_dev, v_dev, prompt,
+                                    prompt_len, c->Hkv, c->pmax_pad, c->stream));
+  }
+  c->plen[prompt] = prompt_len;
+  c->prefilled[prompt][layer] = 1;
+  return INFS_OK;
+}
+
+infs_status infs_refill_slot(infs_ctx* c, int32_t slot, int32_t prompt, int64_t sample_id) {
+  CHECK_CTX(c);
+  if (slot < 0 || slot >= c->S) return fail(c, INFS_E_ARG, "slot %d out of range [0, %d)", slot, c->S);
+  if (prompt != slot / c->m) return fail(c, INFS_E_ARG, "slot %d serves prompt %d, not %d", slot, slot / c->m, prompt);
+  if (sample_id < 0 || sample_id >= c->G)
+    return fail(c, INFS_E_ARG, "sample_id %lld out of range [0, %d)", (long long)sample_id, c->G);
+  if (c->step_open) return fail(c, INFS_E_STATE, "refill while a step is open");
+  if (c->slot_sample[slot] >= 0) return fail(c, INFS_E_STATE, "slot %d is live", slot);
+  if (c->dispatched[prompt][sample_id])
+    return fail(c, INFS_E_DUP, "sample %lld of prompt %d was already dispatched", (long long)sample_id, prompt);
+  c->dispatched[prompt][sample_id] = 1;
+  c->slot_sample[slot] = sample_id;
+  c->slot_len[slot] = 0;
+  c->slot_pages[slot].clear();
+  return INFS_OK;
+}
+
+infs_status infs_retire_slot(infs_ctx* c, int32_t slot) {
+  CHECK_CTX(c);
+  if (slot < 0 || slot >= c->S) return fail(c, INFS_E_ARG, "slot %d out of range [0, %d)", slot, c->S);
+  if (c->step_open) return fail(c, INFS_E_STATE, "retire while a step is open");
+  if (c->slot_sample[slot] < 0) return fail(c, INFS_E_STATE, "slot %d is empty", slot);
+  for (int32_t pg : c->slot_pages[slot]) c->free_pages.push(pg);
+  c->slot_pages[slot].clear();
+  c->slot_sample[slot] = -1;
+  c->slot_len[slot] = 0;
+  return INFS_OK;
+}
+
+infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev,
+                             const void* v_new_dev, float* o_dev) {
+  CHECK_CTX(c);
+  if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
+  if (c->step_open && c->layer_done[layer])
+    return fail(c, INFS_E_STATE, "layer %d already decoded in this step", layer);
+  for (int p = 0; p < c->NP; ++p) {
+    bool live = false;
+    for (int s = p * c->m; s < (p + 1) * c->m; ++s) live |= c->slot_sample[s] >= 0;
+    if (live && !c->prefilled[p][layer])
+      return fail(c, INFS_E_STATE, "prompt %d has live slots but layer %d is not prefilled", p, layer);
+  }
+  if (!c->step_open) {
+    infs_status st = open_step(c);
+    if (st != INFS_OK) return st;
+  }
+  if (!c->dry) {
+    StepArgs& a = c->plan;
+    a.q = q_dev;
+    a.knew = k_new_dev;
+    a.vnew = v_new_dev;
+    a.o = o_dev;
+    a.prefix = c->prefix + c->prefix_layer_bytes * layer;
+    a.pool = c->pool + c->pool_layer_bytes * layer;
+    a.count_tokens = layer == 0;
+    infs_status st = timed_launch(c);
+    if (st != INFS_OK) return st;
+  }
+  c->layer_done[layer] = 1;
+  ++c->layers_done;
+  ++c->stats.launches;
+  c->stats.alg_bytes += c->step_bytes;
+  c->stats.alg_flops += c->step_flops;
+  return INFS_OK;
+}
+
+infs_status infs_end_step(infs_ctx* c) {
+  CHECK_CTX(c);
+  if (!c->step_open || c->layers_done != c->L)
+    return fail(c, INFS_E_STATE, "end_step needs every layer decoded once (%d of %d)", c->step_open ? c->layers_done : 0,
+                c->L);
+  for (int s = 0; s < c->S; ++s)
+    if (c->slot_sample[s] >= 0) {
+      ++c->slot_len[s];
+      ++c->stats.tokens;
+    }
+  c->step_open = false;
+  ++c->stats.steps;
+  return INFS_OK;
+}
+
+infs_status infs_slot_state(const infs_ctx* c, int32_t slot, int64_t* sample_id, int32_t* len) {
+  if (!c) return fail(nullptr, INFS_E_ARG, "null context");
+  if (slot < 0 || slot >= c->S) return fail(const_cast<infs_ctx*>(c), INFS_E_ARG, "slot %d out of range", slot);
+  if (!sample_id || !len) return fail(const_cast<infs_ctx*>(c), INFS_E_ARG, "null output pointer");
+  *sample_id = c->slot_sample[slot];
+  *len = c->slot_len[slot];
+  return INFS_OK;
+}
+
+infs_status infs_sample_tokens(infs_ctx* c, int32_t prompt, int32_t* counts_host, int32_t n) {
+  CHECK_CTX(c);
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range", prompt);
+  if (!counts_host || n != c->G) return fail(c, INFS_E_ARG, "counts must hold samples_per_prompt=%d entries", c->G);
+  if (c->dry) return fail(c, INFS_E_STATE, "no device counters in a dry-run context");
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(counts_host, c->tokens + (size_t)prompt * c->G, sizeof(int32_t) * c->G, hipMemcpyDeviceToHost));
+  return INFS_OK;
+}
+
+infs_status infs_sync(infs_ctx* c) {
+  CHECK_CTX(c);
+  if (!c->dry) HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return INFS_OK;
+}
+
+infs_status infs_get_stats(const infs_ctx* c, infs_stats* out) {
+  if (!c || !out) return fail(nullptr, INFS_E_ARG, "null argument");
+  *out = c->stats;
+  return INFS_OK;
+}
+
+infs_status infs_timing_begin(infs_ctx* c) {
+  CHECK_CTX(c);
+  if (c->dry) return fail(c, INFS_E_STATE, "no timing in a dry-run context");
+  Timing& t = c->timing;
+  if (t.start.empty()) {
+    const size_t n = 1024;
+    t.start.resize(n);
+    t.stop.resize(n);
+    for (size_t i = 0; i < n; ++i) {
+      HIP_TRY(c, hipEventCreate(&t.start[i]));
+      HIP_TRY(c, hipEventCreate(&t.stop[i]));
+    }
+  }
+  t.pending.assign(t.start.size(), false);
+  t.next = 0;
+  t.ms = 0.0;
+  t.launches = 0;
+  t.on = true;
+  return INFS_OK;
+}
+
+infs_status infs_timing_end(infs_ctx* c, double* kernel_ms, int64_t* launches) {
+  CHECK_CTX(c);
+  Timing& t = c->timing;
+  if (!t.on) return fail(c, INFS_E_STATE, "timing not started");
+  if (!kernel_ms || !launches) return fail(c, INFS_E_ARG, "null output pointer");
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (size_t i = 0; i < t.start.size(); ++i) {
+    if (!t.pending[i]) continue;
+    float ms = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&ms, t.start[i], t.stop[i]));
+    t.ms += ms;
+    ++t.launches;
+    t.pending[i] = false;
+  }
+  t.on = false;
+  *kernel_ms = t.ms;
+  *launches = t.launches;
+  return INFS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,103 @@
+"""Group decode through the C ABI: the runtime loop of Algorithm 1, phase 2.
+
+Every running step decodes one token for each live slot through every layer
+(``decode_step`` per layer, then ``end_step``); a sample that has produced its
+last token releases its slot (``retire_slot``) and the refill policy of its
+prompt hands the slot a pending sample (``refill_slot``), which decodes from the
+next step on.  The host knows each sample's length (synthetic workloads), so it
+never waits on the GPU inside the loop.
+"""
+
+from typing import Callable, List, Optional, Sequence
+
+from . import infs
+
+
+def context_for(cfg, stream=None, dry_run=False, split_tokens=0, num_pages=0) -> infs.Context:
+    """Create a context for a workload preset (workload.GroupConfig or alike)."""
+    c = infs.make_config(
+        num_layers=cfg.layers, num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
+        head_dim=cfg.head_dim, num_prompts=cfg.num_prompts, slots_per_prompt=cfg.slots_per_prompt,
+        samples_per_prompt=cfg.samples_per_prompt, max_prompt_len=max(cfg.prompt_lens),
+        max_suffix_len=cfg.max_suffix_len, page_tokens=0, num_pages=num_pages,
+        split_tokens=split_tokens, dtype=infs.BF16 if cfg.dtype == "bf16" else infs.F32,
+        scale=0.0, flags=infs.FLAG_DRY_RUN if dry_run else 0)
+    return infs.Context(c, stream=None if dry_run else stream)
+
+
+def schedulers_for(cfg, policy: str, pred=None) -> List[infs.Sched]:
+    """One host scheduler per prompt."""
+    out = []
+    for p in range(cfg.num_prompts):
+        out.append(infs.Sched(cfg.samples_per_prompt, cfg.slots_per_prompt, policy,
+                              None if pred is None else pred[p]))
+    return out
+
+
+def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_layers: int,
+                 provide: Callable, after_step: Optional[Callable] = None,
+                 log: Optional[list] = None) -> int:
+    """Decode every sample of every prompt; returns the number of running steps.
+
+    lengths[p][i]: true length of sample i of prompt p.
+    provide(step, layer) -> (q, k_new, v_new, o) device buffers for that layer-step.
+    after_step(step) is called after each end_step.
+    log, if given, receives one tuple per step: for each slot (prompt, sample, t)
+    with t the response length after this step, or None for an idle slot.
+    """
+    NP = len(scheds)
+    m = ctx.config.slots_per_prompt
+    S = NP * m
+    slot_sample = [-1] * S
+    slot_len = [0] * S
+    Ls = [[int(x) for x in row] for row in lengths]
+
+    def fill():
+        for p in range(NP):
+            sch = scheds[p]
+            for ls in range(m):
+                s = p * m + ls
+                if slot_sample[s] < 0:
+                    i = sch.next(ls)
+                    if i >= 0:
+                        ctx.refill_slot(s, p, i)
+                        slot_sample[s] = i
+                        slot_len[s] = 0
+
+    fill()
+    step = 0
+    while any(x >= 0 for x in slot_sample):
+        if log is not None:
+            log.append(tuple((s // m, slot_sample[s], slot_len[s] + 1) if slot_sample[s] >= 0 else None
+                             for s in range(S)))
+        for layer in range(num_layers):
+            ctx.decode_step(layer, *provide(step, layer))
+        ctx.end_step()
+        if after_step is not None:
+            after_step(step)
+        step += 1
+        for s in range(S):
+            i = slot_sample[s]
+            if i < 0:
+                continue
+            slot_len[s] += 1
+            p = s // m
+            if slot_len[s] == Ls[p][i]:
+                ctx.retire_slot(s)
+                scheds[p].done(s - p * m)
+                slot_sample[s] = -1
+        fill()
+    return step
+
+
+def plan_steps(cfg, lengths, policy: str, pred=None) -> list:
+    """Step log of a group decode, from a dry-run context (bookkeeping only, no GPU)."""
+    ctx = context_for(cfg, dry_run=True)
+    for p in range(cfg.num_prompts):
+        for layer in range(cfg.layers):
+            ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
+    log = []
+    nothing = (None, None, None, None)
+    decode_group(ctx, schedulers_for(cfg, policy, pred), lengths, cfg.layers, lambda s, l: nothing, log=log)
+    ctx.destroy()
+    return log

@@ -1,0 +1,243 @@
+"""ctypes binding of libinfs.so -- argument marshalling only.
+
+Every call maps one-to-one onto the C function of the same name in
+``include/infs.h``; device buffers are passed as integers or as objects with a
+``data_ptr()`` method (e.g. torch tensors), streams as integers or objects with
+a ``cuda_stream`` attribute.  A non-OK status raises ``InfsError``.
+The library must have been built (``python -m paper_2506_22950_amd.build``);
+there is no fallback.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libinfs.so")
+
+OK, E_ARG, E_STATE, E_CAPACITY, E_DUP, E_NOMEM, E_DEVICE = 0, -1, -2, -3, -4, -5, -6
+STATUS_NAMES = {0: "OK", -1: "E_ARG", -2: "E_STATE", -3: "E_CAPACITY", -4: "E_DUP", -5: "E_NOMEM", -6: "E_DEVICE"}
+F32, BF16 = 0, 1
+NAIVE, FIXED_ROW, FIFO, SJF = 0, 1, 2, 3
+POLICY = {"naive": NAIVE, "fixed_row": FIXED_ROW, "fifo": FIFO, "sjf": SJF}
+FLAG_DRY_RUN = 1
+
+# Every symbol include/infs.h declares.
+EXPORTS = (
+    "infs_abi_version", "infs_create", "infs_destroy", "infs_reset", "infs_prefill_shared",
+    "infs_refill_slot", "infs_retire_slot", "infs_decode_step", "infs_end_step", "infs_slot_state",
+    "infs_sample_tokens", "infs_sync", "infs_get_stats", "infs_timing_begin", "infs_timing_end",
+    "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
+    "infs_sched_destroy",
+)
+
+
+class InfsError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [
+        ("num_layers", ctypes.c_int32), ("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32), ("num_prompts", ctypes.c_int32), ("slots_per_prompt", ctypes.c_int32),
+        ("samples_per_prompt", ctypes.c_int32), ("max_prompt_len", ctypes.c_int32),
+        ("max_suffix_len", ctypes.c_int32), ("page_tokens", ctypes.c_int32), ("num_pages", ctypes.c_int32),
+        ("split_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int64), ("launches", ctypes.c_int64), ("tokens", ctypes.c_int64),
+                ("alg_bytes", ctypes.c_double), ("alg_flops", ctypes.c_double)]
+
+
+_lib = None
+
+
+def load():
+    """Load libinfs.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2506_22950_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, F, U32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_uint32
+    sig = {
+        "infs_abi_version": (I32, []),
+        "infs_create": (I32, [ctypes.POINTER(Config), P, ctypes.POINTER(P)]),
+        "infs_destroy": (None, [P]),
+        "infs_reset": (I32, [P]),
+        "infs_prefill_shared": (I32, [P, I32, I32, I32, P, P]),
+        "infs_refill_slot": (I32, [P, I32, I32, I64]),
+        "infs_retire_slot": (I32, [P, I32]),
+        "infs_decode_step": (I32, [P, I32, P, P, P, P]),
+        "infs_end_step": (I32, [P]),
+        "infs_slot_state": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I32)]),
+        "infs_sample_tokens": (I32, [P, I32, ctypes.POINTER(I32), I32]),
+        "infs_sync": (I32, [P]),
+        "infs_get_stats": (I32, [P, ctypes.POINTER(Stats)]),
+        "infs_timing_begin": (I32, [P]),
+        "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
+        "infs_last_error": (ctypes.c_char_p, [P]),
+        "infs_sched_create": (I32, [I32, I32, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(P)]),
+        "infs_sched_next": (I32, [P, I32, ctypes.POINTER(I64)]),
+        "infs_sched_done": (I32, [P, I32]),
+        "infs_sched_pending": (I32, [P]),
+        "infs_sched_destroy": (None, [P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(s):
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return int(s.cuda_stream)
+
+
+def _check(ctx_handle, st):
+    if st != OK:
+        msg = load().infs_last_error(ctx_handle)
+        raise InfsError(st, msg.decode() if msg else "")
+
+
+def make_config(**kw) -> Config:
+    c = Config()
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+class Context:
+    """One infs_ctx.  Methods carry the names of the C calls without the prefix."""
+
+    def __init__(self, config: Config, stream=None):
+        lib = load()
+        h = ctypes.c_void_p()
+        _check(None, lib.infs_create(ctypes.byref(config), _stream(stream), ctypes.byref(h)))
+        self._h = h
+        self.config = config
+
+    def destroy(self):
+        if self._h:
+            load().infs_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    def _call(self, fn, *args):
+        _check(self._h, fn(self._h, *args))
+
+    def reset(self):
+        self._call(load().infs_reset)
+
+    def prefill_shared(self, prompt, layer, prompt_len, k, v):
+        self._call(load().infs_prefill_shared, prompt, layer, prompt_len, _ptr(k), _ptr(v))
+
+    def refill_slot(self, slot, prompt, sample_id):
+        self._call(load().infs_refill_slot, slot, prompt, sample_id)
+
+    def retire_slot(self, slot):
+        self._call(load().infs_retire_slot, slot)
+
+    def decode_step(self, layer, q, k_new, v_new, o):
+        self._call(load().infs_decode_step, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o))
+
+    def end_step(self):
+        self._call(load().infs_end_step)
+
+    def slot_state(self, slot):
+        sid, ln = ctypes.c_int64(), ctypes.c_int32()
+        self._call(load().infs_slot_state, slot, ctypes.byref(sid), ctypes.byref(ln))
+        return sid.value, ln.value
+
+    def sample_tokens(self, prompt):
+        n = self.config.samples_per_prompt
+        buf = (ctypes.c_int32 * n)()
+        self._call(load().infs_sample_tokens, prompt, buf, n)
+        return np.frombuffer(buf, dtype=np.int32).copy()
+
+    def sync(self):
+        self._call(load().infs_sync)
+
+    def get_stats(self) -> Stats:
+        s = Stats()
+        self._call(load().infs_get_stats, ctypes.byref(s))
+        return s
+
+    def timing_begin(self):
+        self._call(load().infs_timing_begin)
+
+    def timing_end(self):
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        self._call(load().infs_timing_end, ctypes.byref(ms), ctypes.byref(n))
+        return ms.value, n.value
+
+    @property
+    def last_error(self):
+        return load().infs_last_error(self._h).decode()
+
+
+class Sched:
+    """One infs_sched (host refill policy for one prompt's m slots)."""
+
+    def __init__(self, G, m, policy, pred_len=None):
+        lib = load()
+        if isinstance(policy, str):
+            policy = POLICY[policy]
+        h = ctypes.c_void_p()
+        arr = None
+        if pred_len is not None:
+            self._pred = np.ascontiguousarray(pred_len, dtype=np.float64)
+            arr = self._pred.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+        st = lib.infs_sched_create(G, m, policy, arr, ctypes.byref(h))
+        if st != OK:
+            raise InfsError(st, "infs_sched_create")
+        self._h = h
+
+    def next(self, slot):
+        out = ctypes.c_int64()
+        st = load().infs_sched_next(self._h, slot, ctypes.byref(out))
+        if st != OK:
+            raise InfsError(st, f"infs_sched_next(slot={slot})")
+        return out.value
+
+    def done(self, slot):
+        st = load().infs_sched_done(self._h, slot)
+        if st != OK:
+            raise InfsError(st, f"infs_sched_done(slot={slot})")
+
+    @property
+    def pending(self):
+        return load().infs_sched_pending(self._h)
+
+    def __del__(self):
+        try:
+            if self._h:
+                load().infs_sched_destroy(self._h)
+                self._h = None
+        except Exception:
+            pass

@@ -1,0 +1,138 @@
+"""Run a group decode on the GPU through the C ABI and compare with the oracle.
+
+Inputs are staged on the device in windows of steps, so workloads whose
+per-step inputs exceed device memory still run in the launch configuration the
+benchmark uses.  Outputs of selected steps are copied back for comparison.
+"""
+
+import sys
+import time
+
+import numpy as np
+
+from oracle import attend_slot, simulate_group
+from paper_2506_22950_amd.group import context_for, decode_group, plan_steps, schedulers_for
+from workload import Workload
+from workload.staging import DeviceInputs
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None):
+    import torch
+
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    wl = wl or Workload(cfg)
+    log = plan_steps(cfg, wl.L, policy, wl.L_hat)
+    dev = DeviceInputs(wl)
+    stream = torch.cuda.current_stream()
+    ctx = context_for(cfg, stream=stream, split_tokens=split)
+    keep = []
+    for p in range(cfg.num_prompts):
+        for layer in range(cfg.layers):
+            k, v = dev.prefix(layer, p)
+            keep.append((k, v))
+            ctx.prefill_shared(p, layer, cfg.prompt_lens[p], k, v)
+    L, S, Hq, Hkv, d = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    es = cfg.elem_bytes
+    o = torch.empty((L, S, Hq, d), dtype=torch.float32, device="cuda")
+    o_ptr = o.data_ptr()
+    n = len(log)
+    win = {"w0": 0, "w1": 0, "bufs": None}
+
+    def provide(k, layer):
+        if not (win["w0"] <= k < win["w1"]):
+            win["bufs"] = None
+            w1 = min(n, k + window)
+            win["bufs"] = dev.stage(log, k, w1)
+            win["w0"], win["w1"] = k, w1
+            win["ptrs"] = [t.data_ptr() for t in win["bufs"]]
+        j = (k - win["w0"]) * L + layer
+        qp, kp, vp = win["ptrs"]
+        return (qp + j * S * Hq * d * es, kp + j * S * Hkv * d * es, vp + j * S * Hkv * d * es,
+                o_ptr + layer * S * Hq * d * 4)
+
+    captured = {}
+
+    def after(step):
+        if capture(step):
+            captured[step] = o.cpu().numpy()
+
+    t0 = time.time()
+    steps = decode_group(ctx, schedulers_for(cfg, policy, wl.L_hat), wl.L, L, provide, after_step=after)
+    torch.cuda.synchronize()
+    tokens = np.stack([ctx.sample_tokens(p) for p in range(cfg.num_prompts)])
+    stats = ctx.get_stats()
+    ctx.destroy()
+    say(f"  [{cfg.name} {policy}] {steps} steps, {n * L} launches in {time.time() - t0:.1f}s")
+    return wl, log, steps, captured, tokens, stats
+
+
+class _PrefixCache:
+    """The workload with its prefix rows memoised (they are the same for every step)."""
+
+    def __init__(self, wl):
+        self._wl, self.cfg, self._cache = wl, wl.cfg, {}
+
+    def prefix_kv(self, layer, p):
+        if (layer, p) not in self._cache:
+            self._cache[(layer, p)] = self._wl.prefix_kv(layer, p)
+        return self._cache[(layer, p)]
+
+    def suffix_kv(self, layer, p, i, t):
+        return self._wl.suffix_kv(layer, p, i, t)
+
+    def query(self, layer, p, i, t):
+        return self._wl.query(layer, p, i, t)
+
+
+def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None):
+    """Max abs error over every captured live (step, slot, layer) output; idle rows must be 0."""
+    tol = tol if tol is not None else (1e-2 if cfg.dtype == "bf16" else 1e-5)
+    layers = range(cfg.layers) if layers is None else layers
+    wl = _PrefixCache(wl)
+    worst = 0.0
+    checked = 0
+    for k, o in captured.items():
+        for s, e in enumerate(log[k]):
+            if e is None:
+                assert not o[:, s].any(), f"idle slot {s} at step {k} has nonzero output"
+                continue
+            p, i, t = e
+            for layer in layers:
+                ref = attend_slot(wl, layer, p, i, t)
+                err = float(np.abs(o[layer, s].astype(np.float64) - ref).max())
+                assert np.isfinite(o[layer, s]).all()
+                if err > worst:
+                    worst = err
+                assert err <= tol, f"step {k} slot {s} sample {i} t {t} layer {layer}: max abs err {err:.3g} > {tol}"
+                checked += 1
+    return worst, checked
+
+
+def oracle_log(cfg, wl, policy):
+    total, res = simulate_group(wl.L, cfg.slots_per_prompt, policy, wl.L_hat)
+    m = cfg.slots_per_prompt
+    out = []
+    for k in range(total):
+        row = []
+        for p, r in enumerate(res):
+            for ls in range(m):
+                e = r.log[k][ls] if k < r.steps else None
+                row.append(None if e is None else (p, e[0], e[1]))
+        out.append(tuple(row))
+    return out
+
+
+def sample_steps(log, every=13, edge=4):
+    """Steps to check: every `every`-th, the first and last `edge`, and every step
+    where some slot decodes its first token (just refilled)."""
+    n = len(log)
+    keep = set(range(0, n, every)) | set(range(min(edge, n))) | set(range(max(0, n - edge), n))
+    for k, row in enumerate(log):
+        if any(e is not None and e[2] == 1 for e in row):
+            keep.add(k)
+    return keep

@@ -1,0 +1,209 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+* libinfs.so loads and exports every function include/infs.h declares;
+* the refill scheduler plus the context's slot bookkeeping (dry-run contexts)
+  reproduce the oracle simulator's step logs bit for bit;
+* every argument and state error is reported synchronously with its code.
+"""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import POLICIES, simulate, simulate_group
+from paper_2506_22950_amd import infs
+from paper_2506_22950_amd.group import context_for, decode_group, plan_steps, schedulers_for
+from workload import CONFIGS, Workload, get_config
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "infs.h")
+
+
+def test_exports_every_declared_symbol():
+    lib = infs.load()
+    declared = set(re.findall(r"^\s*(?:[\w\s\*]+?)\b(infs_\w+)\s*\(", open(HEADER).read(), re.M))
+    assert declared == set(infs.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.infs_abi_version() == 1
+
+
+def _oracle_log(cfg, L, policy, pred):
+    """Oracle step log in the driver's format: per step, per slot (p, i, t) or None."""
+    total, res = simulate_group(L, cfg.slots_per_prompt, policy, pred)
+    m = cfg.slots_per_prompt
+    log = []
+    for k in range(total):
+        row = []
+        for p, r in enumerate(res):
+            for ls in range(m):
+                e = r.log[k][ls] if k < r.steps else None
+                row.append(None if e is None else (p, e[0], e[1]))
+        log.append(tuple(row))
+    return log
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_dry_run_step_log_matches_simulator_worked_example(policy):
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sim_worked_example.json")))
+    cfg = get_config("tiny_f32").with_(samples_per_prompt=g["G"], slots_per_prompt=g["m"], max_suffix_len=16)
+    L = np.array([g["L"]])
+    pred = np.array([g["pred"]], dtype=float)
+    log = plan_steps(cfg, L, policy, pred)
+    assert len(log) == g["policies"][policy]["steps"]
+    assert log == _oracle_log(cfg, L, policy, pred)
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_dry_run_step_log_matches_simulator_random(policy):
+    rng = np.random.default_rng(7)
+    for trial in range(60):
+        NP = int(rng.integers(1, 4))
+        m = int(rng.integers(1, 6))
+        G = int(rng.integers(1, 14))
+        cfg = get_config("tiny_f32").with_(prompt_lens=tuple(int(x) for x in rng.integers(0, 40, NP)),
+                                           samples_per_prompt=G, slots_per_prompt=m, max_suffix_len=40)
+        L = rng.integers(1, 41, size=(NP, G))
+        pred = L * np.exp(rng.normal(0, 0.3, size=L.shape))
+        assert plan_steps(cfg, L, policy, pred) == _oracle_log(cfg, L, policy, pred), (trial, NP, m, G)
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_dry_run_full_workloads(name):
+    # Full-size bookkeeping of every preset: step counts and logs equal the
+    # simulator's, every sample decodes exactly its length, and continuous
+    # refill needs fewer steps than naive micro groups.
+    cfg = get_config(name)
+    wl = Workload(cfg)
+    log = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
+    assert log == _oracle_log(cfg, wl.L, cfg.policy, wl.L_hat)
+    naive = plan_steps(cfg, wl.L, "naive", wl.L_hat)
+    assert len(log) < len(naive)
+    tokens = np.zeros_like(wl.L)
+    for row in log:
+        for e in row:
+            if e is not None:
+                tokens[e[0], e[1]] += 1
+    assert np.array_equal(tokens, wl.L)
+
+
+def _dry(**over):
+    cfg = get_config("tiny_f32").with_(**over) if over else get_config("tiny_f32")
+    ctx = context_for(cfg, dry_run=True)
+    return cfg, ctx
+
+
+def _code(fn, *a):
+    with pytest.raises(infs.InfsError) as ei:
+        fn(*a)
+    return ei.value.status
+
+
+def test_state_errors():
+    cfg, ctx = _dry()
+    none4 = (None, None, None, None)
+    # decode of a live slot before its prompt is prefilled
+    ctx.refill_slot(0, 0, 3)
+    assert _code(ctx.decode_step, 0, *none4) == infs.E_STATE
+    ctx.prefill_shared(0, 0, 32, None, None)
+    assert _code(ctx.refill_slot, 0, 0, 4) == infs.E_STATE          # slot is live
+    assert _code(ctx.refill_slot, 1, 0, 3) == infs.E_DUP            # id already dispatched
+    assert _code(ctx.retire_slot, 1) == infs.E_STATE                # slot is empty
+    assert _code(ctx.end_step) == infs.E_STATE                      # no layer decoded
+    ctx.decode_step(0, *none4)
+    assert _code(ctx.decode_step, 0, *none4) == infs.E_STATE        # same layer twice in a step
+    assert _code(ctx.refill_slot, 1, 0, 5) == infs.E_STATE          # step is open
+    assert _code(ctx.retire_slot, 0) == infs.E_STATE
+    assert _code(ctx.prefill_shared, 0, 0, 32, None, None) == infs.E_STATE
+    ctx.end_step()
+    assert ctx.slot_state(0) == (3, 1)
+    assert ctx.slot_state(1) == (-1, 0)
+    ctx.retire_slot(0)
+    assert ctx.slot_state(0) == (-1, 0)
+    st = ctx.get_stats()
+    assert (st.steps, st.launches, st.tokens) == (1, 1, 1)
+
+
+def test_argument_errors():
+    cfg, ctx = _dry()
+    assert _code(ctx.refill_slot, 4, 0, 0) == infs.E_ARG    # slot out of range (S = 4)
+    assert _code(ctx.refill_slot, 0, 1, 0) == infs.E_ARG    # prompt 1 does not exist
+    assert _code(ctx.refill_slot, 0, 0, 8) == infs.E_ARG    # sample id >= G
+    assert _code(ctx.refill_slot, 0, 0, -1) == infs.E_ARG
+    assert _code(ctx.prefill_shared, 0, 1, 8, None, None) == infs.E_ARG   # layer out of range
+    assert _code(ctx.prefill_shared, 0, 0, 33, None, None) == infs.E_ARG  # longer than max_prompt_len
+    ctx.prefill_shared(0, 0, 8, None, None)
+    assert _code(ctx.decode_step, 1, None, None, None, None) == infs.E_ARG
+    assert _code(ctx.slot_state, 9) == infs.E_ARG
+    assert _code(ctx.sample_tokens, 0) == infs.E_STATE        # no device counters in dry run
+
+
+def test_capacity_errors():
+    # Response longer than max_suffix_len.
+    cfg, ctx = _dry(max_suffix_len=3)
+    ctx.prefill_shared(0, 0, 32, None, None)
+    ctx.refill_slot(0, 0, 0)
+    none4 = (None, None, None, None)
+    for _ in range(3):
+        ctx.decode_step(0, *none4)
+        ctx.end_step()
+    assert _code(ctx.decode_step, 0, *none4) == infs.E_CAPACITY
+    # Page pool too small: two slots need two pages, the pool has one.
+    cfg = get_config("tiny_f32")
+    ctx = context_for(cfg, dry_run=True, num_pages=1)
+    ctx.prefill_shared(0, 0, 32, None, None)
+    ctx.refill_slot(0, 0, 0)
+    ctx.refill_slot(1, 0, 1)
+    assert _code(ctx.decode_step, 0, *none4) == infs.E_CAPACITY
+    ctx.retire_slot(1)
+    ctx.decode_step(0, *none4)   # the failed attempt changed nothing; one page suffices now
+    ctx.end_step()
+
+
+def test_pages_recycled():
+    # A slot's pages return to the pool on retire: with a pool of exactly one
+    # slot's worth, consecutive samples can reuse it indefinitely.
+    cfg = get_config("tiny_f32").with_(max_suffix_len=40)
+    ctx = context_for(cfg, dry_run=True, num_pages=3)
+    ctx.prefill_shared(0, 0, 32, None, None)
+    none4 = (None, None, None, None)
+    for i in range(8):
+        ctx.refill_slot(0, 0, i)
+        for _ in range(40):
+            ctx.decode_step(0, *none4)
+            ctx.end_step()
+        ctx.retire_slot(0)
+
+
+def test_create_validation():
+    base = dict(num_layers=1, num_q_heads=4, num_kv_heads=2, head_dim=64, num_prompts=1, slots_per_prompt=4,
+                samples_per_prompt=8, max_prompt_len=32, max_suffix_len=64, page_tokens=0, num_pages=0,
+                split_tokens=0, dtype=infs.F32, scale=0.0, flags=infs.FLAG_DRY_RUN)
+    infs.Context(infs.make_config(**base)).destroy()
+    bad = [dict(num_q_heads=3), dict(head_dim=96), dict(num_prompts=0), dict(num_prompts=17),
+           dict(slots_per_prompt=65), dict(samples_per_prompt=0), dict(max_suffix_len=0), dict(page_tokens=32),
+           dict(split_tokens=100), dict(dtype=7), dict(scale=-1.0), dict(flags=2), dict(num_layers=0),
+           dict(slots_per_prompt=16)]   # fp32 with 32 prefix rows: no kernel
+    for b in bad:
+        with pytest.raises(infs.InfsError) as ei:
+            infs.Context(infs.make_config(**{**base, **b}))
+        assert ei.value.status == infs.E_ARG, b
+        assert infs.load().infs_last_error(None).decode() != "no error"
+
+
+def test_sched_errors():
+    s = infs.Sched(4, 2, "fifo")
+    assert s.next(0) == 0
+    with pytest.raises(infs.InfsError):
+        s.next(0)           # slot already holds a sample
+    with pytest.raises(infs.InfsError):
+        s.done(1)           # slot 1 is empty
+    with pytest.raises(infs.InfsError):
+        s.next(2)           # slot out of range
+    with pytest.raises(infs.InfsError):
+        infs.Sched(4, 2, "sjf")   # SJF needs predictions
+    with pytest.raises(infs.InfsError):
+        infs.Sched(4, 2, "sjf", pred_len=[1.0, float("nan"), 2.0, 3.0])
+    assert s.pending == 3

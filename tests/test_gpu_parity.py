@@ -1,0 +1,115 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Bookkeeping (step counts, step logs, device per-sample token counters) must be
+bit-exact; attention outputs within 1e-5 (fp32) or 1e-2 (bf16 K/V, fp32
+accumulation) max abs error; idle slots' rows exactly 0.
+"""
+
+import numpy as np
+import pytest
+
+from tests.gpu_harness import (check_against_oracle, oracle_log, run_gpu_group, sample_steps, say)
+from workload import Workload, get_config
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_and_check(cfg, policy, capture=None, layers=None, split=0, window=1024):
+    wl = Workload(cfg)
+    want_log = oracle_log(cfg, wl, policy)
+    cap = capture(want_log).__contains__ if capture else (lambda k: True)
+    wl, log, steps, captured, tokens, stats = run_gpu_group(cfg, policy, capture=cap, split=split,
+                                                          window=window, wl=wl)
+    assert log == want_log, "step log differs from the oracle simulator"
+    assert steps == len(want_log)
+    assert np.array_equal(tokens, wl.L), "device token counters differ from the drawn lengths"
+    worst, n = check_against_oracle(cfg, wl, log, captured, layers=layers)
+    say(f"  [{cfg.name} {policy}] checked {n} (slot, layer) outputs over {len(captured)} steps, "
+        f"max abs err {worst:.3g}")
+    return wl, log, captured
+
+
+@pytest.mark.parametrize("policy", ["naive", "fifo"])
+def test_tiny_f32_every_step(policy):
+    # 1 layer, 4Q/2KV, d=64, P=32, G=8, m=4, L~U[1,64], fp32: every output of every step.
+    _run_and_check(get_config("tiny_f32"), policy)
+
+
+def test_tiny_f32_multichunk_ragged():
+    # fp32 wavefront path over several split-K chunks with ragged tails:
+    # P=300 with 128-token chunks, responses up to 400.
+    cfg = get_config("tiny_f32").with_(prompt_lens=(300,), length_dist=("uniform", 1, 400), max_suffix_len=400)
+    _run_and_check(cfg, "fifo", split=128, capture=lambda log: sample_steps(log, every=3))
+
+
+def test_qwen3_1layer_bf16_mfma16():
+    # Qwen3-1.7B-shaped layer: 16Q/8KV, d=128, P=512, G=32, m=8 (16 prefix rows: MFMA), FIFO.
+    cfg = get_config("qwen3_1p7b_l1_g32")
+    _run_and_check(cfg, "fifo", capture=lambda log: sample_steps(log, every=11))
+
+
+def test_bf16_mfma32_small_every_step():
+    # The throughput workload's shape (16Q/8KV, d=128, m=16: 32 prefix rows) on a
+    # small group: 2 layers, P=700 (ragged last MFMA block), 128-token chunks.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(700,), samples_per_prompt=24,
+                                             length_dist=("lognormal", 4.0, 1.0, 1, 300), max_suffix_len=300,
+                                             pool_rows=None)
+    _run_and_check(cfg, "sjf", split=128, capture=lambda log: sample_steps(log, every=2))
+
+
+def test_bf16_mfma64_and_hpk4_multi_prompt():
+    # Qwen3-8B shape (32Q/8KV: 4 query heads per KV head, 64 prefix rows), three
+    # prompts of different lengths including an empty prefix.
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(0, 130, 511), samples_per_prompt=20,
+                                                length_dist=("lognormal", 4.0, 1.0, 1, 260),
+                                                max_suffix_len=260, pool_rows=None)
+    _run_and_check(cfg, "sjf", split=128, capture=lambda log: sample_steps(log, every=3))
+
+
+def test_bf16_single_slot_wave_prefix():
+    # m=1: 2 prefix rows, so the prefix runs on the wavefront path in bf16.
+    cfg = get_config("qwen3_1p7b_l1_g32").with_(slots_per_prompt=1, samples_per_prompt=4, prompt_lens=(257,),
+                                                length_dist=("lognormal", 4.0, 0.8, 1, 300), max_suffix_len=300)
+    _run_and_check(cfg, "fifo", capture=lambda log: sample_steps(log, every=5))
+
+
+def test_response_reaches_capacity():
+    # Samples of exactly max_suffix_len tokens: the last page fills completely.
+    cfg = get_config("qwen3_1p7b_l1_g32").with_(samples_per_prompt=8, length_dist=("uniform", 1, 64),
+                                                max_suffix_len=64)
+    wl = Workload(cfg, lengths=np.array([[64, 1, 64, 17, 16, 33, 64, 2]]))
+    want = oracle_log(cfg, wl, "fifo")
+    _, log, steps, captured, tokens, _ = run_gpu_group(cfg, "fifo", wl=wl)
+    assert log == want and np.array_equal(tokens, wl.L)
+    check_against_oracle(cfg, wl, log, captured)
+
+
+def test_schedule_invariance_and_determinism():
+    # The output for (layer, sample, t) does not depend on the schedule or slot
+    # that served it: naive and FIFO runs agree bit for bit wherever both
+    # decode the same (sample, t); a repeated run is bitwise identical.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=1, prompt_lens=(384,), samples_per_prompt=12,
+                                             length_dist=("lognormal", 4.0, 1.0, 1, 200), max_suffix_len=200,
+                                             pool_rows=None)
+    runs = {}
+    for name, policy in (("fifo", "fifo"), ("naive", "naive"), ("fifo2", "fifo")):
+        _, log, _, captured, _, _ = run_gpu_group(cfg, policy, split=128)
+        vals = {}
+        for k, o in captured.items():
+            for s, e in enumerate(log[k]):
+                if e is not None:
+                    vals[(e[1], e[2])] = o[0, s].copy()
+        runs[name] = vals
+    assert runs["fifo"].keys() == runs["naive"].keys()
+    for key, v in runs["fifo"].items():
+        assert np.array_equal(v, runs["naive"][key]), key
+        assert np.array_equal(v, runs["fifo2"][key]), key
+
+
+@pytest.mark.parametrize("name", ["qwen3_1p7b_g64"])
+def test_full_size_sampled(name):
+    # Full workload in the launch configuration the benchmark times; outputs of
+    # sampled steps on layers {0, L/2, L-1} against the oracle.
+    cfg = get_config(name)
+    _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=397, edge=2),
+                   layers=(0, cfg.layers - 1), window=512)
