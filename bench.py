@@ -1,0 +1,250 @@
+"""Benchmark: shared-prefix continuous-sampling group decode on one MI355X.
+
+One benchmark step is one whole group decode of the throughput workload
+(28 layers, 16 query / 8 KV heads, head_dim 128, a 2048-token shared prompt,
+G=64 samples on m=16 slots, lognormal lengths, SJF refill on noisy predicted
+lengths, bf16 K/V): prefill of the shared prompt KV for every layer, then every
+running step (refill, one decode_step per layer, end_step, retire) until all 64
+samples are done.  All inputs are synthetic and staged in HBM before timing.
+
+Prints one JSON line with tokens/s (value), the roofline of the decode kernel
+(algorithmic bytes per launch over its average duration, timed with HIP events
+on the library's stream in a separate pass), and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "generated tokens/sec per group decode + achieved HBM TB/s vs peak, 1 MI355X"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(cfg, steplog):
+    """Algorithmic HBM bytes of all decode launches, from the step log alone:
+    prefix K/V once per prompt with a live slot, each live slot's response K/V
+    (new token included), the append write, Q read and fp32 O write."""
+    kvrow = cfg.num_kv_heads * cfg.head_dim * cfg.elem_bytes
+    total = 0.0
+    for row in steplog:
+        live_prompts = {e[0] for e in row if e is not None}
+        b = sum(2.0 * cfg.prompt_lens[p] * kvrow for p in live_prompts)
+        for e in row:
+            if e is not None:
+                b += 2.0 * e[2] * kvrow + 2.0 * kvrow + cfg.num_q_heads * cfg.head_dim * (cfg.elem_bytes + 4)
+        total += b
+    return total * cfg.layers
+
+
+class Bench:
+    def __init__(self, cfg_name, split=0):
+        import numpy as np
+        import torch
+
+        from paper_2506_22950_amd import infs
+        from paper_2506_22950_amd.group import context_for, plan_steps
+        from workload import Workload, get_config
+        from workload.staging import DeviceInputs
+
+        self.np, self.torch = np, torch
+        infs.load()
+        cfg = get_config(cfg_name)
+        self.cfg = cfg
+        t0 = time.time()
+        self.wl = wl = Workload(cfg)
+        self.log = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
+        self.naive_steps = len(plan_steps(cfg, wl.L, "naive", wl.L_hat))
+        dev = DeviceInputs(wl)
+        self.prefix = [[dev.prefix(l, p) for l in range(cfg.layers)] for p in range(cfg.num_prompts)]
+        self.q, self.k, self.v = dev.stage(self.log, 0, len(self.log))
+        del dev
+        torch.cuda.synchronize()
+        self.stream = torch.cuda.current_stream()
+        self.ctx = context_for(cfg, stream=self.stream, split_tokens=split)
+        L, S, Hq, Hkv, d, es = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.elem_bytes
+        self.o = torch.empty((L, S, Hq, d), dtype=torch.float32, device="cuda")
+        self.qp, self.kp, self.vp, self.op = (self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(),
+                                              self.o.data_ptr())
+        self.sq, self.skv, self.so = S * Hq * d * es, S * Hkv * d * es, S * Hq * d * 4
+        self.L = L
+        self.tokens = wl.total_tokens
+        self.alg_bytes = algorithmic_bytes(cfg, self.log)
+        log(f"setup {time.time() - t0:.1f}s: {len(self.log)} steps ({cfg.policy}) vs {self.naive_steps} naive, "
+            f"{self.tokens} tokens, staged {(self.q.numel() + self.k.numel() + self.v.numel()) * es / 2**30:.1f} GiB")
+
+    def provide(self, k, layer):
+        j = k * self.L + layer
+        return (self.qp + j * self.sq, self.kp + j * self.skv, self.vp + j * self.skv, self.op + layer * self.so)
+
+    def group_decode(self):
+        """One benchmark step: prefill every layer, then decode the whole group."""
+        from paper_2506_22950_amd.group import decode_group, schedulers_for
+
+        cfg, ctx = self.cfg, self.ctx
+        ctx.reset()
+        for p in range(cfg.num_prompts):
+            for layer in range(cfg.layers):
+                k, v = self.prefix[p][layer]
+                ctx.prefill_shared(p, layer, cfg.prompt_lens[p], k, v)
+        return decode_group(ctx, schedulers_for(cfg, cfg.policy, self.wl.L_hat), self.wl.L, cfg.layers,
+                            self.provide)
+
+    def check_bookkeeping(self, steps):
+        np = self.np
+        assert steps == len(self.log), (steps, len(self.log))
+        for p in range(self.cfg.num_prompts):
+            assert np.array_equal(self.ctx.sample_tokens(p), self.wl.L[p]), "token counters"
+
+    def kernel_timing(self):
+        """One more whole group decode with kernel timing on: the summed device
+        wall-clock time of the decode launches (first block start to last block
+        end of each), and the HIP-event time of the whole pass on the
+        library's stream."""
+        self.ctx.timing_begin()
+        self.group_decode()
+        ms, region_ms, n = self.ctx.timing_end()
+        st = self.ctx.get_stats()
+        return ms, region_ms, n, st.alg_bytes, st.launches
+
+
+def cpu_baseline(bench, budget_s=15.0):
+    """The float64 oracle on the host, single-threaded, on whole decode steps
+    (every layer, every live slot) sampled evenly over the run."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    from oracle import attend_slot
+
+    cfg, wl, steplog = bench.cfg, bench.wl, bench.log
+    n = len(steplog)
+    order = [int(x) for x in np.linspace(0, n - 1, 64)]
+    # visit the evenly spaced steps in a bit-reversed-like order so any prefix is spread out
+    order = order[::8] + [x for i, x in enumerate(order) if i % 8]
+    done, spent, toks = [], 0.0, 0
+    with threadpool_limits(limits=1):
+        for k in order:
+            t0 = time.perf_counter()
+            for e in steplog[k]:
+                if e is None:
+                    continue
+                p, i, t = e
+                for layer in range(cfg.layers):
+                    attend_slot(wl, layer, p, i, t)
+            spent += time.perf_counter() - t0
+            done.append(k)
+            if spent >= budget_s and len(done) >= 2:
+                break
+    per_step = spent / len(done)
+    est_total = per_step * n
+    return {
+        "value": round(bench.tokens / est_total, 4),
+        "unit": "tokens/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{len(done)} whole decode steps (all {cfg.layers} layers x live slots) of {n}, evenly spaced; "
+                   f"{spent:.1f}s measured, {per_step:.2f}s/step extrapolated to {n} steps and "
+                   f"{bench.tokens} tokens; float64 numpy, 1 BLAS thread"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="qwen3_1p7b_g64")
+    ap.add_argument("--split", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    b = Bench(args.workload, split=args.split)
+
+    for w in range(args.warmup):
+        t0 = time.time()
+        steps = b.group_decode()
+        torch.cuda.synchronize()
+        b.check_bookkeeping(steps)
+        log(f"warmup {w}: {time.time() - t0:.2f}s")
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        steps = b.group_decode()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    b.check_bookkeeping(steps)
+    ms_per_step = elapsed * 1000.0 / args.steps
+    value = b.tokens * args.steps / elapsed
+    log(f"timed {args.steps} group decodes: {ms_per_step:.1f} ms each, {value:.0f} tokens/s, "
+        f"end-to-end {b.alg_bytes / (ms_per_step / 1e3) / 1e9:.0f} GB/s algorithmic")
+
+    roof = None
+    if not args.no_kernel_timing:
+        ms, region_ms, n, alg, launches = b.kernel_timing()
+        assert n == launches, (n, launches)
+        rel = abs(alg - b.alg_bytes) / b.alg_bytes
+        assert rel < 1e-9, f"library and step-log byte counts differ: {alg} vs {b.alg_bytes}"
+        avg_us = ms * 1000.0 / n
+        per_launch = alg / n
+        achieved = per_launch / (avg_us * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
+                "alg_bytes_per_launch": round(per_launch),
+                "timing": "device wall clock, first block start to last block end, every launch of one group decode",
+                "event_region_ms": round(region_ms, 2),
+                "event_us_per_launch": round(region_ms * 1000.0 / n, 3)}
+        log(f"kernel: {n} launches, avg {avg_us:.2f} us, {per_launch / 1e6:.2f} MB/launch -> {achieved:.0f} GB/s; "
+            f"HIP-event region {region_ms:.1f} ms = {region_ms * 1000.0 / n:.2f} us per launch")
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(b)
+    cfg = b.cfg
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name,
+            "layers": cfg.layers, "q_heads": cfg.num_q_heads, "kv_heads": cfg.num_kv_heads,
+            "head_dim": cfg.head_dim, "prompt_len": list(cfg.prompt_lens), "G": cfg.samples_per_prompt,
+            "m": cfg.slots_per_prompt, "policy": cfg.policy, "decode_steps": len(b.log),
+            "naive_decode_steps": b.naive_steps, "generated_tokens": b.tokens,
+            "alg_bytes_per_group": round(b.alg_bytes),
+            "end_to_end_alg_GBps": round(b.alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
+        },
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -90,7 +90,10 @@ typedef struct infs_config {
     int32_t max_suffix_len;      /* capacity of one response, >= 1 */
     int32_t page_tokens;         /* tokens per response page; 0 or 16 */
     int32_t num_pages;           /* response page pool size; 0: enough for every slot at capacity */
-    int32_t split_tokens;        /* split-K chunk length in tokens; 0: 256; a multiple of 128 */
+    int32_t split_tokens;        /* split-K chunk length of responses in tokens; 0: 256; a multiple of 128
+                                    up to 4096.  Prefixes are split in 128-token chunks when they run on
+                                    MFMA tiles, else in split_tokens chunks; prefix plus response chunks
+                                    of one slot must not exceed 128 */
     int32_t dtype;               /* infs_dtype of Q, K, V */
     float scale;                 /* softmax scale; 0: 1/sqrt(head_dim) */
     uint32_t flags;              /* INFS_FLAG_* */
@@ -162,16 +165,19 @@ infs_status infs_slot_state(const infs_ctx* ctx, int32_t slot, int64_t* sample_i
    0, counted on the GPU) into counts_host[0..n).  n must equal samples_per_prompt. */
 infs_status infs_sample_tokens(infs_ctx* ctx, int32_t prompt, int32_t* counts_host, int32_t n);
 
-/* Wait for all work enqueued by the context. */
+/* Wait for all work enqueued by the context.  Also reports (E_DEVICE) a decode launch whose merge
+   stage stopped waiting for its producers, which leaves that launch's outputs invalid (NaN). */
 infs_status infs_sync(infs_ctx* ctx);
 
 infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
 
-/* Kernel timing: between begin and end every decode_step launch is bracketed by HIP events on
-   the context's stream.  infs_timing_end synchronises and returns the summed kernel time (ms) and
-   the number of timed launches. */
+/* Kernel timing.  Between begin and end every decode_step launch records, on the device wall
+   clock, the start of its first work-group and the end of its last one.  infs_timing_end
+   synchronises and returns the summed kernel time (ms) of the timed launches, their number, and
+   the time between the two calls measured by HIP events on the context's stream (region_ms,
+   which also covers gaps between launches and any other work on the stream). */
 infs_status infs_timing_begin(infs_ctx* ctx);
-infs_status infs_timing_end(infs_ctx* ctx, double* kernel_ms, int64_t* launches);
+infs_status infs_timing_end(infs_ctx* ctx, double* kernel_ms, double* region_ms, int64_t* launches);
 
 /* Message of the last failed call on ctx (NULL ctx: last failed infs_create / infs_sched_create
    of this thread).  Never NULL. */

@@ -118,7 +118,6 @@ struct Shape {
   static constexpr int ROWB = D * ES;              // bytes of one K or V row of one head
   static constexpr int LPT = ROWB / 16;            // lanes per token (wavefront path)
   static constexpr int TPI = 64 / LPT;             // tokens per load instruction
-  static constexpr int U = (32 / TPI) < 8 ? (32 / TPI) : 8;  // unrolled loads per iteration
   static constexpr int PAGEB = kPageTokens * ROWB; // bytes of one page of one head, K or V
   static constexpr int NB = PR / 16;               // MFMA row blocks
   static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
@@ -126,24 +125,70 @@ struct Shape {
   static constexpr int WAVE_NR = (!MFMA && PR > HPK) ? PR : HPK;
   static constexpr int WAVE_SMEM = 4 * WAVE_NR * (D + 2);
   static constexpr int MFMA_SLOT = MFMA ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
-  static constexpr int MFMA_SMEM = 2 * MFMA_SLOT;
+  static constexpr int MFMA_SMEM = 4 * MFMA_SLOT;
   static constexpr int SMEM = WAVE_SMEM > MFMA_SMEM ? WAVE_SMEM : MFMA_SMEM;
+  // 64 MFMA rows keep 128 accumulator registers live, and 16 wavefront rows
+  // as many: those shapes run 1 wavefront per SIMD rather than spill; every
+  // other shape runs 2 per SIMD.
+  static constexpr int MIN_WAVES = ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
   static_assert(LPT >= 2 && LPT <= 64, "row size");
   static_assert(!MFMA || BF, "MFMA path is bf16");
   static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
 };
 
 // ----------------------------------------------------------------------------
-// Wavefront path: NR query rows, token range [t0, t1) of one KV head.
-// Lane layout: LPT consecutive lanes hold one token's row (16 B each); a load
-// instruction covers TPI tokens.  Each token group keeps its own running
-// (m, l, o) and the groups are combined at the end.
+// Partials are exchanged between work-groups through agent-scope atomic
+// stores and loads (coherent across the XCDs' L2 caches), ordered by waiting
+// for the stores to complete before the arrival counter is bumped.  This
+// avoids the whole-cache write-back and invalidate of an agent-scope fence.
 // ----------------------------------------------------------------------------
+__device__ __forceinline__ void st_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) x = fmaxf(x, __shfl_xor(x, s));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) x += __shfl_xor(x, s);
+  return x;
+}
+
+// ----------------------------------------------------------------------------
+// Wavefront path: NR query rows over the token range [t0, t1) of one KV head.
+// LPT consecutive lanes hold one token's row (16 B each), so a load
+// instruction covers TPI tokens; U loads per lane for K and for V are issued
+// together before any arithmetic.  Each token group keeps its own running
+// (m, l, o); the groups are combined at the end.  t0 must be a multiple of 16
+// (page-aligned) so that every load instruction stays inside one page.
+// ----------------------------------------------------------------------------
+template <class SH, int NR>
+struct WaveCfg {
+  // Loads per lane per iteration, sized so that K/V buffers, scores and
+  // accumulators of NR rows stay within the two-wavefronts-per-SIMD budget.
+  static constexpr int UMAX = NR <= 2 ? 16 : NR <= 4 ? 8 : 4;
+  static constexpr int U = (64 / SH::TPI) < UMAX ? (64 / SH::TPI) : UMAX;
+  static_assert(16 % SH::TPI == 0, "a load instruction must not straddle a page");
+};
+
 template <class SH, int NR, class Addr>
 __device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, const u32x4 (&q)[NR], float sl2,
                                              float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
-  constexpr int LPT = SH::LPT, TPI = SH::TPI, U = SH::U, EPL = SH::EPL;
-  const int lane = threadIdx.x & 63, ts = lane / LPT, ch = lane % LPT;
+  constexpr int LPT = SH::LPT, TPI = SH::TPI, EPL = SH::EPL, U = WaveCfg<SH, NR>::U;
+  // Loads are issued in sub-blocks of SB per lane (K, then V) and the online
+  // softmax runs per sub-block, so the arithmetic on early sub-blocks overlaps
+  // the arrival of later ones.  Every load is unconditional: tokens past t1
+  // read a valid row (Addr keeps addresses in bounds) and are masked to -inf.
+  constexpr int SB = U >= 8 ? 4 : U;
+  constexpr int NSB = U / SB;
+  static_assert(U % SB == 0 && SB % 2 == 0, "sub-blocks of token pairs");
+  const int lane = threadIdx.x & 63, ts = lane / LPT;
 #pragma unroll
   for (int r = 0; r < NR; ++r) {
     m[r] = NEG_INF;
@@ -151,52 +196,106 @@ __device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, con
 #pragma unroll
     for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
   }
+  constexpr int PGI = (U * TPI + 15) / 16;  // 16-token pages touched per iteration
   for (int base = t0; base < t1; base += U * TPI) {
+    // Page numbers first, in straight-line code: the compiler then waits for
+    // the page-table load once instead of before every K/V load.
+    int pg[PGI];
+#pragma unroll
+    for (int i = 0; i < PGI; ++i) pg[i] = ad.page(((base - t0) >> 4) + i);
     u32x4 kk[U], vv[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int tok = base + u * TPI + ts;
-      if (tok < t1) {
-        kk[u] = *ad.k(tok, ch);
-        vv[u] = *ad.v(tok, ch);
-      } else {
-        kk[u] = u32x4{0, 0, 0, 0};
-        vv[u] = u32x4{0, 0, 0, 0};
-      }
-    }
-    float s[U][NR];
+    for (int b = 0; b < NSB; ++b) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const bool ok = base + u * TPI + ts < t1;
+      for (int kind = 0; kind < 2; ++kind)
+#pragma unroll
+        for (int u = b * SB; u < b * SB + SB; ++u) {
+          u32x4& dst = kind ? vv[u] : kk[u];
+          dst = *ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1);
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < NSB; ++b) {
+      float s[SB][NR];
+#pragma unroll
+      for (int x = 0; x < SB; ++x) {
+        const int u = b * SB + x;
+        const bool ok = base + u * TPI + ts < t1;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+          const float y = group_sum<LPT>(dot16B<SH::BF>(kk[u], q[r])) * sl2;
+          s[x][r] = ok ? y : NEG_INF;
+        }
+      }
 #pragma unroll
       for (int r = 0; r < NR; ++r) {
-        const float x = group_sum<LPT>(dot16B<SH::BF>(kk[u], q[r])) * sl2;
-        s[u][r] = ok ? x : NEG_INF;
-      }
-    }
+        float mb = s[0][r];
 #pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      float mb = s[0][r];
+        for (int x = 1; x < SB; ++x) mb = fmaxf(mb, s[x][r]);
+        const float mn = fmaxf(m[r], mb);
+        const float mu = (mn == NEG_INF) ? 0.f : mn;
+        const float corr = exp2_fast(m[r] - mu);
+        m[r] = mn;
+        l[r] *= corr;
 #pragma unroll
-      for (int u = 1; u < U; ++u) mb = fmaxf(mb, s[u][r]);
-      const float mn = fmaxf(m[r], mb);
-      const float mu = (mn == NEG_INF) ? 0.f : mn;
-      const float corr = exp2_fast(m[r] - mu);
-      m[r] = mn;
-      l[r] *= corr;
+        for (int e = 0; e < EPL; ++e) o[r][e] *= corr;
+        if constexpr (SH::BF) {
+          // P.V two tokens at a time with bf16 dot products: the probabilities
+          // are rounded to bf16 and the normaliser sums the same rounded values.
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) o[r][e] *= corr;
+          for (int x = 0; x < SB; x += 2) {
+            const int u = b * SB + x;
+            const __bf16 h0 = (__bf16)exp2_fast(s[x][r] - mu), h1 = (__bf16)exp2_fast(s[x + 1][r] - mu);
+            l[r] += (float)h0 + (float)h1;
+            const bf16x2 pb = {h0, h1};
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float p = exp2_fast(s[u][r] - mu);
-        l[r] += p;
-        axpy16B<SH::BF>(o[r], p, vv[u]);
+            for (int k = 0; k < 4; ++k) {
+              const uint32_t lo = __builtin_amdgcn_perm(vv[u + 1][k], vv[u][k], 0x05040100u);  // elems 2k
+              const uint32_t hi = __builtin_amdgcn_perm(vv[u + 1][k], vv[u][k], 0x07060302u);  // elems 2k+1
+              o[r][2 * k] = __builtin_amdgcn_fdot2_f32_bf16(pb, __builtin_bit_cast(bf16x2, lo), o[r][2 * k], false);
+              o[r][2 * k + 1] = __builtin_amdgcn_fdot2_f32_bf16(pb, __builtin_bit_cast(bf16x2, hi), o[r][2 * k + 1], false);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int x = 0; x < SB; ++x) {
+            const float p = exp2_fast(s[x][r] - mu);
+            l[r] += p;
+            axpy16B<false>(o[r], p, vv[b * SB + x]);
+          }
+        }
       }
     }
   }
-  // Combine the TPI token groups of this wavefront (lanes ch, ch+LPT, ...).
+}
+
+// Fold one token (K row chunk k, V row chunk v held by every token group) into
+// token group 0's running partial.  All lanes take part in the reduction.
+template <class SH, int NR>
+__device__ __forceinline__ void fold_token(const u32x4& k, const u32x4& v, const u32x4 (&q)[NR], float sl2,
+                                           float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
+  const bool mine = (threadIdx.x & 63) < SH::LPT;
 #pragma unroll
-  for (int mask = LPT; mask < 64; mask <<= 1) {
+  for (int r = 0; r < NR; ++r) {
+    const float x = group_sum<SH::LPT>(dot16B<SH::BF>(k, q[r])) * sl2;
+    if (mine) {
+      const float mn = fmaxf(m[r], x);
+      const float corr = exp2_fast(m[r] - mn);
+      const float p = exp2_fast(x - mn);
+      m[r] = mn;
+      l[r] = l[r] * corr + p;
+#pragma unroll
+      for (int e = 0; e < SH::EPL; ++e) o[r][e] *= corr;
+      axpy16B<SH::BF>(o[r], p, v);
+    }
+  }
+}
+
+// Combine the TPI token groups of a wavefront (lanes ch, ch+LPT, ...).
+template <class SH, int NR>
+__device__ __forceinline__ void wave_combine_groups(float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
+#pragma unroll
+  for (int mask = SH::LPT; mask < 64; mask <<= 1) {
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
       const float m2 = __shfl_xor(m[r], mask);
@@ -204,7 +303,7 @@ __device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, con
       float a, b;
       lse_combine(m[r], l[r], m2, l2, a, b);
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) o[r][e] = o[r][e] * a + __shfl_xor(o[r][e], mask) * b;
+      for (int e = 0; e < SH::EPL; ++e) o[r][e] = o[r][e] * a + __shfl_xor(o[r][e], mask) * b;
     }
   }
 }
@@ -246,42 +345,41 @@ __device__ __forceinline__ void block_store_partial(float* smem, const float (&m
       L += wgt * sml[(v * NR + r) * 2 + 1];
       O += wgt * so[(v * NR + r) * D + d];
     }
-    ws_o[(rec0 + r) * D + d] = O;
+    st_coherent(ws_o + (rec0 + r) * D + d, O);
     if (d == 0) {
-      ws_ml[(rec0 + r) * 2 + 0] = M;
-      ws_ml[(rec0 + r) * 2 + 1] = L;
+      st_coherent(ws_ml + (rec0 + r) * 2 + 0, M);
+      st_coherent(ws_ml + (rec0 + r) * 2 + 1, L);
     }
   }
 }
 
 // Addressing of the plain prefix store: [prompt][kv][K|V][max_prompt_len][D].
+// Row of token tokbase + (lane / LPT), clamped below `end` so that masked
+// tokens still read inside this head's region.
 template <class SH>
 struct PrefixAddr {
-  const char* kb;
-  const char* vb;
-  __device__ const u32x4* k(int tok, int ch) const { return (const u32x4*)(kb + (int64_t)tok * SH::ROWB) + ch; }
-  __device__ const u32x4* v(int tok, int ch) const { return (const u32x4*)(vb + (int64_t)tok * SH::ROWB) + ch; }
+  const char* base[2];
+  __device__ int page(int) const { return 0; }
+  __device__ const u32x4* row(int kind, int tokbase, int, int, int end) const {
+    const int lane = threadIdx.x & 63;
+    const int tok = min(tokbase + lane / SH::LPT, end - 1);
+    return (const u32x4*)(base[kind] + (int64_t)tok * SH::ROWB) + lane % SH::LPT;
+  }
 };
 
-// Addressing of a slot's response: pages [page][kv][K|V][16][D]; the token of
-// this step (position len-1) is read from the caller's new K/V rows.
+// Addressing of a slot's stored response tokens: pages [page][kv][K|V][16][D].
+// Lane i of `pages` holds the page of the wave's i-th 16-token group.  A load
+// instruction covers TPI consecutive tokens of one page, so its address is
+// (page base) + (token in page) * ROWB + lane * 16 -- uniform plus lane offset.
 template <class SH>
 struct SuffixAddr {
   const char* pool;
-  const int32_t* pt;   // this slot's page table
-  const char* knew;    // this slot's new K row for this KV head
-  const char* vnew;
-  int last;
+  int pages;
   int hkv, g;
-  __device__ const char* page(int tok, int kind) const {
-    const int pg = pt[tok >> 4];
-    return pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tok & 15) * SH::ROWB;
-  }
-  __device__ const u32x4* k(int tok, int ch) const {
-    return (tok == last) ? (const u32x4*)knew + ch : (const u32x4*)page(tok, 0) + ch;
-  }
-  __device__ const u32x4* v(int tok, int ch) const {
-    return (tok == last) ? (const u32x4*)vnew + ch : (const u32x4*)page(tok, 1) + ch;
+  __device__ int page(int pslot) const { return __builtin_amdgcn_readlane(pages, pslot); }
+  __device__ const u32x4* row(int kind, int tokbase, int, int pg, int) const {
+    const int lane = threadIdx.x & 63;
+    return (const u32x4*)(pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tokbase & 15) * SH::ROWB) + lane;
   }
 };
 
@@ -297,8 +395,8 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
   constexpr int PR = SH::PR, HPK = SH::HPK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
   const int plen = a.prompt[p].plen;
-  const int t0 = c * a.split, t1 = min(t0 + a.split, plen);
-  const int sub = a.split / 4;
+  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
+  const int sub = a.prefix_split / 4;
   const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
   u32x4 q[PR];
 #pragma unroll
@@ -310,10 +408,11 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
       q[r] = u32x4{0, 0, 0, 0};
   }
   const int64_t head = ((int64_t)p * a.Hkv + g) * 2;
-  PrefixAddr<SH> ad{(const char*)a.prefix + head * a.max_prompt_len * SH::ROWB,
-                    (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::ROWB};
+  PrefixAddr<SH> ad{{(const char*)a.prefix + head * a.max_prompt_len * SH::ROWB,
+                     (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::ROWB}};
   float m[PR], l[PR], o[PR][SH::EPL];
   wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
+  wave_combine_groups<SH, PR>(m, l, o);
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * PR;
   block_store_partial<SH, PR>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
 }
@@ -326,16 +425,65 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
 // online-softmax rescale needs no cross-lane transpose.  The P^T operand takes
 // the 8 probabilities a lane already holds; the contraction index (token) is
 // the same permutation on both operands, and the prefix store keeps V in that
-// order (see prefill_mfma_kernel).
+// order (see prefill_mfma_kernel).  Two blocks are loaded per round.
 // ----------------------------------------------------------------------------
+template <class SH>
+__device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const bf16x8 (&va)[SH::DB],
+                                           const bf16x8 (&bq)[SH::NB][SH::KB], int tb, int t1, float sl2,
+                                           f32x4 (&acc)[SH::NB][SH::DB], float (&mrow)[SH::NB],
+                                           float (&lrow)[SH::NB]) {
+  constexpr int NB = SH::NB, KB = SH::KB, DB = SH::DB;
+  const int lane = threadIdx.x & 63, q4 = lane >> 4;
+  f32x4 st[2][NB];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mb][kb], bq[nb][kb], t, 0, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int tok = tb + mb * 16 + q4 * 4 + e;
+        t[e] = (tok < t1) ? t[e] * sl2 : NEG_INF;
+      }
+      st[mb][nb] = t;
+    }
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    float mb_ = fmaxf(fmaxf(fmaxf(st[0][nb][0], st[0][nb][1]), fmaxf(st[0][nb][2], st[0][nb][3])),
+                      fmaxf(fmaxf(st[1][nb][0], st[1][nb][1]), fmaxf(st[1][nb][2], st[1][nb][3])));
+    mb_ = fmaxf(mb_, __shfl_xor(mb_, 16));
+    mb_ = fmaxf(mb_, __shfl_xor(mb_, 32));
+    const float mn = fmaxf(mrow[nb], mb_);
+    const float mu = (mn == NEG_INF) ? 0.f : mn;
+    const float corr = exp2_fast(mrow[nb] - mu);
+    mrow[nb] = mn;
+    lrow[nb] *= corr;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[nb][db] *= corr;
+    bf16x8 pb;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const __bf16 h = (__bf16)exp2_fast(st[mb][nb][e] - mu);
+        pb[mb * 4 + e] = h;
+        lrow[nb] += (float)h;
+      }
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[db], pb, acc[nb][db], 0, 0, 0);
+  }
+}
+
 template <class SH>
 __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
   constexpr int D = SH::D, NB = SH::NB, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
   const int plen = a.prompt[p].plen;
-  const int t0 = c * a.split, t1 = min(t0 + a.split, plen);
+  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
   const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
-  const int bpw = a.split / kMfmaBlock / 4;
+  const int bpw = a.prefix_split / kMfmaBlock / 4;
   const int b0 = w * bpw, b1 = min(b0 + bpw, nblk);
   const float sl2 = a.scale_log2;
 
@@ -366,59 +514,20 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
 
   const uint16_t* head = (const uint16_t*)a.prefix +
                          ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D);
+  // One 32-token block (16 KB of K and V) in flight per wavefront: the
+  // register budget is kept at two wavefronts per SIMD, and the second
+  // wavefront hides this one's load latency.
   for (int b = b0; b < b1; ++b) {
-    const int tb = t0 + b * kMfmaBlock;
-    const uint16_t* kblk = head + (int64_t)(tb / kMfmaBlock) * (2 * kMfmaBlock * D);
-    const uint16_t* vblk = kblk + kMfmaBlock * D;
     bf16x8 ka[2][KB], va[DB];
+    const uint16_t* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D);
+    const uint16_t* vblk = kblk + kMfmaBlock * D;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = *(const bf16x8*)(kblk + ((mb * KB + kb) * 64 + lane) * 8);
 #pragma unroll
     for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
-
-    f32x4 st[2][NB];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        f32x4 t = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mb][kb], bq[nb][kb], t, 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int tok = tb + mb * 16 + q4 * 4 + e;
-          t[e] = (tok < t1) ? t[e] * sl2 : NEG_INF;
-        }
-        st[mb][nb] = t;
-      }
-
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float mb_ = fmaxf(fmaxf(fmaxf(st[0][nb][0], st[0][nb][1]), fmaxf(st[0][nb][2], st[0][nb][3])),
-                        fmaxf(fmaxf(st[1][nb][0], st[1][nb][1]), fmaxf(st[1][nb][2], st[1][nb][3])));
-      mb_ = fmaxf(mb_, __shfl_xor(mb_, 16));
-      mb_ = fmaxf(mb_, __shfl_xor(mb_, 32));
-      const float mn = fmaxf(mrow[nb], mb_);
-      const float mu = (mn == NEG_INF) ? 0.f : mn;
-      const float corr = exp2_fast(mrow[nb] - mu);
-      mrow[nb] = mn;
-      lrow[nb] *= corr;
-#pragma unroll
-      for (int db = 0; db < DB; ++db) acc[nb][db] *= corr;
-      bf16x8 pb;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const __bf16 h = (__bf16)exp2_fast(st[mb][nb][e] - mu);
-          pb[mb * 4 + e] = h;
-          lrow[nb] += (float)h;
-        }
-#pragma unroll
-      for (int db = 0; db < DB; ++db) acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[db], pb, acc[nb][db], 0, 0, 0);
-    }
+    mfma_block<SH>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
   }
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
@@ -437,33 +546,38 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
       sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
     }
   };
-  auto take = [&](const float* sl) {
+  // All four wavefronts publish their partials; after one barrier each
+  // combines the four for a quarter of the head dimension and stores it.
+  put(smem + w * SH::MFMA_SLOT);
+  __syncthreads();
+  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+  constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
+  static_assert(DB % 4 == 0, "head_dim blocks per wave");
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      float a, b;
-      lse_combine(mrow[nb], lrow[nb], sl[OFL + nb * 64 + lane], sl[OFL + NB * 64 + nb * 64 + lane], a, b);
+  for (int nb = 0; nb < NB; ++nb) {
+    float M = NEG_INF;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) acc[nb][db] = acc[nb][db] * a + *(const f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) * b;
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, smem[v * SH::MFMA_SLOT + OFL + nb * 64 + lane]);
+    const float Mu = (M == NEG_INF) ? 0.f : M;
+    float wv[4], L = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      wv[v] = exp2_fast(smem[v * SH::MFMA_SLOT + OFL + nb * 64 + lane] - Mu);
+      L += wv[v] * smem[v * SH::MFMA_SLOT + OFL + NB * 64 + nb * 64 + lane];
     }
-  };
-  if (w >= 2) put(smem + (w - 2) * SH::MFMA_SLOT);
-  __syncthreads();
-  if (w < 2) take(smem + w * SH::MFMA_SLOT);
-  __syncthreads();
-  if (w == 1) put(smem);
-  __syncthreads();
-  if (w == 0) {
-    take(smem);
-    const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+    const int64_t rec = rec0 + nb * 16 + r16;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const int64_t rec = rec0 + nb * 16 + r16;
+    for (int x = 0; x < DBW; ++x) {
+      const int db = w * DBW + x;
+      f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int db = 0; db < DB; ++db) *(f32x4*)(a.ws_o + rec * D + db * 16 + q4 * 4) = acc[nb][db];
-      if (q4 == 0) {
-        a.ws_ml[rec * 2 + 0] = mrow[nb];
-        a.ws_ml[rec * 2 + 1] = lrow[nb];
-      }
+      for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * SH::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) st_coherent(a.ws_o + rec * D + db * 16 + q4 * 4 + e, acc4[e]);
+    }
+    if (w == 0 && q4 == 0) {
+      st_coherent(a.ws_ml + rec * 2 + 0, M);
+      st_coherent(a.ws_ml + rec * 2 + 1, L);
     }
   }
 }
@@ -481,111 +595,142 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   const int t0 = c * a.split, t1 = min(t0 + a.split, len);
   const int sub = a.split / 4;
   const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
+  // Page indices of this wavefront's range (lane i: the i-th 16-token group) and
+  // the query rows, loaded together.
+  const int npg = (wt1 - wt0 + kPageTokens - 1) / kPageTokens;
+  const int32_t* ptab = a.page_table + (int64_t)s * a.pages_per_slot + (wt0 >> 4);
+  const int pages = lane < npg ? ptab[lane] : 0;
   u32x4 q[HPK];
 #pragma unroll
   for (int r = 0; r < HPK; ++r)
     q[r] = *((const u32x4*)((const char*)a.q + ((int64_t)s * a.Hq + g * HPK + r) * SH::ROWB) + ch);
+  // The newest token (position len-1) comes from the caller's rows: the wave
+  // whose range holds it loads it up front, folds it in after the stored
+  // tokens, and stores it into its page.
+  const int last = len - 1;
+  const bool has_new = last >= wt0 && last < wt1;
   const int64_t newrow = ((int64_t)s * a.Hkv + g) * SH::ROWB;
-  SuffixAddr<SH> ad{(const char*)a.pool, a.page_table + (int64_t)s * a.pages_per_slot,
-                    (const char*)a.knew + newrow, (const char*)a.vnew + newrow, len - 1, a.Hkv, g};
+  u32x4 knew = u32x4{0, 0, 0, 0}, vnew = u32x4{0, 0, 0, 0};
+  if (has_new) {
+    knew = *((const u32x4*)((const char*)a.knew + newrow) + ch);
+    vnew = *((const u32x4*)((const char*)a.vnew + newrow) + ch);
+  }
+  SuffixAddr<SH> ad{(const char*)a.pool, pages, a.Hkv, g};
   float m[HPK], l[HPK], o[HPK][SH::EPL];
-  wave_partial<SH, HPK>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
+  wave_partial<SH, HPK>(ad, wt0, has_new ? last : wt1, q, a.scale_log2, m, l, o);
+  if (has_new) {
+    fold_token<SH, HPK>(knew, vnew, q, a.scale_log2, m, l, o);
+    if (lane < SH::LPT) {
+      char* row = (char*)a.pool + (int64_t)(sp.cur_page * a.Hkv + g) * 2 * SH::PAGEB + (last & 15) * SH::ROWB;
+      *((u32x4*)row + ch) = knew;
+      *((u32x4*)(row + SH::PAGEB) + ch) = vnew;
+    }
+  }
+  wave_combine_groups<SH, HPK>(m, l, o);
   const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.suffix_chunks_max + c) * a.Hkv + g) * HPK;
   block_store_partial<SH, HPK>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
 
-  if (t1 == len) {  // append this step's K/V at position len-1
+  if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
     const int pos = len - 1;
-    const int tid = threadIdx.x;
-    if (tid < 2 * SH::LPT) {
-      const int kind = tid / SH::LPT, cc = tid % SH::LPT;
-      const u32x4* src = (const u32x4*)((const char*)(kind ? a.vnew : a.knew) + newrow) + cc;
-      char* dst = (char*)a.pool + ((int64_t)(sp.cur_page * a.Hkv + g) * 2 + kind) * SH::PAGEB + (pos & 15) * SH::ROWB;
-      *((u32x4*)dst + cc) = *src;
-    }
-    if (g == 0 && tid == 0) {
-      a.page_table[(int64_t)s * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
-      if (a.count_tokens) {
-        const int p = s / a.m;
-        a.tokens[p * a.G + sp.sample] += 1;
-      }
-    }
+    a.page_table[(int64_t)s * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
+    if (a.count_tokens)
+      __hip_atomic_fetch_add(&a.tokens[(s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
 // ----------------------------------------------------------------------------
-// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. g*hpk+hpk-1.
+// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. +hpk-1.
+// Partial c < nP is prefix chunk c, then the response chunks.  Lane c holds
+// partial c's (m, l) (and c+64's), so the maximum and the normaliser take one
+// load round and a wavefront reduction; the weighted sum of outputs streams
+// the partial rows with all loads of a round independent.  The output is cut
+// into groups of 64 consecutive elements of one row, dealt to the wavefronts.
 // ----------------------------------------------------------------------------
 template <class SH>
-__device__ void merge_slot(const StepArgs& a, int s, int g) {
+__device__ void merge_outputs(const StepArgs& a, int s, int g) {
   constexpr int D = SH::D, HPK = SH::HPK;
+  static_assert(D % 64 == 0, "output groups");
+  constexpr int NGROUP = HPK * D / 64;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int p = s / a.m, si = s - p * a.m;
   const int nP = a.prompt[p].nchunks;
-  const int nS = (a.slot[s].len + a.split - 1) / a.split;
-  const int64_t pbase = ((int64_t)p * a.prefix_chunks_max * a.Hkv + g) * SH::PR;  // + c*Hkv*PR + row
+  const int n = nP + (a.slot[s].len + a.split - 1) / a.split;
+  const int64_t pbase = ((int64_t)p * a.prefix_chunks_max * a.Hkv + g) * SH::PR + si * HPK;
   const int64_t pstride = (int64_t)a.Hkv * SH::PR;
   const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
   const int64_t sstride = (int64_t)a.Hkv * HPK;
-  for (int idx = threadIdx.x; idx < HPK * D; idx += kBlockThreads) {
-    const int j = idx / D, d = idx - j * D;
-    const int64_t prow = pbase + si * HPK + j, srow = sbase + j;
-    float M = NEG_INF;
-    for (int c = 0; c < nP; ++c) M = fmaxf(M, a.ws_ml[(prow + c * pstride) * 2]);
-    for (int c = 0; c < nS; ++c) M = fmaxf(M, a.ws_ml[(srow + c * sstride) * 2]);
-    float L = 0.f, O = 0.f;
-    for (int c = 0; c < nP; ++c) {
-      const int64_t rec = prow + c * pstride;
-      const float wgt = exp2_fast(a.ws_ml[rec * 2] - M);
-      L += wgt * a.ws_ml[rec * 2 + 1];
-      O += wgt * a.ws_o[rec * D + d];
-    }
-    for (int c = 0; c < nS; ++c) {
-      const int64_t rec = srow + c * sstride;
-      const float wgt = exp2_fast(a.ws_ml[rec * 2] - M);
-      L += wgt * a.ws_ml[rec * 2 + 1];
-      O += wgt * a.ws_o[rec * D + d];
-    }
-    a.o[((int64_t)s * a.Hq + g * HPK + j) * D + d] = O / L;
-  }
-}
+  auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + c * pstride : sbase + (c - nP) * sstride) + j; };
 
-// Count this block's arrival at each listed live slot (first_slot .. +nslots-1)
-// for KV head g; the block that completes a slot's set of partials merges it.
-template <class SH>
-__device__ void arrive_and_merge(const StepArgs& a, int g, int first_slot, int nslots, unsigned long long* flag) {
-  __threadfence();  // release this block's partials
-  __syncthreads();
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    bool last = false;
-    if (lane < nslots) {
-      const int s = first_slot + lane;
-      const int len = a.slot[s].len;
-      if (len > 0) {
-        const int old = atomicAdd(&a.counters[s * a.Hkv + g], 1);
-        last = (old == a.slot[s].n_expect - 1);
+  for (int e = w; e < NGROUP; e += 4) {
+    const int j = (e * 64) / D, d = (e * 64) % D + lane;
+    float mm[2], ll[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int c = lane + 64 * k;
+      mm[k] = c < n ? ld_coherent(a.ws_ml + rec(c, j) * 2) : NEG_INF;
+      ll[k] = c < n ? ld_coherent(a.ws_ml + rec(c, j) * 2 + 1) : 0.f;
+    }
+    const float M = wave_max(fmaxf(mm[0], mm[1]));
+    const float w0 = exp2_fast(mm[0] - M), w1 = exp2_fast(mm[1] - M);
+    const float inv = 1.f / wave_sum(w0 * ll[0] + w1 * ll[1]);
+    float acc = 0.f;
+    constexpr int CU = 8;  // partials per round, all loads issued before use
+    for (int c0 = 0; c0 < n; c0 += CU) {
+      float v[CU];
+#pragma unroll
+      for (int u = 0; u < CU; ++u) v[u] = c0 + u < n ? ld_coherent(a.ws_o + rec(c0 + u, j) * D + d) : 0.f;
+#pragma unroll
+      for (int u = 0; u < CU; ++u) {
+        const int c = c0 + u;
+        if (c >= n) break;
+        acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c < 64 ? w0 : w1), c & 63)) * v[u];
       }
     }
-    const unsigned long long mk = __ballot(last);
-    if (lane == 0) *flag = mk;
-  }
-  __syncthreads();
-  unsigned long long mk = *flag;
-  if (mk) {
-    __threadfence();  // acquire the other blocks' partials
-    while (mk) {
-      const int b = __ffsll((long long)mk) - 1;
-      mk &= mk - 1;
-      const int s = first_slot + b;
-      merge_slot<SH>(a, s, g);
-      if (threadIdx.x == 0) a.counters[s * a.Hkv + g] = 0;
-    }
+    a.o[((int64_t)s * a.Hq + g * HPK + j) * D + d] = acc * inv;
   }
 }
 
+// A producer block has stored its partial: count it at each listed live slot
+// (first_slot .. +nslots-1) for KV head g.
+__device__ __forceinline__ void arrive(const StepArgs& a, int g, int first_slot, int nslots) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
+  __syncthreads();                // ... and so have every thread's
+  if (threadIdx.x < nslots) {
+    const int s = first_slot + threadIdx.x;
+    if (a.slot[s].len > 0)
+      __hip_atomic_fetch_add(&a.counters[s * a.Hkv + g], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Merge block of (slot s, KV head g): wait until all of its producers have
+// arrived (bounded), merge, and re-arm the counter for the next launch.
 template <class SH>
-__global__ __launch_bounds__(kBlockThreads) void decode_kernel(const StepArgs a) {
-  __shared__ __attribute__((aligned(16))) float smem[SH::SMEM];
-  __shared__ unsigned long long flag;
+__device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag) {
+  int32_t* ctr = &a.counters[s * a.Hkv + g];
+  if (threadIdx.x == 0) {
+    const int need = a.slot[s].n_expect;
+    int spins = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need && spins < kMergeSpins) {
+      __builtin_amdgcn_s_sleep(2);
+      ++spins;
+    }
+    *flag = spins < kMergeSpins;
+  }
+  __syncthreads();
+  if (!*flag) {
+    if (threadIdx.x == 0) __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
+    for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = __builtin_nanf("");
+    return;
+  }
+  merge_outputs<SH>(a, s, g);
+  __syncthreads();
+  if (threadIdx.x == 0) *ctr = 0;
+}
+
+template <class SH>
+__device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, unsigned long long* flagp) {
   const int item = blockIdx.x / a.Hkv;
   const int g = blockIdx.x - item * a.Hkv;
   if (item < a.n_prefix_items) {
@@ -597,10 +742,10 @@ __global__ __launch_bounds__(kBlockThreads) void decode_kernel(const StepArgs a)
       prefix_mfma<SH>(a, p, c, g, smem);
     else
       prefix_wave<SH>(a, p, c, g, smem);
-    arrive_and_merge<SH>(a, g, p * a.m, a.m, &flag);
+    arrive(a, g, p * a.m, a.m);
     return;
   }
-  const int it = item - a.n_prefix_items;
+  int it = item - a.n_prefix_items;
   if (it < a.n_suffix_items) {
     const int lane = threadIdx.x & 63;
     bool hit = false;
@@ -612,13 +757,37 @@ __global__ __launch_bounds__(kBlockThreads) void decode_kernel(const StepArgs a)
     if (s < 0) return;  // unreachable with a consistent plan
     const int c = it - a.slot[s].item_begin;
     suffix_chunk<SH>(a, s, c, g, smem);
-    arrive_and_merge<SH>(a, g, s, 1, &flag);
+    arrive(a, g, s, 1);
     return;
   }
-  const int z = it - a.n_suffix_items;
-  const int s = a.zero_slot[z];
-  float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
-  for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = 0.f;
+  it -= a.n_suffix_items;
+  if (it < a.n_zero_items) {
+    const int s = a.zero_slot[it];
+    float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
+    for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = 0.f;
+    return;
+  }
+  it -= a.n_zero_items;
+  merge_block<SH>(a, a.live_slot[it], g, flagp);
+}
+
+// Timing mode (a.clock_start != null): every block folds its start and end
+// time (device wall clock) into one of this launch's start / end slots.
+template <class SH>
+__global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(const StepArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[SH::SMEM];
+  __shared__ unsigned long long flag;
+  const int cs = blockIdx.x % kClockSlots;
+  if (a.clock_start && threadIdx.x == 0)
+    __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  decode_block<SH>(a, smem, &flag);
+  if (a.clock_start) {
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_max(a.clock_end + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // ----------------------------------------------------------------------------

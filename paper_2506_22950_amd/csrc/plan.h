@@ -13,10 +13,19 @@ constexpr int kMaxPrompts = 16;
 constexpr int kPageTokens = 16;    // tokens per response page
 constexpr int kBlockThreads = 256; // 4 wavefronts of 64
 constexpr int kMfmaBlock = 32;     // prefix tokens per MFMA block
+constexpr int kMfmaPrefixSplit = 4 * kMfmaBlock;  // MFMA prefix chunk: one block per wavefront
+constexpr int kMaxPartials = 128;  // prefix + response chunks merged for one slot
+constexpr int kMaxSplit = 4096;    // split-K chunk length limit (a wavefront covers <= 64 pages)
 
-// Work item kinds, in grid order: prefix chunks, response chunks, idle slots.
-// Grid x = item * Hkv + kv_head, so with 8 KV heads each head's items stay on
-// one XCD (work-groups are dealt round-robin over the 8 XCDs).
+constexpr int kMergeSpins = 1 << 20;
+constexpr int kClockSlots = 64;  // bound on a merge block's wait for its producers
+
+// Work item kinds, in grid order: prefix chunks, response chunks, idle slots,
+// then one merge item per live slot.  Grid x = item * Hkv + kv_head, so with 8
+// KV heads each head's items stay on one XCD (work-groups are dealt
+// round-robin over the 8 XCDs).  Merge items come last so that every XCD has
+// dispatched all of its producer work-groups before any merge work-group,
+// whose only wait is for producers to finish.
 
 struct SlotPlan {
   int32_t len;         // response length after this step's append; 0 = idle
@@ -48,21 +57,29 @@ struct StepArgs {
   float* ws_ml;        // partial (max, sum) [..., 2]
   int32_t* counters;   // [S, Hkv] arrivals per (slot, kv head); the merging block resets it
   int32_t* tokens;     // [num_prompts, G] per-sample token counters
+  int32_t* status;     // device status word: nonzero after a merge wait hit its bound
+  // Timing mode (else null): kClockSlots start/end slots of this launch; block b
+  // folds its start into min slot b % kClockSlots and its end into max slot
+  // b % kClockSlots (spread so the atomics do not queue on one address).
+  unsigned long long* clock_start;
+  unsigned long long* clock_end;
   // geometry
   int32_t S, m, G, Hq, Hkv, prefix_rows;  // prefix_rows = m * hpk (real rows)
   int32_t max_prompt_len;     // prefix store row capacity (multiple of 32)
   int32_t pages_per_slot;
-  int32_t split;              // chunk length in tokens (prefix and response)
-  int32_t prefix_chunks_max;  // ceil(max_prompt_len / split)
+  int32_t split;              // response chunk length in tokens
+  int32_t prefix_split;       // prefix chunk length in tokens
+  int32_t prefix_chunks_max;  // ceil(max_prompt_len / prefix_split)
   int32_t suffix_chunks_max;  // ceil(max_suffix_len / split)
   int32_t count_tokens;       // 1 on layer 0
   float scale_log2;           // softmax scale * log2(e)
   // this step
-  int32_t n_prefix_items, n_suffix_items, n_zero_items;
+  int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;
   int32_t num_prompts;
   PromptPlan prompt[kMaxPrompts];
   SlotPlan slot[kMaxSlots];
   int8_t zero_slot[kMaxSlots];
+  int8_t live_slot[kMaxSlots];
 };
 
 }  // namespace infs

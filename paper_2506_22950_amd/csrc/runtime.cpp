@@ -25,13 +25,18 @@ static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must fit 4 KiB");
 namespace {
 thread_local std::string g_thread_error = "no error";
 
+// Timing mode: each decode launch folds its blocks' device wall-clock start
+// and end times into one {min start, max end} pair of a device array; a HIP
+// event pair brackets the whole timed region on the context's stream.
 struct Timing {
   bool on = false;
-  std::vector<hipEvent_t> start, stop;
-  std::vector<bool> pending;
-  size_t next = 0;
-  double ms = 0.0;
+  unsigned long long* clocks = nullptr;  // [capacity][kClockSlots] starts, then the same for ends
+  int64_t capacity = 0;
+  int64_t used = 0;                      // pairs written since the last harvest
+  double kernel_ms = 0.0;
   int64_t launches = 0;
+  hipEvent_t region[2] = {nullptr, nullptr};
+  double ticks_per_ms = 0.0;
 };
 }  // namespace
 
@@ -41,7 +46,7 @@ struct infs_ctx {
   hipStream_t stream = nullptr;
   KernelKey key{};
   int S = 0, m = 0, G = 0, hpk = 0, D = 0, Hkv = 0, Hq = 0, L = 0, NP = 0;
-  int pmax_pad = 0, split = 0, pages_per_slot = 0, num_pages = 0, pcmax = 0, scmax = 0;
+  int pmax_pad = 0, split = 0, prefix_split = 0, pages_per_slot = 0, num_pages = 0, pcmax = 0, scmax = 0;
   size_t es = 0;
   size_t prefix_layer_bytes = 0, pool_layer_bytes = 0;
   int64_t ws_records = 0;
@@ -53,6 +58,7 @@ struct infs_ctx {
   float* ws_ml = nullptr;
   int32_t* counters = nullptr;
   int32_t* tokens = nullptr;
+  int32_t* status = nullptr;
   // host state
   std::vector<int32_t> plen;                       // per prompt, -1 before its first prefill
   std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
@@ -117,6 +123,7 @@ void free_device(infs_ctx* c) {
   hipFree(c->ws_ml);
   hipFree(c->counters);
   hipFree(c->tokens);
+  hipFree(c->status);
 }
 
 void reset_host(infs_ctx* c) {
@@ -161,14 +168,14 @@ infs_status open_step(infs_ctx* c) {
   for (int p = 0; p < c->NP; ++p) {
     infs::PromptPlan& pp = a.prompt[p];
     pp.plen = std::max(c->plen[p], 0);
-    pp.nchunks = live[p] > 0 ? ceil_div(pp.plen, c->split) : 0;
+    pp.nchunks = live[p] > 0 ? ceil_div(pp.plen, c->prefix_split) : 0;
     pp.item_begin = items;
     items += pp.nchunks;
     if (live[p] > 0) bytes += 2.0 * pp.plen * kvrow;
   }
   a.n_prefix_items = items;
   items = 0;
-  int zeros = 0;
+  int zeros = 0, lives = 0;
   for (int s = 0; s < c->S; ++s) {
     infs::SlotPlan& sp = a.slot[s];
     sp = infs::SlotPlan{};
@@ -183,6 +190,7 @@ infs_status open_step(infs_ctx* c) {
       c->slot_pages[s].push_back(c->free_pages.top());
       c->free_pages.pop();
     }
+    a.live_slot[lives++] = (int8_t)s;
     sp.len = len;
     sp.item_begin = items;
     sp.cur_page = c->slot_pages[s][pos / infs::kPageTokens];
@@ -196,7 +204,8 @@ infs_status open_step(infs_ctx* c) {
   }
   a.n_suffix_items = items;
   a.n_zero_items = zeros;
-  c->grid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items) * c->Hkv;
+  a.n_merge_items = lives;
+  c->grid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items + a.n_merge_items) * c->Hkv;
   c->step_bytes = bytes;
   c->step_flops = flops;
   c->step_open = true;
@@ -205,27 +214,63 @@ infs_status open_step(infs_ctx* c) {
   return INFS_OK;
 }
 
+// Start times to all ones (so the first block's minimum wins), end times to 0.
+infs_status arm_clocks(infs_ctx* c) {
+  Timing& t = c->timing;
+  const size_t n = (size_t)t.capacity * infs::kClockSlots;
+  HIP_TRY(c, hipMemsetAsync(t.clocks, 0xFF, sizeof(unsigned long long) * n, c->stream));
+  HIP_TRY(c, hipMemsetAsync(t.clocks + n, 0, sizeof(unsigned long long) * n, c->stream));
+  return INFS_OK;
+}
+
+// Add up the durations of the launches timed so far and re-arm the arrays.
+infs_status harvest_clocks(infs_ctx* c) {
+  Timing& t = c->timing;
+  if (t.used > 0) {
+    const size_t n = (size_t)t.capacity * infs::kClockSlots;
+    std::vector<unsigned long long> h(2 * n);
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    HIP_TRY(c, hipMemcpy(h.data(), t.clocks, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    for (int64_t i = 0; i < t.used; ++i) {
+      unsigned long long a = ~0ull, b = 0;
+      for (int k = 0; k < infs::kClockSlots; ++k) {
+        const size_t x = (size_t)i * infs::kClockSlots + k;
+        if (h[n + x] == 0) continue;  // slot not reached by any block
+        a = std::min(a, h[x]);
+        b = std::max(b, h[n + x]);
+      }
+      if (b > a) t.kernel_ms += (double)(b - a) / t.ticks_per_ms;
+    }
+    t.launches += t.used;
+    t.used = 0;
+  }
+  return arm_clocks(c);
+}
+
+// After a synchronisation: report a merge block that stopped waiting.
+infs_status check_status(infs_ctx* c) {
+  int32_t st = 0;
+  HIP_TRY(c, hipMemcpy(&st, c->status, sizeof st, hipMemcpyDeviceToHost));
+  if (st != 0) {
+    c->dead = true;
+    return fail(c, INFS_E_DEVICE, "a merge work-group gave up waiting for its producers; outputs are invalid");
+  }
+  return INFS_OK;
+}
+
 infs_status timed_launch(infs_ctx* c) {
   Timing& t = c->timing;
-  size_t slot = 0;
+  c->plan.clock_start = c->plan.clock_end = nullptr;
   if (t.on) {
-    slot = t.next;
-    t.next = (t.next + 1) % t.start.size();
-    if (t.pending[slot]) {
-      HIP_TRY(c, hipEventSynchronize(t.stop[slot]));
-      float ms = 0.f;
-      HIP_TRY(c, hipEventElapsedTime(&ms, t.start[slot], t.stop[slot]));
-      t.ms += ms;
-      ++t.launches;
-      t.pending[slot] = false;
+    if (t.used == t.capacity) {
+      infs_status st = harvest_clocks(c);
+      if (st != INFS_OK) return st;
     }
-    HIP_TRY(c, hipEventRecord(t.start[slot], c->stream));
+    c->plan.clock_start = t.clocks + (size_t)t.used * infs::kClockSlots;
+    c->plan.clock_end = t.clocks + ((size_t)t.capacity + t.used) * infs::kClockSlots;
+    ++t.used;
   }
   HIP_TRY(c, infs::launch_decode(c->key, c->plan, c->grid, c->stream));
-  if (t.on) {
-    HIP_TRY(c, hipEventRecord(t.stop[slot], c->stream));
-    t.pending[slot] = true;
-  }
   return INFS_OK;
 }
 
@@ -258,8 +303,8 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     return fail(nullptr, INFS_E_ARG, "max_suffix_len must be in [1, 2^20]");
   if (k.page_tokens != 0 && k.page_tokens != infs::kPageTokens)
     return fail(nullptr, INFS_E_ARG, "page_tokens must be 0 or %d", infs::kPageTokens);
-  if (k.split_tokens < 0 || k.split_tokens % 128 || k.split_tokens > (1 << 16))
-    return fail(nullptr, INFS_E_ARG, "split_tokens must be 0 or a multiple of 128 up to 65536");
+  if (k.split_tokens < 0 || k.split_tokens % 128 || k.split_tokens > infs::kMaxSplit)
+    return fail(nullptr, INFS_E_ARG, "split_tokens must be 0 or a multiple of 128 up to %d", infs::kMaxSplit);
   if (k.num_pages < 0) return fail(nullptr, INFS_E_ARG, "num_pages must be >= 0");
   if (k.dtype != INFS_F32 && k.dtype != INFS_BF16) return fail(nullptr, INFS_E_ARG, "dtype must be INFS_F32 or INFS_BF16");
   if (!(k.scale >= 0.f) || !std::isfinite(k.scale)) return fail(nullptr, INFS_E_ARG, "scale must be finite and >= 0");
@@ -272,7 +317,15 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
                 "no kernel for dtype=%s head_dim=%d heads_per_kv=%d prefix rows=%d (bf16 supports up to 64 rows, "
                 "fp32 up to 16)",
                 k.dtype == INFS_BF16 ? "bf16" : "f32", k.head_dim, hpk, k.slots_per_prompt * hpk);
-
+  {
+    const int split = k.split_tokens ? k.split_tokens : 256;
+    const int psplit = key.mfma ? infs::kMfmaPrefixSplit : split;
+    const int parts = (k.max_prompt_len + psplit - 1) / psplit + (k.max_suffix_len + split - 1) / split;
+    if (parts > infs::kMaxPartials)
+      return fail(nullptr, INFS_E_ARG,
+                  "max_prompt_len and max_suffix_len need %d split-K chunks per slot (limit %d): raise split_tokens",
+                  parts, infs::kMaxPartials);
+  }
   infs_ctx* c = new (std::nothrow) infs_ctx;
   if (!c) return fail(nullptr, INFS_E_NOMEM, "host allocation failed");
   c->cfg = k;
@@ -293,7 +346,8 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->pmax_pad = std::max(32, (k.max_prompt_len + 31) / 32 * 32);
   c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);
   c->num_pages = k.num_pages ? k.num_pages : c->S * c->pages_per_slot;
-  c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->split));
+  c->prefix_split = key.mfma ? infs::kMfmaPrefixSplit : c->split;
+  c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->prefix_split));
   c->scmax = ceil_div(k.max_suffix_len, c->split);
   c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->es;
   c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->es;
@@ -310,6 +364,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   a.max_prompt_len = c->pmax_pad;
   a.pages_per_slot = c->pages_per_slot;
   a.split = c->split;
+  a.prefix_split = c->prefix_split;
   a.prefix_chunks_max = c->pcmax;
   a.suffix_chunks_max = c->scmax;
   a.num_prompts = c->NP;
@@ -335,6 +390,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     if (st == INFS_OK) st = alloc((void**)&c->ws_ml, sizeof(float) * c->ws_records * 2, "workspace");
     if (st == INFS_OK) st = alloc((void**)&c->counters, sizeof(int32_t) * c->S * c->Hkv, "counters");
     if (st == INFS_OK) st = alloc((void**)&c->tokens, sizeof(int32_t) * c->NP * c->G, "token counters");
+    if (st == INFS_OK) st = alloc((void**)&c->status, sizeof(int32_t), "status word");
     if (st != INFS_OK) {
       free_device(c);
       delete c;
@@ -345,6 +401,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     a.ws_ml = c->ws_ml;
     a.counters = c->counters;
     a.tokens = c->tokens;
+    a.status = c->status;
   }
   *out = c;
   return INFS_OK;
@@ -354,8 +411,9 @@ void infs_destroy(infs_ctx* c) {
   if (!c) return;
   if (!c->dry) {
     hipStreamSynchronize(c->stream);
-    for (auto e : c->timing.start) hipEventDestroy(e);
-    for (auto e : c->timing.stop) hipEventDestroy(e);
+    if (c->timing.clocks) hipFree(c->timing.clocks);
+    for (auto e : c->timing.region)
+      if (e) hipEventDestroy(e);
     free_device(c);
   }
   delete c;
@@ -488,13 +546,14 @@ infs_status infs_sample_tokens(infs_ctx* c, int32_t prompt, int32_t* counts_host
   if (c->dry) return fail(c, INFS_E_STATE, "no device counters in a dry-run context");
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   HIP_TRY(c, hipMemcpy(counts_host, c->tokens + (size_t)prompt * c->G, sizeof(int32_t) * c->G, hipMemcpyDeviceToHost));
-  return INFS_OK;
+  return check_status(c);
 }
 
 infs_status infs_sync(infs_ctx* c) {
   CHECK_CTX(c);
-  if (!c->dry) HIP_TRY(c, hipStreamSynchronize(c->stream));
-  return INFS_OK;
+  if (c->dry) return INFS_OK;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return check_status(c);
 }
 
 infs_status infs_get_stats(const infs_ctx* c, infs_stats* out) {
@@ -507,39 +566,42 @@ infs_status infs_timing_begin(infs_ctx* c) {
   CHECK_CTX(c);
   if (c->dry) return fail(c, INFS_E_STATE, "no timing in a dry-run context");
   Timing& t = c->timing;
-  if (t.start.empty()) {
-    const size_t n = 1024;
-    t.start.resize(n);
-    t.stop.resize(n);
-    for (size_t i = 0; i < n; ++i) {
-      HIP_TRY(c, hipEventCreate(&t.start[i]));
-      HIP_TRY(c, hipEventCreate(&t.stop[i]));
-    }
+  if (!t.clocks) {
+    t.capacity = 1 << 13;
+    HIP_TRY(c, hipMalloc((void**)&t.clocks, sizeof(unsigned long long) * 2 * t.capacity * infs::kClockSlots));
+    HIP_TRY(c, hipEventCreate(&t.region[0]));
+    HIP_TRY(c, hipEventCreate(&t.region[1]));
+    int dev = 0, khz = 0;
+    HIP_TRY(c, hipGetDevice(&dev));
+    HIP_TRY(c, hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev));
+    if (khz <= 0) return fail(c, INFS_E_DEVICE, "device wall clock rate unavailable");
+    t.ticks_per_ms = (double)khz;
   }
-  t.pending.assign(t.start.size(), false);
-  t.next = 0;
-  t.ms = 0.0;
+  t.used = 0;
+  t.kernel_ms = 0.0;
   t.launches = 0;
+  infs_status st = arm_clocks(c);
+  if (st != INFS_OK) return st;
+  HIP_TRY(c, hipEventRecord(t.region[0], c->stream));
   t.on = true;
   return INFS_OK;
 }
 
-infs_status infs_timing_end(infs_ctx* c, double* kernel_ms, int64_t* launches) {
+infs_status infs_timing_end(infs_ctx* c, double* kernel_ms, double* region_ms, int64_t* launches) {
   CHECK_CTX(c);
   Timing& t = c->timing;
   if (!t.on) return fail(c, INFS_E_STATE, "timing not started");
-  if (!kernel_ms || !launches) return fail(c, INFS_E_ARG, "null output pointer");
-  HIP_TRY(c, hipStreamSynchronize(c->stream));
-  for (size_t i = 0; i < t.start.size(); ++i) {
-    if (!t.pending[i]) continue;
-    float ms = 0.f;
-    HIP_TRY(c, hipEventElapsedTime(&ms, t.start[i], t.stop[i]));
-    t.ms += ms;
-    ++t.launches;
-    t.pending[i] = false;
-  }
+  if (!kernel_ms || !region_ms || !launches) return fail(c, INFS_E_ARG, "null output pointer");
+  HIP_TRY(c, hipEventRecord(t.region[1], c->stream));
+  HIP_TRY(c, hipEventSynchronize(t.region[1]));
+  float ms = 0.f;
+  HIP_TRY(c, hipEventElapsedTime(&ms, t.region[0], t.region[1]));
+  infs_status st = harvest_clocks(c);
+  if (st != INFS_OK) return st;
   t.on = false;
-  *kernel_ms = t.ms;
+  c->plan.clock_start = c->plan.clock_end = nullptr;
+  *kernel_ms = t.kernel_ms;
+  *region_ms = ms;
   *launches = t.launches;
   return INFS_OK;
 }

@@ -82,7 +82,8 @@ def load():
         "infs_sync": (I32, [P]),
         "infs_get_stats": (I32, [P, ctypes.POINTER(Stats)]),
         "infs_timing_begin": (I32, [P]),
-        "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]),
+        "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(I64)]),
         "infs_last_error": (ctypes.c_char_p, [P]),
         "infs_sched_create": (I32, [I32, I32, I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(P)]),
         "infs_sched_next": (I32, [P, I32, ctypes.POINTER(I64)]),
@@ -192,9 +193,10 @@ class Context:
         self._call(load().infs_timing_begin)
 
     def timing_end(self):
-        ms, n = ctypes.c_double(), ctypes.c_int64()
-        self._call(load().infs_timing_end, ctypes.byref(ms), ctypes.byref(n))
-        return ms.value, n.value
+        """(summed kernel ms, region ms from HIP events, launches)."""
+        ms, region, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+        self._call(load().infs_timing_end, ctypes.byref(ms), ctypes.byref(region), ctypes.byref(n))
+        return ms.value, region.value, n.value
 
     @property
     def last_error(self):
