@@ -24,11 +24,120 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
+COPY_CAL_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_traffic_{workload}.txt")
+KERNEL_SOURCES = ("paper_2506_22950_amd/csrc/kernels.hip", "paper_2506_22950_amd/csrc/kernels.h",
+                  "paper_2506_22950_amd/csrc/plan.h")
 METRIC = "generated tokens/sec per group decode + achieved HBM TB/s vs peak, 1 MI355X"
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def read_traffic(workload):
+    """HBM bytes per decode launch from the committed counter summary of this
+    workload, or None when there is none or the kernel source has changed since."""
+    path = TRAFFIC_FILE.format(workload=workload)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for ln in fh:
+            if "=" in ln and not ln.startswith("#"):
+                k, v = ln.split("=", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+def copy_calibration(torch):
+    """Three device-to-device copies of COPY_CAL_BYTES: the plain copy kernel whose
+    FETCH_SIZE / WRITE_SIZE readings scale the decode kernel's."""
+    src = torch.empty(COPY_CAL_BYTES, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
+def _pmc_rows(path, counter):
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {path}")
+    rows = []
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    rows.append(r)
+    return rows
+
+
+def summarize_pmc(workload, fetch_dir, write_dir):
+    """Text summary of two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of
+    `bench.py --steps 1 --warmup 0 --no-kernel-timing --no-cpu-baseline --copy-calibration`:
+    per-launch HBM traffic of decode_kernel, each counter scaled by its reading for
+    the calibration copy of known size."""
+    from paper_2506_22950_amd.group import plan_steps
+    from workload import Workload, get_config
+
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _pmc_rows(d, counter)
+        dec = [float(r["Counter_Value"]) for r in rows if "decode_kernel" in r["Kernel_Name"]]
+        cps = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        gmax = max(int(r["Grid_Size"]) for r in cps)
+        cal = [float(r["Counter_Value"]) for r in cps if int(r["Grid_Size"]) == gmax]
+        if len(cal) < 3 or not dec:
+            raise SystemExit(f"{counter}: {len(cal)} calibration copies, {len(dec)} decode launches")
+        cal_kib = sorted(cal)[len(cal) // 2]
+        scale = COPY_CAL_BYTES / (cal_kib * 1024.0)
+        out[counter] = (len(dec), sum(dec) / len(dec), cal_kib, scale)
+    cfg = get_config(workload)
+    wl = Workload(cfg)
+    steplog = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
+    launches = len(steplog) * cfg.layers
+    alg = algorithmic_bytes(cfg, steplog) / launches
+    nf, fk, cf, sf = out["FETCH_SIZE"]
+    nw, wk, cw, sw = out["WRITE_SIZE"]
+    if nf != launches or nw != launches:
+        raise SystemExit(f"expected {launches} decode launches, got {nf} / {nw}")
+    fetch_b, write_b = fk * 1024.0 * sf, wk * 1024.0 * sw
+    lines = [
+        f"kernel_source_sha256 = {kernel_source_hash()}",
+        f"workload = {workload}",
+        f"decode_launches = {launches}",
+        f"copy_bytes = {COPY_CAL_BYTES}",
+        f"copy_fetch_kib = {cf:.1f}",
+        f"copy_write_kib = {cw:.1f}",
+        f"fetch_scale = {sf:.4f}",
+        f"write_scale = {sw:.4f}",
+        f"decode_fetch_kib_per_launch = {fk:.1f}",
+        f"decode_write_kib_per_launch = {wk:.1f}",
+        f"fetch_bytes_per_launch = {fetch_b:.0f}",
+        f"write_bytes_per_launch = {write_b:.0f}",
+        f"traffic_bytes_per_launch = {fetch_b + write_b:.0f}",
+        f"alg_bytes_per_launch = {alg:.0f}",
+        f"traffic_over_alg = {(fetch_b + write_b) / alg:.3f}",
+    ]
+    return "\n".join(lines)
 
 
 def algorithmic_bytes(cfg, steplog):
@@ -167,7 +276,14 @@ def main():
     ap.add_argument("--split", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print the traffic summary of two rocprofv3 --pmc output folders and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(summarize_pmc(args.workload, *args.summarize_pmc))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
@@ -176,6 +292,8 @@ def main():
     import torch
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        copy_calibration(torch)
     b = Bench(args.workload, split=args.split)
 
     for w in range(args.warmup):
@@ -207,7 +325,7 @@ def main():
         per_launch = alg / n
         achieved = per_launch / (avg_us * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": read_traffic(args.workload),
                 "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
                 "alg_bytes_per_launch": round(per_launch),
                 "timing": "device wall clock, first block start to last block end, every launch of one group decode",

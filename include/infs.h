@@ -129,7 +129,7 @@ infs_status infs_reset(infs_ctx* ctx);
 
 /* Copy one prompt's prefill K and V for one layer into the shared-prefix store (Section 3.1:
    the prompt's KV cache is kept and shared by every micro group).
-   k_dev, v_dev: [prompt_len, Hkv, head_dim] row-major, context dtype.  prompt_len in
+   k_dev, v_dev: [prompt_len, Hkv, head_dim] row-major, context dtype, 16-byte aligned.  prompt_len in
    [0, max_prompt_len]; every layer of a prompt must use the same prompt_len.  Not allowed while
    a step is open (between the first decode_step of a step and end_step). */
 infs_status infs_prefill_shared(infs_ctx* ctx, int32_t prompt, int32_t layer, int32_t prompt_len,
@@ -148,7 +148,8 @@ infs_status infs_retire_slot(infs_ctx* ctx, int32_t slot);
    live slots append this step's K/V (position = current length) to their response, then attend
    over [prefix ; response]; idle slots' rows are ignored and their O rows are written as 0.
    q_dev: [S, Hq, d]; k_new_dev, v_new_dev: [S, Hkv, d] (context dtype); o_dev: [S, Hq, d] fp32,
-   with S = num_prompts * slots_per_prompt, slot-major.  Each layer must be decoded exactly once
+   with S = num_prompts * slots_per_prompt, slot-major; all four 16-byte aligned (E_ARG otherwise).
+   Each layer must be decoded exactly once
    per step.  E_STATE: layer already decoded in this step, or a live slot's prompt has no prefix
    for this layer.  E_CAPACITY: a response would pass max_suffix_len or the page pool is empty. */
 infs_status infs_decode_step(infs_ctx* ctx, int32_t layer, const void* q_dev, const void* k_new_dev,

@@ -148,6 +148,19 @@ __device__ __forceinline__ void st_coherent(float* p, float v) {
 __device__ __forceinline__ float ld_coherent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// 16-byte store into the partial-output workspace with the cache policy of
+// the agent-scope atomic store above (write through to the coherence point),
+// so that a lane's four consecutive floats leave as one write instead of
+// four partial-line writes.  The workspace is addressed by a raw buffer
+// resource over its whole size; byte_off must be below ws_o_bytes.
+constexpr int kCoherentPolicy = 16;  // sc1
+constexpr int kRawBufferWord3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t ws_rsrc(const StepArgs& a) {
+  return __builtin_amdgcn_make_buffer_rsrc(a.ws_o, 0, (int)a.ws_o_bytes, kRawBufferWord3);
+}
+__device__ __forceinline__ void st_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kCoherentPolicy);
+}
 
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
@@ -551,6 +564,7 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
   put(smem + w * SH::MFMA_SLOT);
   __syncthreads();
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
   constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
   static_assert(DB % 4 == 0, "head_dim blocks per wave");
 #pragma unroll
@@ -572,8 +586,7 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
       f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * SH::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) st_coherent(a.ws_o + rec * D + db * 16 + q4 * 4 + e, acc4[e]);
+      st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
     }
     if (w == 0 && q4 == 0) {
       st_coherent(a.ws_ml + rec * 2 + 0, M);
@@ -639,18 +652,29 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
 }
 
 // ----------------------------------------------------------------------------
-// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. +hpk-1.
-// Partial c < nP is prefix chunk c, then the response chunks.  Lane c holds
-// partial c's (m, l) (and c+64's), so the maximum and the normaliser take one
-// load round and a wavefront reduction; the weighted sum of outputs streams
-// the partial rows with all loads of a round independent.  The output is cut
-// into groups of 64 consecutive elements of one row, dealt to the wavefronts.
+// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. +hpk-1
+// (the log-sum-exp combination of split-K partial softmaxes).  Partial c < nP
+// is prefix chunk c, then the response chunks.  The hpk*d outputs are cut into
+// 4-float vectors, one per lane (MV vectors per lane when they exceed 64); the
+// partials are dealt round-robin to the four wavefronts, each of which loads a
+// round of MCU partials at once (16-byte loads, no load waits on another) and
+// folds them into a running (max, sum, output); the four wavefronts' results
+// are then combined through LDS.
 // ----------------------------------------------------------------------------
 template <class SH>
-__device__ void merge_outputs(const StepArgs& a, int s, int g) {
-  constexpr int D = SH::D, HPK = SH::HPK;
-  static_assert(D % 64 == 0, "output groups");
-  constexpr int NGROUP = HPK * D / 64;
+struct MergeShape {
+  static constexpr int OPP = SH::HPK * SH::D;          // outputs per partial
+  static constexpr int NVEC = OPP / 4;                 // 4-float vectors per partial
+  static constexpr int MV = (NVEC + 63) / 64;          // vectors per lane
+  static constexpr int MCU = MV == 1 ? 8 : 4;          // partials per load round and wavefront
+  static constexpr int SMEM = 4 * 64 * MV * 8;         // per wave and lane vector: max, sum, 2 pad, 4 outputs
+  static_assert(SH::D % 4 == 0, "vectors");
+};
+
+template <class SH>
+__device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
+  using MS = MergeShape<SH>;
+  constexpr int D = SH::D, HPK = SH::HPK, MV = MS::MV, MCU = MS::MCU;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int p = s / a.m, si = s - p * a.m;
   const int nP = a.prompt[p].nchunks;
@@ -660,33 +684,77 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g) {
   const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
   const int64_t sstride = (int64_t)a.Hkv * HPK;
   auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + c * pstride : sbase + (c - nP) * sstride) + j; };
+  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
 
-  for (int e = w; e < NGROUP; e += 4) {
-    const int j = (e * 64) / D, d = (e * 64) % D + lane;
-    float mm[2], ll[2];
+  float M[MV], L[MV];
+  f32x4 O[MV];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int c = lane + 64 * k;
-      mm[k] = c < n ? ld_coherent(a.ws_ml + rec(c, j) * 2) : NEG_INF;
-      ll[k] = c < n ? ld_coherent(a.ws_ml + rec(c, j) * 2 + 1) : 0.f;
-    }
-    const float M = wave_max(fmaxf(mm[0], mm[1]));
-    const float w0 = exp2_fast(mm[0] - M), w1 = exp2_fast(mm[1] - M);
-    const float inv = 1.f / wave_sum(w0 * ll[0] + w1 * ll[1]);
-    float acc = 0.f;
-    constexpr int CU = 8;  // partials per round, all loads issued before use
-    for (int c0 = 0; c0 < n; c0 += CU) {
-      float v[CU];
+  for (int v = 0; v < MV; ++v) {
+    M[v] = NEG_INF;
+    L[v] = 0.f;
+    O[v] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int c0 = w; c0 < n; c0 += 4 * MCU) {
+    uint64_t ml[MCU][MV];
+    f32x4 ov[MCU][MV];
 #pragma unroll
-      for (int u = 0; u < CU; ++u) v[u] = c0 + u < n ? ld_coherent(a.ws_o + rec(c0 + u, j) * D + d) : 0.f;
+    for (int u = 0; u < MCU; ++u) {
+      const int c = c0 + 4 * u;
 #pragma unroll
-      for (int u = 0; u < CU; ++u) {
-        const int c = c0 + u;
-        if (c >= n) break;
-        acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(c < 64 ? w0 : w1), c & 63)) * v[u];
+      for (int v = 0; v < MV; ++v) {
+        const int x = (v * 64 + lane) * 4, j = x / D, d = x - j * D;
+        if (c < n && x < MS::OPP) {
+          const int64_t r = rec(c, j);
+          ml[u][v] = __hip_atomic_load((const uint64_t*)(a.ws_ml + r * 2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ov[u][v] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(wsr, (uint32_t)((r * D + d) * 4), 0, kCoherentPolicy));
+        } else {
+          ml[u][v] = (uint64_t)__float_as_uint(NEG_INF);
+          ov[u][v] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
       }
     }
-    a.o[((int64_t)s * a.Hq + g * HPK + j) * D + d] = acc * inv;
+#pragma unroll
+    for (int u = 0; u < MCU; ++u)
+#pragma unroll
+      for (int v = 0; v < MV; ++v) {
+        const float mc = __uint_as_float((uint32_t)ml[u][v]), lc = __uint_as_float((uint32_t)(ml[u][v] >> 32));
+        const float nm = fmaxf(M[v], mc);
+        const float base = nm == NEG_INF ? 0.f : nm;
+        const float al = exp2_fast(M[v] - base), be = mc == NEG_INF ? 0.f : exp2_fast(mc - base);
+        L[v] = L[v] * al + lc * be;
+        O[v] = O[v] * al + ov[u][v] * be;
+        M[v] = nm;
+      }
+  }
+#pragma unroll
+  for (int v = 0; v < MV; ++v) {
+    float* e = smem + ((w * MV + v) * 64 + lane) * 8;
+    e[0] = M[v];
+    e[1] = L[v];
+    *(f32x4*)(e + 4) = O[v];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < MS::NVEC; t += kBlockThreads) {
+    const int v = t >> 6, ln = t & 63;
+    float mw[4], mx = NEG_INF;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      mw[q] = smem[((q * MV + v) * 64 + ln) * 8];
+      mx = fmaxf(mx, mw[q]);
+    }
+    const float base = mx == NEG_INF ? 0.f : mx;
+    float Lt = 0.f;
+    f32x4 Ot = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float* e = smem + ((q * MV + v) * 64 + ln) * 8;
+      const float wq = mw[q] == NEG_INF ? 0.f : exp2_fast(mw[q] - base);
+      Lt += wq * e[1];
+      Ot += *(const f32x4*)(e + 4) * wq;
+    }
+    const int x = t * 4, j = x / D, d = x - j * D;
+    *(f32x4*)(a.o + ((int64_t)s * a.Hq + g * HPK + j) * D + d) = Ot * (1.f / Lt);
   }
 }
 
@@ -706,7 +774,7 @@ __device__ __forceinline__ void arrive(const StepArgs& a, int g, int first_slot,
 // Merge block of (slot s, KV head g): wait until all of its producers have
 // arrived (bounded), merge, and re-arm the counter for the next launch.
 template <class SH>
-__device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag) {
+__device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag, float* smem) {
   int32_t* ctr = &a.counters[s * a.Hkv + g];
   if (threadIdx.x == 0) {
     const int need = a.slot[s].n_expect;
@@ -724,7 +792,7 @@ __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long*
     for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = __builtin_nanf("");
     return;
   }
-  merge_outputs<SH>(a, s, g);
+  merge_outputs<SH>(a, s, g, smem);
   __syncthreads();
   if (threadIdx.x == 0) *ctr = 0;
 }
@@ -768,14 +836,15 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     return;
   }
   it -= a.n_zero_items;
-  merge_block<SH>(a, a.live_slot[it], g, flagp);
+  merge_block<SH>(a, a.live_slot[it], g, flagp, smem);
 }
 
 // Timing mode (a.clock_start != null): every block folds its start and end
 // time (device wall clock) into one of this launch's start / end slots.
 template <class SH>
 __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(const StepArgs a) {
-  __shared__ __attribute__((aligned(16))) float smem[SH::SMEM];
+  constexpr int SMEM = SH::SMEM > MergeShape<SH>::SMEM ? SH::SMEM : MergeShape<SH>::SMEM;
+  __shared__ __attribute__((aligned(16))) float smem[SMEM];
   __shared__ unsigned long long flag;
   const int cs = blockIdx.x % kClockSlots;
   if (a.clock_start && threadIdx.x == 0)

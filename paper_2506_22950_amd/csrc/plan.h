@@ -73,6 +73,7 @@ struct StepArgs {
   int32_t suffix_chunks_max;  // ceil(max_suffix_len / split)
   int32_t count_tokens;       // 1 on layer 0
   float scale_log2;           // softmax scale * log2(e)
+  uint32_t ws_o_bytes;        // size of ws_o (below 2^31)
   // this step
   int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;
   int32_t num_prompts;

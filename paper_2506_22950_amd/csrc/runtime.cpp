@@ -325,6 +325,13 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       return fail(nullptr, INFS_E_ARG,
                   "max_prompt_len and max_suffix_len need %d split-K chunks per slot (limit %d): raise split_tokens",
                   parts, infs::kMaxPartials);
+    const int64_t ws_bytes =
+        infs::workspace_records(key, k.num_prompts, k.num_kv_heads, std::max(1, (k.max_prompt_len + psplit - 1) / psplit),
+                                k.num_prompts * k.slots_per_prompt, (k.max_suffix_len + split - 1) / split) *
+        k.head_dim * (int64_t)sizeof(float);
+    if (ws_bytes >= (int64_t(1) << 31))
+      return fail(nullptr, INFS_E_ARG, "split-K workspace of %lld bytes exceeds 2 GiB: lower num_kv_heads or raise split_tokens",
+                  (long long)ws_bytes);
   }
   infs_ctx* c = new (std::nothrow) infs_ctx;
   if (!c) return fail(nullptr, INFS_E_NOMEM, "host allocation failed");
@@ -370,6 +377,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   a.num_prompts = c->NP;
   const float scale = k.scale > 0.f ? k.scale : 1.0f / std::sqrt((float)k.head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
+  a.ws_o_bytes = (uint32_t)(c->ws_records * c->D * sizeof(float));
 
   if (!c->dry) {
     auto alloc = [&](void** p, size_t bytes, const char* what) -> infs_status {
@@ -440,6 +448,8 @@ infs_status infs_prefill_shared(infs_ctx* c, int32_t prompt, int32_t layer, int3
     return fail(c, INFS_E_ARG, "prompt %d was prefilled with %d tokens in another layer", prompt, c->plen[prompt]);
   if (c->step_open) return fail(c, INFS_E_STATE, "prefill while a step is open");
   if (!c->dry && prompt_len > 0 && (!k_dev || !v_dev)) return fail(c, INFS_E_ARG, "null K/V pointer");
+  if (!c->dry && prompt_len > 0 && (((uintptr_t)k_dev | (uintptr_t)v_dev) & 15))
+    return fail(c, INFS_E_ARG, "K/V must be 16-byte aligned");
   if (!c->dry) {
     HIP_TRY(c, infs::launch_prefill(c->key, c->prefix + c->prefix_layer_bytes * layer, k_dev, v_dev, prompt,
                                     prompt_len, c->Hkv, c->pmax_pad, c->stream));
@@ -483,6 +493,8 @@ infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, cons
   CHECK_CTX(c);
   if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
   if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
+  if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
+    return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
   if (c->step_open && c->layer_done[layer])
     return fail(c, INFS_E_STATE, "layer %d already decoded in this step", layer);
   for (int p = 0; p < c->NP; ++p) {
