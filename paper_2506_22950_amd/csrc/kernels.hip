@@ -10,8 +10,9 @@
 //     below that, on wavefront dot products;
 //   * split-K attention over each live slot's private response (hpk rows per
 //     KV byte, wavefront dot products);
-//   * log-sum-exp merge: the last work-group to finish for a (slot, KV head)
-//     combines the partial softmaxes of all its chunks and writes O.
+//   * log-sum-exp merge: one work-group per live (slot, KV head), placed at
+//     the end of the grid, waits (bounded) until every chunk of that slot has
+//     published its partial, combines the partial softmaxes and writes O.
 // Idle slots get O = 0.
 //
 // A partial over a key set J is (M, L, O) with scores in log2 units
@@ -438,7 +439,8 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
 // online-softmax rescale needs no cross-lane transpose.  The P^T operand takes
 // the 8 probabilities a lane already holds; the contraction index (token) is
 // the same permutation on both operands, and the prefix store keeps V in that
-// order (see prefill_mfma_kernel).  Two blocks are loaded per round.
+// order (see prefill_mfma_kernel).  Each wavefront keeps one block in flight
+// (the accumulators of 32+ rows leave no registers for a second).
 // ----------------------------------------------------------------------------
 template <class SH>
 __device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const bf16x8 (&va)[SH::DB],
