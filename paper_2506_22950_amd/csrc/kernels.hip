@@ -491,6 +491,64 @@ __device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const 
   }
 }
 
+// Combine the four wavefronts' MFMA partials of one chunk (same rows, disjoint
+// token ranges) and store rows 0 .. nrows-1 as records rec0 + row.  Every
+// wavefront publishes its fragments to LDS; after one barrier each combines
+// the four for a quarter of the head dimension and stores it.
+template <class XS>
+__device__ void mfma_combine_store(const StepArgs& a, float* smem, f32x4 (&acc)[XS::NB][XS::DB],
+                                   float (&mrow)[XS::NB], float (&lrow)[XS::NB], int64_t rec0, int nrows) {
+  constexpr int NB = XS::NB, DB = XS::DB, D = XS::D;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    lrow[nb] += __shfl_xor(lrow[nb], 16);
+    lrow[nb] += __shfl_xor(lrow[nb], 32);
+  }
+  constexpr int OFL = NB * DB * 64 * 4;
+  {
+    float* sl = smem + w * XS::MFMA_SLOT;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
+      sl[OFL + nb * 64 + lane] = mrow[nb];
+      sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
+    }
+  }
+  __syncthreads();
+  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
+  constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
+  static_assert(DB % 4 == 0, "head_dim blocks per wave");
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    if (nb * 16 + r16 >= nrows) continue;
+    float M = NEG_INF;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) M = fmaxf(M, smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane]);
+    const float Mu = (M == NEG_INF) ? 0.f : M;
+    float wv[4], L = 0.f;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      wv[v] = exp2_fast(smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane] - Mu);
+      L += wv[v] * smem[v * XS::MFMA_SLOT + OFL + NB * 64 + nb * 64 + lane];
+    }
+    const int64_t rec = rec0 + nb * 16 + r16;
+#pragma unroll
+    for (int x = 0; x < DBW; ++x) {
+      const int db = w * DBW + x;
+      f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * XS::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
+      st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
+    }
+    if (w == 0 && q4 == 0) {
+      st_coherent(a.ws_ml + rec * 2 + 0, M);
+      st_coherent(a.ws_ml + rec * 2 + 1, L);
+    }
+  }
+}
+
 template <class SH>
 __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
   constexpr int D = SH::D, NB = SH::NB, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
@@ -544,57 +602,8 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
     for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
     mfma_block<SH>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
   }
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    lrow[nb] += __shfl_xor(lrow[nb], 16);
-    lrow[nb] += __shfl_xor(lrow[nb], 32);
-  }
-
-  // Tree-combine the four wavefronts through two LDS slots (lane-major fragments).
-  constexpr int OFL = NB * DB * 64 * 4;
-  auto put = [&](float* sl) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-      for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
-      sl[OFL + nb * 64 + lane] = mrow[nb];
-      sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
-    }
-  };
-  // All four wavefronts publish their partials; after one barrier each
-  // combines the four for a quarter of the head dimension and stores it.
-  put(smem + w * SH::MFMA_SLOT);
-  __syncthreads();
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
-  constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
-  static_assert(DB % 4 == 0, "head_dim blocks per wave");
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    float M = NEG_INF;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, smem[v * SH::MFMA_SLOT + OFL + nb * 64 + lane]);
-    const float Mu = (M == NEG_INF) ? 0.f : M;
-    float wv[4], L = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      wv[v] = exp2_fast(smem[v * SH::MFMA_SLOT + OFL + nb * 64 + lane] - Mu);
-      L += wv[v] * smem[v * SH::MFMA_SLOT + OFL + NB * 64 + nb * 64 + lane];
-    }
-    const int64_t rec = rec0 + nb * 16 + r16;
-#pragma unroll
-    for (int x = 0; x < DBW; ++x) {
-      const int db = w * DBW + x;
-      f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * SH::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
-      st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
-    }
-    if (w == 0 && q4 == 0) {
-      st_coherent(a.ws_ml + rec * 2 + 0, M);
-      st_coherent(a.ws_ml + rec * 2 + 1, L);
-    }
-  }
+  mfma_combine_store<SH>(a, smem, acc, mrow, lrow, rec0, SH::PR);
 }
 
 // ----------------------------------------------------------------------------
@@ -760,28 +769,37 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
   }
 }
 
-// A producer block has stored its partial: count it at each listed live slot
-// (first_slot .. +nslots-1) for KV head g.
-__device__ __forceinline__ void arrive(const StepArgs& a, int g, int first_slot, int nslots) {
+// A producer block has stored its partial: once every thread's stores have
+// completed, count one arrival on `ctr`.
+__device__ __forceinline__ void arrive(int32_t* ctr) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
   __syncthreads();                // ... and so have every thread's
-  if (threadIdx.x < nslots) {
-    const int s = first_slot + threadIdx.x;
-    if (a.slot[s].len > 0)
-      __hip_atomic_fetch_add(&a.counters[s * a.Hkv + g], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t* prefix_counter(const StepArgs& a, int p, int g) {
+  return a.counters + (int64_t)(p * a.Hkv + g) * kCounterStride;
+}
+__device__ __forceinline__ int32_t* suffix_counter(const StepArgs& a, int s, int g) {
+  return a.counters + (int64_t)((a.num_prompts + s) * a.Hkv + g) * kCounterStride;
+}
+// Counters wrap: `reached` compares by the sign of the difference.
+__device__ __forceinline__ bool reached(const int32_t* ctr, int32_t target) {
+  const int32_t v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return (int32_t)((uint32_t)v - (uint32_t)target) >= 0;
 }
 
-// Merge block of (slot s, KV head g): wait until all of its producers have
-// arrived (bounded), merge, and re-arm the counter for the next launch.
+// Merge block of (slot s, KV head g): wait until the prefix chunks of its
+// prompt and its own response chunks have all arrived (bounded), then merge.
 template <class SH>
 __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag, float* smem) {
-  int32_t* ctr = &a.counters[s * a.Hkv + g];
   if (threadIdx.x == 0) {
-    const int need = a.slot[s].n_expect;
+    const int p = s / a.m;
+    const int32_t* pc = prefix_counter(a, p, g);
+    const int32_t* sc = suffix_counter(a, s, g);
+    const int32_t pt = a.prompt[p].target, stg = a.slot[s].target;
     int spins = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need && spins < kMergeSpins) {
+    while (!(reached(sc, stg) && reached(pc, pt)) && spins < kMergeSpins) {
       __builtin_amdgcn_s_sleep(2);
       ++spins;
     }
@@ -795,8 +813,6 @@ __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long*
     return;
   }
   merge_outputs<SH>(a, s, g, smem);
-  __syncthreads();
-  if (threadIdx.x == 0) *ctr = 0;
 }
 
 template <class SH>
@@ -812,7 +828,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
       prefix_mfma<SH>(a, p, c, g, smem);
     else
       prefix_wave<SH>(a, p, c, g, smem);
-    arrive(a, g, p * a.m, a.m);
+    arrive(prefix_counter(a, p, g));
     return;
   }
   int it = item - a.n_prefix_items;
@@ -827,7 +843,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     if (s < 0) return;  // unreachable with a consistent plan
     const int c = it - a.slot[s].item_begin;
     suffix_chunk<SH>(a, s, c, g, smem);
-    arrive(a, g, s, 1);
+    arrive(suffix_counter(a, s, g));
     return;
   }
   it -= a.n_suffix_items;

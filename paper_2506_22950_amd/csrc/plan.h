@@ -18,6 +18,7 @@ constexpr int kMaxPartials = 128;  // prefix + response chunks merged for one sl
 constexpr int kMaxSplit = 4096;    // split-K chunk length limit (a wavefront covers <= 64 pages)
 
 constexpr int kMergeSpins = 1 << 20;
+constexpr int kCounterStride = 32;  // int32 per arrival counter: each counter has a 128-byte line of its own
 constexpr int kClockSlots = 64;  // bound on a merge block's wait for its producers
 
 // Work item kinds, in grid order: prefix chunks, response chunks, idle slots,
@@ -32,7 +33,7 @@ struct SlotPlan {
   int32_t item_begin;  // first response-chunk item of this slot
   int32_t cur_page;    // page holding position len-1 (where this step's K/V go)
   int32_t sample;      // sample id (token counters)
-  int32_t n_expect;    // partials merged for this slot: prefix chunks + response chunks
+  int32_t target;      // response-arrival counter value once this launch's chunks of the slot arrived
   int32_t pad_[3];
 };
 
@@ -40,7 +41,7 @@ struct PromptPlan {
   int32_t plen;        // prefix length
   int32_t nchunks;     // prefix chunks this step (0 when the prompt has no live slot)
   int32_t item_begin;  // first prefix item
-  int32_t pad_;
+  int32_t target;      // prefix-arrival counter value once this launch's prefix chunks arrived
 };
 
 struct StepArgs {
@@ -55,7 +56,9 @@ struct StepArgs {
   int32_t* page_table; // [S, pages_per_slot]
   float* ws_o;         // partial outputs   [..., d]
   float* ws_ml;        // partial (max, sum) [..., 2]
-  int32_t* counters;   // [S, Hkv] arrivals per (slot, kv head); the merging block resets it
+  int32_t* counters;   // arrival counters, kCounterStride apart: [num_prompts][Hkv] prefix chunks,
+                       // then [S][Hkv] response chunks.  They only grow (wrapping); each launch
+                       // carries the values they reach once its producers have all arrived.
   int32_t* tokens;     // [num_prompts, G] per-sample token counters
   int32_t* status;     // device status word: nonzero after a merge wait hit its bound
   // Timing mode (else null): kClockSlots start/end slots of this launch; block b

@@ -67,6 +67,9 @@ struct infs_ctx {
   std::vector<std::vector<int32_t>> slot_pages;    // host copy of each slot's page list
   std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_pages;
   std::vector<std::vector<uint8_t>> dispatched;    // [prompt][G]
+  // Arrivals each device counter has been sent so far (the same for every KV
+  // head): prefix counters per prompt, response counters per slot.
+  std::vector<uint32_t> prefix_arrivals, suffix_arrivals;
   bool step_open = false;
   std::vector<uint8_t> layer_done;
   int layers_done = 0;
@@ -126,6 +129,10 @@ void free_device(infs_ctx* c) {
   hipFree(c->status);
 }
 
+size_t counter_bytes(const infs_ctx* c) {
+  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->NP + c->S) * c->Hkv;
+}
+
 void reset_host(infs_ctx* c) {
   c->plen.assign(c->NP, -1);
   c->prefilled.assign(c->NP, std::vector<uint8_t>(c->L, 0));
@@ -135,6 +142,8 @@ void reset_host(infs_ctx* c) {
   c->free_pages = {};
   for (int i = 0; i < c->num_pages; ++i) c->free_pages.push(i);
   c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
+  c->prefix_arrivals.assign(c->NP, 0);
+  c->suffix_arrivals.assign(c->S, 0);
   c->step_open = false;
   c->layer_done.assign(c->L, 0);
   c->layers_done = 0;
@@ -196,7 +205,6 @@ infs_status open_step(infs_ctx* c) {
     sp.cur_page = c->slot_pages[s][pos / infs::kPageTokens];
     sp.sample = (int32_t)c->slot_sample[s];
     const int nch = ceil_div(len, c->split);
-    sp.n_expect = a.prompt[s / c->m].nchunks + nch;
     items += nch;
     const int P = a.prompt[s / c->m].plen;
     bytes += 2.0 * len * kvrow + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
@@ -258,7 +266,21 @@ infs_status check_status(infs_ctx* c) {
   return INFS_OK;
 }
 
+// Advance the arrival targets by this launch's producers.
+void set_targets(infs_ctx* c) {
+  StepArgs& a = c->plan;
+  for (int p = 0; p < c->NP; ++p) {
+    c->prefix_arrivals[p] += (uint32_t)a.prompt[p].nchunks;
+    a.prompt[p].target = (int32_t)c->prefix_arrivals[p];
+  }
+  for (int s = 0; s < c->S; ++s) {
+    if (a.slot[s].len > 0) c->suffix_arrivals[s] += (uint32_t)ceil_div(a.slot[s].len, c->split);
+    a.slot[s].target = (int32_t)c->suffix_arrivals[s];
+  }
+}
+
 infs_status timed_launch(infs_ctx* c) {
+  set_targets(c);
   Timing& t = c->timing;
   c->plan.clock_start = c->plan.clock_end = nullptr;
   if (t.on) {
@@ -396,7 +418,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     if (st == INFS_OK) st = alloc((void**)&c->page_table, sizeof(int32_t) * c->S * c->pages_per_slot, "page table");
     if (st == INFS_OK) st = alloc((void**)&c->ws_o, sizeof(float) * c->ws_records * c->D, "workspace");
     if (st == INFS_OK) st = alloc((void**)&c->ws_ml, sizeof(float) * c->ws_records * 2, "workspace");
-    if (st == INFS_OK) st = alloc((void**)&c->counters, sizeof(int32_t) * c->S * c->Hkv, "counters");
+    if (st == INFS_OK) st = alloc((void**)&c->counters, counter_bytes(c), "counters");
     if (st == INFS_OK) st = alloc((void**)&c->tokens, sizeof(int32_t) * c->NP * c->G, "token counters");
     if (st == INFS_OK) st = alloc((void**)&c->status, sizeof(int32_t), "status word");
     if (st != INFS_OK) {
@@ -432,7 +454,7 @@ infs_status infs_reset(infs_ctx* c) {
   reset_host(c);
   if (!c->dry) {
     HIP_TRY(c, hipMemsetAsync(c->tokens, 0, sizeof(int32_t) * c->NP * c->G, c->stream));
-    HIP_TRY(c, hipMemsetAsync(c->counters, 0, sizeof(int32_t) * c->S * c->Hkv, c->stream));
+    HIP_TRY(c, hipMemsetAsync(c->counters, 0, counter_bytes(c), c->stream));
   }
   return INFS_OK;
 }
