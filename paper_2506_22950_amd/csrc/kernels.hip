@@ -864,7 +864,7 @@ __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(co
   constexpr int SMEM = SH::SMEM > MergeShape<SH>::SMEM ? SH::SMEM : MergeShape<SH>::SMEM;
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
   __shared__ unsigned long long flag;
-  const int cs = blockIdx.x % kClockSlots;
+  const int cs = (blockIdx.x % kClockSlots) * kClockStride;
   if (a.clock_start && threadIdx.x == 0)
     __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);

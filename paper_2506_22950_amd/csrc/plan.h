@@ -17,9 +17,10 @@ constexpr int kMfmaPrefixSplit = 4 * kMfmaBlock;  // MFMA prefix chunk: one bloc
 constexpr int kMaxPartials = 128;  // prefix + response chunks merged for one slot
 constexpr int kMaxSplit = 4096;    // split-K chunk length limit (a wavefront covers <= 64 pages)
 
-constexpr int kMergeSpins = 1 << 20;
-constexpr int kCounterStride = 32;  // int32 per arrival counter: each counter has a 128-byte line of its own
-constexpr int kClockSlots = 64;  // bound on a merge block's wait for its producers
+constexpr int kMergeSpins = 1 << 20;   // bound on a merge block's wait for its producers
+constexpr int kCounterStride = 32;     // int32 per arrival counter: each counter has a 128-byte line of its own
+constexpr int kClockSlots = 16;        // timing slots per launch (see StepArgs::clock_start)
+constexpr int kClockStride = 16;       // uint64 per timing slot: one 128-byte line each
 
 // Work item kinds, in grid order: prefix chunks, response chunks, idle slots,
 // then one merge item per live slot.  Grid x = item * Hkv + kv_head, so with 8
@@ -61,9 +62,10 @@ struct StepArgs {
                        // carries the values they reach once its producers have all arrived.
   int32_t* tokens;     // [num_prompts, G] per-sample token counters
   int32_t* status;     // device status word: nonzero after a merge wait hit its bound
-  // Timing mode (else null): kClockSlots start/end slots of this launch; block b
-  // folds its start into min slot b % kClockSlots and its end into max slot
-  // b % kClockSlots (spread so the atomics do not queue on one address).
+  // Timing mode (else null): kClockSlots start/end slots of this launch,
+  // kClockStride apart; block b folds its start into the minimum of slot
+  // b % kClockSlots and its end into the maximum of that slot (spread over
+  // cache lines so the atomics do not queue on one line).
   unsigned long long* clock_start;
   unsigned long long* clock_end;
   // geometry

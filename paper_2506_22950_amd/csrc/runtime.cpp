@@ -30,7 +30,7 @@ thread_local std::string g_thread_error = "no error";
 // event pair brackets the whole timed region on the context's stream.
 struct Timing {
   bool on = false;
-  unsigned long long* clocks = nullptr;  // [capacity][kClockSlots] starts, then the same for ends
+  unsigned long long* clocks = nullptr;  // [capacity][kClockSlots * kClockStride] starts, then ends
   int64_t capacity = 0;
   int64_t used = 0;                      // pairs written since the last harvest
   double kernel_ms = 0.0;
@@ -39,6 +39,8 @@ struct Timing {
   double ticks_per_ms = 0.0;
 };
 }  // namespace
+
+constexpr size_t kClockWords = (size_t)infs::kClockSlots * infs::kClockStride;  // per launch
 
 struct infs_ctx {
   infs_config cfg{};
@@ -119,14 +121,14 @@ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 void free_device(infs_ctx* c) {
   if (c->dry) return;
-  hipFree(c->prefix);
-  hipFree(c->pool);
-  hipFree(c->page_table);
-  hipFree(c->ws_o);
-  hipFree(c->ws_ml);
-  hipFree(c->counters);
-  hipFree(c->tokens);
-  hipFree(c->status);
+  (void)hipFree(c->prefix);
+  (void)hipFree(c->pool);
+  (void)hipFree(c->page_table);
+  (void)hipFree(c->ws_o);
+  (void)hipFree(c->ws_ml);
+  (void)hipFree(c->counters);
+  (void)hipFree(c->tokens);
+  (void)hipFree(c->status);
 }
 
 size_t counter_bytes(const infs_ctx* c) {
@@ -225,7 +227,7 @@ infs_status open_step(infs_ctx* c) {
 // Start times to all ones (so the first block's minimum wins), end times to 0.
 infs_status arm_clocks(infs_ctx* c) {
   Timing& t = c->timing;
-  const size_t n = (size_t)t.capacity * infs::kClockSlots;
+  const size_t n = (size_t)t.capacity * kClockWords;
   HIP_TRY(c, hipMemsetAsync(t.clocks, 0xFF, sizeof(unsigned long long) * n, c->stream));
   HIP_TRY(c, hipMemsetAsync(t.clocks + n, 0, sizeof(unsigned long long) * n, c->stream));
   return INFS_OK;
@@ -235,14 +237,14 @@ infs_status arm_clocks(infs_ctx* c) {
 infs_status harvest_clocks(infs_ctx* c) {
   Timing& t = c->timing;
   if (t.used > 0) {
-    const size_t n = (size_t)t.capacity * infs::kClockSlots;
+    const size_t n = (size_t)t.capacity * kClockWords;
     std::vector<unsigned long long> h(2 * n);
     HIP_TRY(c, hipStreamSynchronize(c->stream));
     HIP_TRY(c, hipMemcpy(h.data(), t.clocks, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
     for (int64_t i = 0; i < t.used; ++i) {
       unsigned long long a = ~0ull, b = 0;
       for (int k = 0; k < infs::kClockSlots; ++k) {
-        const size_t x = (size_t)i * infs::kClockSlots + k;
+        const size_t x = (size_t)i * kClockWords + (size_t)k * infs::kClockStride;
         if (h[n + x] == 0) continue;  // slot not reached by any block
         a = std::min(a, h[x]);
         b = std::max(b, h[n + x]);
@@ -288,8 +290,8 @@ infs_status timed_launch(infs_ctx* c) {
       infs_status st = harvest_clocks(c);
       if (st != INFS_OK) return st;
     }
-    c->plan.clock_start = t.clocks + (size_t)t.used * infs::kClockSlots;
-    c->plan.clock_end = t.clocks + ((size_t)t.capacity + t.used) * infs::kClockSlots;
+    c->plan.clock_start = t.clocks + (size_t)t.used * kClockWords;
+    c->plan.clock_end = t.clocks + ((size_t)t.capacity + t.used) * kClockWords;
     ++t.used;
   }
   HIP_TRY(c, infs::launch_decode(c->key, c->plan, c->grid, c->stream));
@@ -440,10 +442,10 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
 void infs_destroy(infs_ctx* c) {
   if (!c) return;
   if (!c->dry) {
-    hipStreamSynchronize(c->stream);
-    if (c->timing.clocks) hipFree(c->timing.clocks);
+    (void)hipStreamSynchronize(c->stream);
+    if (c->timing.clocks) (void)hipFree(c->timing.clocks);
     for (auto e : c->timing.region)
-      if (e) hipEventDestroy(e);
+      if (e) (void)hipEventDestroy(e);
     free_device(c);
   }
   delete c;
@@ -601,8 +603,8 @@ infs_status infs_timing_begin(infs_ctx* c) {
   if (c->dry) return fail(c, INFS_E_STATE, "no timing in a dry-run context");
   Timing& t = c->timing;
   if (!t.clocks) {
-    t.capacity = 1 << 13;
-    HIP_TRY(c, hipMalloc((void**)&t.clocks, sizeof(unsigned long long) * 2 * t.capacity * infs::kClockSlots));
+    t.capacity = 1 << 12;
+    HIP_TRY(c, hipMalloc((void**)&t.clocks, sizeof(unsigned long long) * 2 * t.capacity * kClockWords));
     HIP_TRY(c, hipEventCreate(&t.region[0]));
     HIP_TRY(c, hipEventCreate(&t.region[1]));
     int dev = 0, khz = 0;
