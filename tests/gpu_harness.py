@@ -127,12 +127,14 @@ def oracle_log(cfg, wl, policy):
     return out
 
 
-def sample_steps(log, every=13, edge=4):
-    """Steps to check: every `every`-th, the first and last `edge`, and every step
-    where some slot decodes its first token (just refilled)."""
+def sample_steps(log, every=13, edge=4, refills=None):
+    """Steps to check: every `every`-th, the first and last `edge`, and the steps
+    where some slot decodes its first token (just refilled) -- all of them, or
+    `refills` of them spread evenly."""
     n = len(log)
     keep = set(range(0, n, every)) | set(range(min(edge, n))) | set(range(max(0, n - edge), n))
-    for k, row in enumerate(log):
-        if any(e is not None and e[2] == 1 for e in row):
-            keep.add(k)
+    fills = [k for k, row in enumerate(log) if any(e is not None and e[2] == 1 for e in row)]
+    if refills is not None and len(fills) > refills:
+        fills = [fills[int(i)] for i in np.linspace(0, len(fills) - 1, refills)]
+    keep.update(fills)
     return keep

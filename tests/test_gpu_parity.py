@@ -106,10 +106,15 @@ def test_schedule_invariance_and_determinism():
         assert np.array_equal(v, runs["fifo2"][key]), key
 
 
-@pytest.mark.parametrize("name", ["qwen3_1p7b_g64"])
-def test_full_size_sampled(name):
-    # Full workload in the launch configuration the benchmark times; outputs of
-    # sampled steps on layers {0, L/2, L-1} against the oracle.
+@pytest.mark.parametrize("name,every,window", [
+    ("qwen3_1p7b_g64", 397, 512),      # the benchmark workload: 32 prefix rows, 16 slots
+    ("longtail_g128", 997, 256),       # m=32 (64 prefix rows), responses up to 8192
+    ("qwen3_8b_4prompts", 1201, 128),  # four prefixes of 256..4096, hpk=4 (64 rows per prompt), 64 slots
+])
+def test_full_size_sampled(name, every, window):
+    # Whole workload in the launch configuration the benchmark uses; outputs of
+    # sampled steps (and the first and last ones) on the first and last layer
+    # against the oracle.
     cfg = get_config(name)
-    _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=397, edge=2),
-                   layers=(0, cfg.layers - 1), window=512)
+    _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=every, edge=2, refills=8),
+                   layers=(0, cfg.layers - 1), window=window)
