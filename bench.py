@@ -140,6 +140,36 @@ def summarize_pmc(workload, fetch_dir, write_dir):
     return "\n".join(lines)
 
 
+def schedule_table(n_groups=64, G=32, m=4, cap=1024):
+    """Running steps of the refill policies, Table-2 style, from the library's
+    host scheduler in dry-run mode (no GPU): n_groups groups of G samples on m
+    slots per length setting; steps summed over the groups."""
+    import math
+
+    from paper_2506_22950_amd.group import plan_steps
+    from workload import SCHEDULER_STUDY, get_config, scheduler_study_lengths
+
+    cfg = get_config("tiny_f32").with_(layers=1, samples_per_prompt=G, slots_per_prompt=m, max_suffix_len=cap)
+    rows = [("naive micro groups", "naive", "pred"), ("fixed-slot", "fixed_row", "pred"),
+            ("FPTAS only", "fptas", "pred"), ("SJF only", "sjf", "pred"), ("FPTAS + SJF", "fptas_sjf", "pred"),
+            ("post-hoc LPT (true lengths)", "lpt", "true")]
+    out = [f"{n_groups} groups of G={G} on m={m} slots, lengths capped at {cap}, "
+           f"predictions L*exp(N(0, 0.2^2)); running steps summed over the groups (ratio to fixed-slot)"]
+    for k, (label, mu, sigma) in enumerate(SCHEDULER_STUDY):
+        L, pred = scheduler_study_lengths(mu, sigma, n_groups, G, cap=cap, seed=k)
+        tot = {}
+        for _, policy, key in rows:
+            tot[policy] = sum(len(plan_steps(cfg, L[n:n + 1], policy, (L if key == "true" else pred)[n:n + 1]))
+                              for n in range(n_groups))
+        lb = sum(max(math.ceil(int(L[n].sum()) / m), int(L[n].max())) for n in range(n_groups))
+        out.append(f"\n{label}: mean length {L.mean():.0f}")
+        base = tot["fixed_row"]
+        for name, policy, _ in rows:
+            out.append(f"  {name:30s} {tot[policy]:8d}  (x{tot[policy] / base:.2f})")
+        out.append(f"  {'lower bound max(sum/m, max)':30s} {lb:8d}  (x{lb / base:.2f})")
+    return "\n".join(out)
+
+
 def algorithmic_bytes(cfg, steplog):
     """Algorithmic HBM bytes of all decode launches, from the step log alone:
     prefix K/V once per prompt with a live slot, each live slot's response K/V
@@ -280,9 +310,14 @@ def main():
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the traffic summary of two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--schedules", action="store_true",
+                    help="print the running steps of the refill policies (host only, no GPU) and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
         print(summarize_pmc(args.workload, *args.summarize_pmc))
+        return
+    if args.schedules:
+        print(schedule_table())
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",

@@ -70,9 +70,19 @@ typedef enum infs_policy {
                             with the next m sample ids (Section 3.1) */
     INFS_FIXED_ROW = 1,  /* fixed-slot continuous sampling: slot s runs s, s+m, s+2m, ... (Section 3.2) */
     INFS_FIFO = 2,       /* continuous refill with the lowest pending sample id */
-    INFS_SJF = 3         /* continuous refill with the smallest predicted length, ties to the
+    INFS_SJF = 3,        /* continuous refill with the smallest predicted length, ties to the
                             lowest id (Algorithm 3) */
+    INFS_FPTAS = 4,      /* static pre-planning only: Algorithm 2 groups the samples into m bins by
+                            predicted length (epsilon INFS_FPTAS_EPSILON) and slot s runs bin s in
+                            position order (Table 2, "FPTAS only") */
+    INFS_FPTAS_SJF = 5,  /* Algorithm 1: each slot starts with position 0 of its bin, every later
+                            refill is SJF (Table 2, "Infinite") */
+    INFS_LPT = 6         /* continuous refill with the largest predicted length, ties to the lowest
+                            id; given the true lengths, the post-hoc list schedule that serves as
+                            the reference of Tables 1 and 2 */
 } infs_policy;
+
+#define INFS_FPTAS_EPSILON 0.1
 
 /* Bookkeeping only: no device memory, no kernels, pointers are not read.
    Lets the slot / page / step state machine run on a host without a GPU. */
@@ -193,8 +203,8 @@ const char* infs_last_error(const infs_ctx* ctx);
  * ------------------------------------------------------------------------------------------- */
 typedef struct infs_sched infs_sched;
 
-/* pred_len: G predicted lengths (float64), required for INFS_SJF, ignored otherwise (may be NULL).
-   The array is copied. */
+/* pred_len: G predicted lengths (float64), required for INFS_SJF, INFS_FPTAS, INFS_FPTAS_SJF and
+   INFS_LPT, ignored otherwise (may be NULL).  The array is copied. */
 infs_status infs_sched_create(int32_t G, int32_t m, int32_t policy, const double* pred_len,
                               infs_sched** out);
 
@@ -210,6 +220,16 @@ infs_status infs_sched_done(infs_sched* s, int32_t slot);
 int32_t infs_sched_pending(const infs_sched* s);
 
 void infs_sched_destroy(infs_sched* s);
+
+/* FPTAS-based micro-group assignment (Algorithm 2), on the host.  With S the sum of pred_len (summed
+   in id order) and K = (epsilon * S) / N, sample i has integer size ceil(pred_len[i] / K) and the
+   bin capacity is ceil(sum of sizes / N).  Samples are placed largest size first (equal sizes:
+   lower id first) into the first bin whose load stays within the capacity; a sample that fits no
+   bin goes to the bin with the least load (lowest index among equals) -- a case the paper leaves
+   open.  Writes group_out[i] (bin of sample i, 0..N-1) and pos_out[i] (its position in the bin).
+   pred_len: G finite values >= 0 with a positive sum; epsilon > 0.  E_ARG otherwise. */
+infs_status infs_fptas_assign(int32_t G, int32_t N, const double* pred_len, double epsilon, int32_t* group_out,
+                              int32_t* pos_out);
 
 #ifdef __cplusplus
 }

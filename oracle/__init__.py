@@ -14,22 +14,25 @@ Two parts, both plain and slow on purpose:
   whole group, one private response buffer per active sample).
 * ``simulator`` -- the step-by-step slot / refill process of naive micro
   sampling groups (Section 3.1), fixed-slot continuous sampling (Section 3.2)
-  and continuous refill in FIFO or shortest-job-first order (Algorithms 1
-  and 3).
+  continuous refill in FIFO or shortest-job-first order (Algorithms 1
+  and 3), FPTAS micro-group assignment (Algorithm 2) alone or followed by
+  shortest-job-first refill, and longest-first list scheduling.
 
 Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
 a library routine, brute force and a hand-derived worked example.
 """
 
 from .attention import attend, attend_slot, attention_weights, default_scale
-from .simulator import POLICIES, SimResult, simulate, simulate_group
+from .simulator import FPTAS_EPSILON, POLICIES, SimResult, fptas_assign, simulate, simulate_group
 
 __all__ = [
     "attend",
     "attend_slot",
     "attention_weights",
     "default_scale",
+    "FPTAS_EPSILON",
     "POLICIES",
+    "fptas_assign",
     "SimResult",
     "simulate",
     "simulate_group",

@@ -19,20 +19,79 @@ Refill policies:
                    first.
 * ``sjf``       -- shortest-job-first refill (Algorithm 3): the pending sample
                    with the smallest predicted length, ties to the lowest id.
+* ``fptas``     -- static pre-planning only (Table 2's "FPTAS only"): the
+                   samples are grouped into m bins by Algorithm 2 on the
+                   predicted lengths, and slot s runs bin s in position order.
+* ``fptas_sjf`` -- the two-stage scheduler of Algorithm 1 (Table 2's
+                   "Infinite"): every slot starts with position 0 of its bin,
+                   and every later refill is shortest-job-first.
+* ``lpt``       -- continuous refill, longest predicted length first, ties to
+                   the lowest id.  Given the true lengths this is the post-hoc
+                   list schedule used as the reference of Tables 1 and 2.
 
 Readings where the paper is silent: a sample of length L holds its slot for
 exactly L steps; when several slots free up in one step they are refilled in
-ascending slot order; the initial fill uses the same policy as every refill;
-Algorithm 3's candidate set is the samples neither finished nor already
-dispatched (its ``mask`` being the runtime dispatch record).
+ascending slot order; the initial fill uses the same policy as every refill
+(for ``fptas_sjf``: position 0 of the slot's bin, or shortest-job-first if
+the bin is empty or its first sample already left); Algorithm 3's candidate
+set is the samples neither finished nor already dispatched (its ``mask`` being
+the runtime dispatch record); Algorithm 2 runs with one bin per slot.
 """
+
+import math
 
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
 
 import numpy as np
 
-POLICIES = ("naive", "fixed_row", "fifo", "sjf")
+POLICIES = ("naive", "fixed_row", "fifo", "sjf", "fptas", "fptas_sjf", "lpt")
+NEEDS_PRED = ("sjf", "fptas", "fptas_sjf", "lpt")
+FPTAS_EPSILON = 0.1
+
+
+def fptas_assign(pred, N: int, eps: float = FPTAS_EPSILON):
+    """Algorithm 2 (FPTAS-based micro group assignment), step by step.
+
+    The predicted lengths are scaled by K = eps * S / N (S their sum) and
+    rounded up to integers; the bin capacity is the rounded-up mean of the
+    scaled sizes over the N bins; samples are taken in descending scaled
+    size (ties: lower id first) and each goes to the first bin it fits in.
+    The paper leaves unplaced samples unspecified: such a sample goes to the
+    bin with the smallest scaled load (lowest index on ties).
+
+    Returns (group, pos): sample i is the pos[i]-th sample of bin group[i].
+    Floating point: S is summed in id order and K = (eps * S) / N, in float64.
+    """
+    pred = [float(x) for x in pred]
+    G = len(pred)
+    if N < 1:
+        raise ValueError("N must be >= 1")
+    S = 0.0
+    for x in pred:
+        S += x
+    K = (eps * S) / N
+    if not (K > 0.0):
+        raise ValueError("the predicted lengths must have a positive sum")
+    size = [int(math.ceil(x / K)) for x in pred]
+    cap = -(-sum(size) // N)  # ceil of the integer mean
+    load = [0] * N
+    members = [[] for _ in range(N)]
+    group = [-1] * G
+    pos = [-1] * G
+    for i in sorted(range(G), key=lambda i: (-size[i], i)):
+        target = None
+        for n in range(N):
+            if load[n] + size[i] <= cap:
+                target = n
+                break
+        if target is None:
+            target = min(range(N), key=lambda n: (load[n], n))
+        group[i] = target
+        pos[i] = len(members[target])
+        members[target].append(i)
+        load[target] += size[i]
+    return group, pos
 
 
 @dataclass
@@ -55,10 +114,18 @@ def simulate(L, m: int, policy: str, pred=None) -> SimResult:
         raise ValueError("every sample has at least one token")
     if policy not in POLICIES:
         raise ValueError(f"unknown policy {policy!r}")
-    if policy == "sjf":
+    if policy in NEEDS_PRED:
         if pred is None:
-            raise ValueError("sjf needs predicted lengths")
+            raise ValueError(f"{policy} needs predicted lengths")
         pred = [float(x) for x in pred]
+    bins = None
+    if policy in ("fptas", "fptas_sjf"):
+        group, pos = fptas_assign(pred, m)
+        bins = [[] for _ in range(m)]
+        for i in sorted(range(G), key=lambda i: (group[i], pos[i])):
+            bins[group[i]].append(i)
+    bin_next = [0] * m            # fptas: next position of each slot's bin
+    started = [False] * m         # fptas_sjf: slot has had its initial fill
 
     slot_sample = [None] * m      # sample id held by each slot, or None
     slot_len = [0] * m            # tokens generated so far by that sample
@@ -89,14 +156,29 @@ def simulate(L, m: int, policy: str, pred=None) -> SimResult:
                 if j >= G:
                     continue
                 row_next[s] = j + m
+            elif policy == "fptas":
+                if bin_next[s] >= len(bins[s]):
+                    continue
+                j = bins[s][bin_next[s]]
+                bin_next[s] += 1
             elif policy == "fifo":
                 if not pending:
                     return
                 j = min(pending)
-            else:  # sjf
+            elif policy == "lpt":
                 if not pending:
                     return
-                j = min(pending, key=lambda i: (pred[i], i))
+                j = min(pending, key=lambda i: (-pred[i], i))
+            else:  # sjf, fptas_sjf
+                if not pending:
+                    return
+                j = None
+                if policy == "fptas_sjf" and not started[s]:
+                    started[s] = True
+                    if bins[s] and bins[s][0] in pending:
+                        j = bins[s][0]
+                if j is None:
+                    j = min(pending, key=lambda i: (pred[i], i))
             give(s, j)
 
     def give(s, j):

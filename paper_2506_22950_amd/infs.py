@@ -19,8 +19,10 @@ LIB_PATH = os.path.join(HERE, "libinfs.so")
 OK, E_ARG, E_STATE, E_CAPACITY, E_DUP, E_NOMEM, E_DEVICE = 0, -1, -2, -3, -4, -5, -6
 STATUS_NAMES = {0: "OK", -1: "E_ARG", -2: "E_STATE", -3: "E_CAPACITY", -4: "E_DUP", -5: "E_NOMEM", -6: "E_DEVICE"}
 F32, BF16 = 0, 1
-NAIVE, FIXED_ROW, FIFO, SJF = 0, 1, 2, 3
-POLICY = {"naive": NAIVE, "fixed_row": FIXED_ROW, "fifo": FIFO, "sjf": SJF}
+NAIVE, FIXED_ROW, FIFO, SJF, FPTAS, FPTAS_SJF, LPT = 0, 1, 2, 3, 4, 5, 6
+POLICY = {"naive": NAIVE, "fixed_row": FIXED_ROW, "fifo": FIFO, "sjf": SJF, "fptas": FPTAS, "fptas_sjf": FPTAS_SJF,
+          "lpt": LPT}
+FPTAS_EPSILON = 0.1
 FLAG_DRY_RUN = 1
 
 # Every symbol include/infs.h declares.
@@ -29,7 +31,7 @@ EXPORTS = (
     "infs_refill_slot", "infs_retire_slot", "infs_decode_step", "infs_end_step", "infs_slot_state",
     "infs_sample_tokens", "infs_sync", "infs_get_stats", "infs_timing_begin", "infs_timing_end",
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
-    "infs_sched_destroy",
+    "infs_sched_destroy", "infs_fptas_assign",
 )
 
 
@@ -90,6 +92,8 @@ def load():
         "infs_sched_done": (I32, [P, I32]),
         "infs_sched_pending": (I32, [P]),
         "infs_sched_destroy": (None, [P]),
+        "infs_fptas_assign": (I32, [I32, I32, ctypes.POINTER(ctypes.c_double), ctypes.c_double,
+                                    ctypes.POINTER(I32), ctypes.POINTER(I32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -243,3 +247,17 @@ class Sched:
                 self._h = None
         except Exception:
             pass
+
+
+def fptas_assign(pred_len, N, epsilon=FPTAS_EPSILON):
+    """infs_fptas_assign: (group, pos) arrays of Algorithm 2."""
+    pred = np.ascontiguousarray(pred_len, dtype=np.float64)
+    G = len(pred)
+    group = np.zeros(G, dtype=np.int32)
+    pos = np.zeros(G, dtype=np.int32)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    st = load().infs_fptas_assign(G, N, pred.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), epsilon,
+                                  group.ctypes.data_as(I32P), pos.ctypes.data_as(I32P))
+    if st != OK:
+        raise InfsError(st, "infs_fptas_assign")
+    return group, pos

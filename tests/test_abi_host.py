@@ -207,3 +207,44 @@ def test_sched_errors():
     with pytest.raises(infs.InfsError):
         infs.Sched(4, 2, "sjf", pred_len=[1.0, float("nan"), 2.0, 3.0])
     assert s.pending == 3
+
+
+def test_fptas_assign_matches_oracle():
+    # infs_fptas_assign (C++) and the oracle's Algorithm 2 (Python) agree on
+    # the hand-worked cases and bit for bit on random predicted lengths.
+    import json
+    from oracle import fptas_assign
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "sim_worked_example.json")))
+    for case in g["fptas_cases"]:
+        group, pos = infs.fptas_assign(case["pred"], case["N"], case["eps"])
+        assert list(group) == case["group"] and list(pos) == case["pos"], case["note"]
+    rng = np.random.default_rng(11)
+    for _ in range(2000):
+        G = int(rng.integers(1, 70))
+        N = int(rng.integers(1, 17))
+        eps = float(rng.choice([0.01, 0.1, 0.25, 1.0]))
+        pred = np.exp(rng.normal(5.5, 1.2, size=G))
+        if rng.random() < 0.3:
+            pred = np.round(pred)  # integer predictions: many equal sizes
+        group, pos = infs.fptas_assign(pred, N, eps)
+        want_g, want_p = fptas_assign(pred, N, eps)
+        assert list(group) == want_g and list(pos) == want_p
+
+
+def test_fptas_assign_errors():
+    for args in (([1.0, 2.0], 0, 0.1), ([1.0, 2.0], 2, 0.0), ([1.0, float("nan")], 2, 0.1),
+                 ([1.0, -1.0], 2, 0.1), ([0.0, 0.0], 2, 0.1), ([], 2, 0.1)):
+        with pytest.raises(infs.InfsError):
+            infs.fptas_assign(*args)
+    for policy in ("fptas", "fptas_sjf", "lpt"):
+        with pytest.raises(infs.InfsError):
+            infs.Sched(4, 2, policy)  # these policies need predicted lengths
+
+
+@pytest.mark.parametrize("policy", ["fixed_row", "fptas", "sjf", "fptas_sjf", "lpt"])
+def test_dry_run_scheduler_policies_full_workload(policy):
+    # The policies of the scheduler comparison on the benchmark workload's
+    # lengths: step logs equal the simulator's.
+    cfg = get_config("qwen3_1p7b_g64")
+    wl = Workload(cfg)
+    assert plan_steps(cfg, wl.L, policy, wl.L_hat) == _oracle_log(cfg, wl.L, policy, wl.L_hat)

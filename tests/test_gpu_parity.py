@@ -66,6 +66,17 @@ def test_bf16_mfma64_and_hpk4_multi_prompt():
     _run_and_check(cfg, "sjf", split=128, capture=lambda log: sample_steps(log, every=3))
 
 
+@pytest.mark.parametrize("policy", ["fptas", "fptas_sjf"])
+def test_bf16_fptas_schedules(policy):
+    # The decode path under the FPTAS plans (Algorithm 2 alone, and followed
+    # by shortest-job-first refill as in Algorithm 1): bookkeeping bit-exact
+    # and outputs against the oracle.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(300,), samples_per_prompt=20,
+                                             length_dist=("lognormal", 4.0, 1.0, 1, 200), max_suffix_len=200,
+                                             pool_rows=None)
+    _run_and_check(cfg, policy, split=128, capture=lambda log: sample_steps(log, every=4))
+
+
 def test_bf16_single_slot_wave_prefix():
     # m=1: 2 prefix rows, so the prefix runs on the wavefront path in bf16.
     cfg = get_config("qwen3_1p7b_l1_g32").with_(slots_per_prompt=1, samples_per_prompt=4, prompt_lens=(257,),

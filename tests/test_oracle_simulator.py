@@ -4,6 +4,8 @@ Checks: the hand-derived worked example (full timelines), closed forms of the
 naive and fixed-slot step counts, token conservation, Graham's list
 scheduling bound, dominance relations, the special cases m = 1 and m >= G,
 and an independent event-driven implementation of the continuous policies.
+FPTAS (Algorithm 2): hand-worked assignments, partition and ordering
+invariants, and the load bound that its scaling and capacity imply.
 """
 
 import heapq
@@ -15,7 +17,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle import POLICIES, simulate, simulate_group
+from oracle import FPTAS_EPSILON, POLICIES, fptas_assign, simulate, simulate_group
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "sim_worked_example.json")
 
@@ -169,3 +171,88 @@ def test_table_orderings_on_synthetic_lengths():
         assert steps["fifo"] <= steps["naive"]
         assert steps["sjf"] < steps["naive"]
         assert steps["fixed_row"] <= steps["naive"]
+
+
+def test_fptas_golden_cases():
+    g = json.load(open(GOLDEN))
+    for case in g["fptas_cases"]:
+        group, pos = fptas_assign(case["pred"], case["N"], case["eps"])
+        assert group == case["group"], case["note"]
+        assert pos == case["pos"], case["note"]
+
+
+def _fptas_sizes(pred, N, eps):
+    K = (eps * float(sum(float(x) for x in pred))) / N
+    return [math.ceil(float(x) / K) for x in pred], K
+
+
+def test_fptas_invariants_random():
+    rng = np.random.default_rng(7)
+    fitted = 0
+    for _ in range(3000):
+        G = int(rng.integers(1, 40))
+        N = int(rng.integers(1, 9))
+        eps = float(rng.choice([0.05, 0.1, 0.3, 1.0]))
+        pred = np.exp(rng.normal(5.0, 1.0, size=G))
+        group, pos = fptas_assign(pred, N, eps)
+        size, K = _fptas_sizes(pred, N, eps)
+        cap = math.ceil(sum(size) / N)
+        bins = [sorted((pos[i], i) for i in range(G) if group[i] == n) for n in range(N)]
+        # a partition of the samples; positions 0..|bin|-1; descending size, ties by id
+        assert sorted(i for b in bins for _, i in b) == list(range(G))
+        for b in bins:
+            assert [p for p, _ in b] == list(range(len(b)))
+            keys = [(-size[i], i) for _, i in b]
+            assert keys == sorted(keys)
+        loads = [sum(size[i] for _, i in b) for b in bins]
+        if max(loads) <= cap:
+            fitted += 1
+            # every bin within the capacity bounds its predicted load:
+            # sum(pred) <= K * sum(scaled) <= K * cap <= S/N + (G/N + 1) K
+            S = float(sum(pred))
+            for b in bins:
+                assert sum(float(pred[i]) for _, i in b) <= S / N + (G / N + 1) * K + 1e-6
+    assert fitted > 1000
+
+
+def test_fptas_policy_closed_form():
+    # FPTAS only: slot s runs bin s back to back, so the step count is the
+    # largest true load of a bin.
+    for L, m, pred in _instances(2000, seed=3):
+        group, _ = fptas_assign(pred, m, FPTAS_EPSILON)
+        want = max(int(sum(L[i] for i in range(len(L)) if group[i] == s)) for s in range(m))
+        r = simulate(L, m, "fptas", pred=pred)
+        assert r.steps == want
+        assert list(r.tokens) == list(L)
+
+
+def test_fptas_sjf_and_lpt_are_list_schedules():
+    # FPTAS+SJF: slot s starts with position 0 of bin s, then every freed slot
+    # takes the shortest predicted pending sample.  LPT: longest predicted
+    # first.  Both are list schedules, checked by the event-driven scheduler.
+    for L, m, pred in _instances(2000, seed=4):
+        G = len(L)
+        group, pos = fptas_assign(pred, m, FPTAS_EPSILON)
+        heads = [next((i for i in range(G) if group[i] == s and pos[i] == 0), None) for s in range(m)]
+        r = simulate(L, m, "fptas_sjf", pred=pred)
+        if all(h is not None for h in heads):
+            rest = sorted((i for i in range(G) if i not in heads), key=lambda i: (pred[i], i))
+            assert list(r.finish_step) == _event_driven(list(L), m, heads + rest)
+        lo = max(math.ceil(L.sum() / m), int(L.max()))
+        hi = math.floor(L.sum() / m + (1 - 1 / m) * L.max() + 1e-9)
+        assert lo <= r.steps <= hi
+        order = sorted(range(G), key=lambda i: (-pred[i], i))
+        assert list(simulate(L, m, "lpt", pred=pred).finish_step) == _event_driven(list(L), m, order)
+
+
+def test_lpt_on_true_lengths_within_graham_bound_of_optimum():
+    # Longest-processing-time list scheduling on exact lengths is within
+    # 4/3 - 1/(3m) of the optimal makespan (Graham, 1969).
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        G = int(rng.integers(1, 8))
+        m = int(rng.integers(1, 4))
+        L = rng.integers(1, 15, size=G)
+        opt = _optimum(list(L), m)
+        lpt = simulate(L, m, "lpt", pred=L.astype(float)).steps
+        assert opt <= lpt <= (4 / 3 - 1 / (3 * m)) * opt + 1e-9

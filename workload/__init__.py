@@ -7,14 +7,17 @@ without sharing any of the method's code.
 """
 
 from .configs import CONFIGS, GroupConfig, get_config
-from .gen import Workload, bf16_bits_to_f64, f32_to_bf16_bits, splitmix64
+from .gen import (SCHEDULER_STUDY, Workload, bf16_bits_to_f64, f32_to_bf16_bits, scheduler_study_lengths,
+                  splitmix64)
 
 __all__ = [
     "CONFIGS",
     "GroupConfig",
     "get_config",
+    "SCHEDULER_STUDY",
     "Workload",
     "bf16_bits_to_f64",
     "f32_to_bf16_bits",
+    "scheduler_study_lengths",
     "splitmix64",
 ]

@@ -190,3 +190,23 @@ class Workload:
     @property
     def total_tokens(self) -> int:
         return int(self.L.sum())
+
+
+# Length settings of the scheduler comparison: completion lengths
+# clip(rint(exp(N(mu, sigma))), 1, cap), with means of a few hundred tokens at a
+# 1024-token cap as in the paper's experiments (Section 5.1).  They stand in for
+# the datasets' real completion lengths, which are not used.
+SCHEDULER_STUDY = (
+    ("short (mean ~180)", 4.95, 0.75),
+    ("medium (mean ~420)", 5.85, 0.8),
+    ("long (mean ~610)", 6.35, 0.9),
+)
+
+
+def scheduler_study_lengths(mu, sigma, n_groups, G, cap=1024, pred_sigma=0.2, seed=0):
+    """n_groups independent groups of G true lengths and their predictions
+    L * exp(N(0, pred_sigma^2)); PCG64(5000 + seed) and PCG64(6000 + seed)."""
+    rng = np.random.Generator(np.random.PCG64(5000 + seed))
+    L = np.clip(np.rint(np.exp(rng.normal(mu, sigma, size=(n_groups, G)))), 1, cap).astype(np.int32)
+    noise = np.random.Generator(np.random.PCG64(6000 + seed)).normal(0.0, pred_sigma, size=L.shape)
+    return L, L.astype(np.float64) * np.exp(noise)
