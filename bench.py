@@ -141,31 +141,42 @@ def summarize_pmc(workload, fetch_dir, write_dir):
 
 
 def schedule_table(n_groups=64, G=32, m=4, cap=1024):
-    """Running steps of the refill policies, Table-2 style, from the library's
-    host scheduler in dry-run mode (no GPU): n_groups groups of G samples on m
-    slots per length setting; steps summed over the groups."""
+    """Running steps of the refill policies (Table 2 style) and the length bias
+    of dynamic-slot sampling (Table 1 style), from the library's host scheduler
+    in dry-run mode (no GPU): n_groups groups of G samples on m slots per
+    length setting; steps summed over the groups."""
     import math
 
     from paper_2506_22950_amd.group import plan_steps
-    from workload import SCHEDULER_STUDY, get_config, scheduler_study_lengths
+    from workload import SCHEDULER_STUDY, get_config, scheduler_study_lengths, scheduler_study_stream
 
     cfg = get_config("tiny_f32").with_(layers=1, samples_per_prompt=G, slots_per_prompt=m, max_suffix_len=cap)
     rows = [("naive micro groups", "naive", "pred"), ("fixed-slot", "fixed_row", "pred"),
             ("FPTAS only", "fptas", "pred"), ("SJF only", "sjf", "pred"), ("FPTAS + SJF", "fptas_sjf", "pred"),
             ("post-hoc LPT (true lengths)", "lpt", "true")]
     out = [f"{n_groups} groups of G={G} on m={m} slots, lengths capped at {cap}, "
-           f"predictions L*exp(N(0, 0.2^2)); running steps summed over the groups (ratio to fixed-slot)"]
+           f"predictions L*exp(N(0, 0.2^2)); running steps summed over the groups (ratio to fixed-slot); "
+           f"mean length of the G samples kept per group"]
     for k, (label, mu, sigma) in enumerate(SCHEDULER_STUDY):
         L, pred = scheduler_study_lengths(mu, sigma, n_groups, G, cap=cap, seed=k)
         tot = {}
         for _, policy, key in rows:
             tot[policy] = sum(len(plan_steps(cfg, L[n:n + 1], policy, (L if key == "true" else pred)[n:n + 1]))
                               for n in range(n_groups))
+        stream = scheduler_study_stream(mu, sigma, L, 8 * G, cap=cap, seed=k)
+        dcfg = cfg.with_(samples_per_prompt=stream.shape[1])
+        dyn_steps, dyn_len = 0, []
+        for n in range(n_groups):
+            acc = []
+            dyn_steps += len(plan_steps(dcfg, stream[n:n + 1], "fifo", None, stop_after=G, accepted=acc))
+            dyn_len.extend(int(stream[n, i]) for i in acc[0])
         lb = sum(max(math.ceil(int(L[n].sum()) / m), int(L[n].max())) for n in range(n_groups))
         out.append(f"\n{label}: mean length {L.mean():.0f}")
         base = tot["fixed_row"]
         for name, policy, _ in rows:
-            out.append(f"  {name:30s} {tot[policy]:8d}  (x{tot[policy] / base:.2f})")
+            out.append(f"  {name:30s} {tot[policy]:8d}  (x{tot[policy] / base:.2f})  mean length {L.mean():6.1f}")
+        out.append(f"  {'dynamic-slot (stream, first G)':30s} {dyn_steps:8d}  (x{dyn_steps / base:.2f})  "
+                   f"mean length {sum(dyn_len) / len(dyn_len):6.1f}")
         out.append(f"  {'lower bound max(sum/m, max)':30s} {lb:8d}  (x{lb / base:.2f})")
     return "\n".join(out)
 

@@ -16,14 +16,16 @@ Two parts, both plain and slow on purpose:
   sampling groups (Section 3.1), fixed-slot continuous sampling (Section 3.2)
   continuous refill in FIFO or shortest-job-first order (Algorithms 1
   and 3), FPTAS micro-group assignment (Algorithm 2) alone or followed by
-  shortest-job-first refill, and longest-first list scheduling.
+  shortest-job-first refill, longest-first list scheduling, and
+  dynamic-slot sampling from an unbounded stream (Section 3.2, mode 2).
 
 Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
 a library routine, brute force and a hand-derived worked example.
 """
 
 from .attention import attend, attend_slot, attention_weights, default_scale
-from .simulator import FPTAS_EPSILON, POLICIES, SimResult, fptas_assign, simulate, simulate_group
+from .simulator import (FPTAS_EPSILON, POLICIES, DynamicResult, SimResult, fptas_assign, simulate,
+                        simulate_dynamic, simulate_group)
 
 __all__ = [
     "attend",
@@ -34,6 +36,8 @@ __all__ = [
     "POLICIES",
     "fptas_assign",
     "SimResult",
+    "DynamicResult",
+    "simulate_dynamic",
     "simulate",
     "simulate_group",
 ]

@@ -220,3 +220,67 @@ def simulate_group(L, m: int, policy: str, pred=None):
         pred = np.asarray(pred).reshape(L.shape)
     res = [simulate(L[p], m, policy, None if pred is None else pred[p]) for p in range(L.shape[0])]
     return max(r.steps for r in res), res
+
+
+@dataclass
+class DynamicResult:
+    steps: int
+    log: List[Tuple[Optional[Tuple[int, int]], ...]]   # as SimResult.log
+    accepted: List[int]                                 # the first `target` samples to complete
+    mean_length: float                                  # their mean length (Table 1's length bias)
+
+
+def simulate_dynamic(L_stream, m: int, target: int) -> DynamicResult:
+    """Dynamic-slot continuous sampling (Section 3.2, mode 2).
+
+    Samples come from an unbounded stream (ids 0, 1, 2, ... with lengths
+    L_stream); a freed slot takes the next id at once, whatever the group
+    structure.  Decoding stops at the end of the step in which the
+    `target`-th sample completes; samples still decoding are discarded.
+    Readings: completions within one step are counted in ascending slot
+    order, and the stream must be long enough to reach `target` completions.
+    """
+    L = [int(x) for x in L_stream]
+    if m < 1 or target < 1:
+        raise ValueError("m and target must be >= 1")
+    if any(x < 1 for x in L):
+        raise ValueError("every sample has at least one token")
+    slot_sample = [None] * m
+    slot_len = [0] * m
+    nxt = 0
+    accepted = []
+    log = []
+    step = 0
+
+    def fill():
+        nonlocal nxt
+        for s in range(m):
+            if slot_sample[s] is None and nxt < len(L):
+                slot_sample[s] = nxt
+                slot_len[s] = 0
+                nxt += 1
+
+    fill()
+    while len(accepted) < target:
+        if all(x is None for x in slot_sample):
+            raise ValueError("the stream ran out before the target number of completions")
+        step += 1
+        row = []
+        for s in range(m):
+            j = slot_sample[s]
+            if j is None:
+                row.append(None)
+                continue
+            slot_len[s] += 1
+            row.append((j, slot_len[s]))
+        log.append(tuple(row))
+        for s in range(m):
+            j = slot_sample[s]
+            if j is not None and slot_len[s] == L[j]:
+                if len(accepted) < target:
+                    accepted.append(j)
+                slot_sample[s] = None
+        if len(accepted) < target:
+            fill()
+    return DynamicResult(steps=step, log=log, accepted=accepted,
+                         mean_length=sum(L[i] for i in accepted) / len(accepted))

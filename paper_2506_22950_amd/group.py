@@ -36,7 +36,8 @@ def schedulers_for(cfg, policy: str, pred=None) -> List[infs.Sched]:
 
 def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_layers: int,
                  provide: Callable, after_step: Optional[Callable] = None,
-                 log: Optional[list] = None) -> int:
+                 log: Optional[list] = None, stop_after: Optional[int] = None,
+                 accepted: Optional[list] = None) -> int:
     """Decode every sample of every prompt; returns the number of running steps.
 
     lengths[p][i]: true length of sample i of prompt p.
@@ -44,6 +45,11 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     after_step(step) is called after each end_step.
     log, if given, receives one tuple per step: for each slot (prompt, sample, t)
     with t the response length after this step, or None for an idle slot.
+    stop_after: dynamic-slot sampling (Section 3.2, mode 2) -- the samples of a
+    prompt form a stream, and once `stop_after` of them have completed (counted
+    in ascending slot order within a step) the prompt stops: its samples still
+    decoding are discarded (their slots retired) and it is not refilled.
+    accepted, if given, receives per prompt the completed sample ids in order.
     """
     NP = len(scheds)
     m = ctx.config.slots_per_prompt
@@ -51,9 +57,13 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     slot_sample = [-1] * S
     slot_len = [0] * S
     Ls = [[int(x) for x in row] for row in lengths]
+    done = [[] for _ in range(NP)]
+    stopped = [False] * NP
 
     def fill():
         for p in range(NP):
+            if stopped[p]:
+                continue
             sch = scheds[p]
             for ls in range(m):
                 s = p * m + ls
@@ -86,11 +96,23 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
                 ctx.retire_slot(s)
                 scheds[p].done(s - p * m)
                 slot_sample[s] = -1
+                if not stopped[p]:
+                    done[p].append(i)
+                    stopped[p] = stop_after is not None and len(done[p]) >= stop_after
+        for p in range(NP):
+            if stopped[p]:
+                for s in range(p * m, (p + 1) * m):
+                    if slot_sample[s] >= 0:
+                        ctx.retire_slot(s)
+                        scheds[p].done(s - p * m)
+                        slot_sample[s] = -1
         fill()
+    if accepted is not None:
+        accepted.extend(done)
     return step
 
 
-def plan_steps(cfg, lengths, policy: str, pred=None) -> list:
+def plan_steps(cfg, lengths, policy: str, pred=None, stop_after=None, accepted=None) -> list:
     """Step log of a group decode, from a dry-run context (bookkeeping only, no GPU)."""
     ctx = context_for(cfg, dry_run=True)
     for p in range(cfg.num_prompts):
@@ -98,6 +120,7 @@ def plan_steps(cfg, lengths, policy: str, pred=None) -> list:
             ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
     log = []
     nothing = (None, None, None, None)
-    decode_group(ctx, schedulers_for(cfg, policy, pred), lengths, cfg.layers, lambda s, l: nothing, log=log)
+    decode_group(ctx, schedulers_for(cfg, policy, pred), lengths, cfg.layers, lambda s, l: nothing, log=log,
+                 stop_after=stop_after, accepted=accepted)
     ctx.destroy()
     return log

@@ -21,12 +21,12 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None):
+def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None):
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
     wl = wl or Workload(cfg)
-    log = plan_steps(cfg, wl.L, policy, wl.L_hat)
+    log = plan_steps(cfg, wl.L, policy, wl.L_hat, stop_after=stop_after)
     dev = DeviceInputs(wl)
     stream = torch.cuda.current_stream()
     ctx = context_for(cfg, stream=stream, split_tokens=split)
@@ -62,7 +62,8 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
             captured[step] = o.cpu().numpy()
 
     t0 = time.time()
-    steps = decode_group(ctx, schedulers_for(cfg, policy, wl.L_hat), wl.L, L, provide, after_step=after)
+    steps = decode_group(ctx, schedulers_for(cfg, policy, wl.L_hat), wl.L, L, provide, after_step=after,
+                         stop_after=stop_after)
     torch.cuda.synchronize()
     tokens = np.stack([ctx.sample_tokens(p) for p in range(cfg.num_prompts)])
     stats = ctx.get_stats()
@@ -111,6 +112,21 @@ def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None):
                 assert err <= tol, f"step {k} slot {s} sample {i} t {t} layer {layer}: max abs err {err:.3g} > {tol}"
                 checked += 1
     return worst, checked
+
+
+def oracle_dynamic_log(cfg, wl, target):
+    """Step log of dynamic-slot sampling from the oracle simulator (per prompt)."""
+    from oracle import simulate_dynamic
+    res = [simulate_dynamic(wl.L[p], cfg.slots_per_prompt, target) for p in range(cfg.num_prompts)]
+    out = []
+    for k in range(max(r.steps for r in res)):
+        row = []
+        for p, r in enumerate(res):
+            for ls in range(cfg.slots_per_prompt):
+                e = r.log[k][ls] if k < r.steps else None
+                row.append(None if e is None else (p, e[0], e[1]))
+        out.append(tuple(row))
+    return out
 
 
 def oracle_log(cfg, wl, policy):

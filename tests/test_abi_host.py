@@ -248,3 +248,32 @@ def test_dry_run_scheduler_policies_full_workload(policy):
     cfg = get_config("qwen3_1p7b_g64")
     wl = Workload(cfg)
     assert plan_steps(cfg, wl.L, policy, wl.L_hat) == _oracle_log(cfg, wl.L, policy, wl.L_hat)
+
+
+def test_dry_run_dynamic_slot_matches_simulator():
+    # Dynamic-slot sampling through the library (FIFO over a stream, stop
+    # after `target` completions per prompt, in-flight samples discarded):
+    # step logs and accepted samples equal the simulator's.
+    from oracle import simulate_dynamic
+    rng = np.random.default_rng(12)
+    for trial in range(40):
+        NP = int(rng.integers(1, 4))
+        m = int(rng.integers(1, 6))
+        target = int(rng.integers(1, 12))
+        n = 4 * target + 10
+        cfg = get_config("tiny_f32").with_(prompt_lens=tuple(int(x) for x in rng.integers(0, 40, NP)),
+                                           samples_per_prompt=n, slots_per_prompt=m, max_suffix_len=40)
+        L = rng.integers(1, 41, size=(NP, n))
+        acc = []
+        log = plan_steps(cfg, L, "fifo", None, stop_after=target, accepted=acc)
+        res = [simulate_dynamic(L[p], m, target) for p in range(NP)]
+        want = []
+        for k in range(max(r.steps for r in res)):
+            row = []
+            for p, r in enumerate(res):
+                for ls in range(m):
+                    e = r.log[k][ls] if k < r.steps else None
+                    row.append(None if e is None else (p, e[0], e[1]))
+            want.append(tuple(row))
+        assert log == want, trial
+        assert acc == [r.accepted for r in res], trial

@@ -8,7 +8,8 @@ accumulation) max abs error; idle slots' rows exactly 0.
 import numpy as np
 import pytest
 
-from tests.gpu_harness import (check_against_oracle, oracle_log, run_gpu_group, sample_steps, say)
+from tests.gpu_harness import (check_against_oracle, oracle_dynamic_log, oracle_log, run_gpu_group, sample_steps,
+                               say)
 from workload import Workload, get_config
 
 pytestmark = pytest.mark.gpu
@@ -75,6 +76,29 @@ def test_bf16_fptas_schedules(policy):
                                              length_dist=("lognormal", 4.0, 1.0, 1, 200), max_suffix_len=200,
                                              pool_rows=None)
     _run_and_check(cfg, policy, split=128, capture=lambda log: sample_steps(log, every=4))
+
+
+def test_bf16_dynamic_slot_stream():
+    # Dynamic-slot sampling (Section 3.2, mode 2): 8 slots draw from a stream
+    # of 60 samples and stop after 16 completions, discarding the samples
+    # still decoding.  Step log equal to the simulator's; device token
+    # counters equal the tokens each sample decoded (discarded ones included).
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(250,), samples_per_prompt=60,
+                                             slots_per_prompt=8, length_dist=("lognormal", 3.5, 1.0, 1, 150),
+                                             max_suffix_len=150, pool_rows=None)
+    wl = Workload(cfg)
+    want = oracle_dynamic_log(cfg, wl, 16)
+    _, log, steps, captured, tokens, _ = run_gpu_group(cfg, "fifo", wl=wl, split=128, stop_after=16,
+                                                       capture=lambda k: k % 3 == 0 or k == len(want) - 1)
+    assert log == want and steps == len(want)
+    counts = np.zeros_like(wl.L)
+    for row in log:
+        for e in row:
+            if e is not None:
+                counts[e[0], e[1]] += 1
+    assert np.array_equal(tokens, counts)
+    worst, n = check_against_oracle(cfg, wl, log, captured)
+    say(f"  [dynamic-slot] {steps} steps, checked {n} outputs, max abs err {worst:.3g}")
 
 
 def test_bf16_single_slot_wave_prefix():

@@ -17,7 +17,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle import FPTAS_EPSILON, POLICIES, fptas_assign, simulate, simulate_group
+from oracle import FPTAS_EPSILON, POLICIES, fptas_assign, simulate, simulate_dynamic, simulate_group
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "sim_worked_example.json")
 
@@ -256,3 +256,49 @@ def test_lpt_on_true_lengths_within_graham_bound_of_optimum():
         opt = _optimum(list(L), m)
         lpt = simulate(L, m, "lpt", pred=L.astype(float)).steps
         assert opt <= lpt <= (4 / 3 - 1 / (3 * m)) * opt + 1e-9
+
+
+def test_dynamic_golden_case():
+    g = json.load(open(GOLDEN))["dynamic_case"]
+    r = simulate_dynamic(g["stream"], g["m"], g["target"])
+    assert r.steps == g["steps"]
+    assert r.accepted == g["accepted"]
+    assert r.mean_length * g["mean_length_den"] == g["mean_length_num"]
+    assert [tuple(None if e is None else tuple(e) for e in row) for row in g["log"]] == r.log
+
+
+def test_dynamic_closed_forms():
+    rng = np.random.default_rng(9)
+    for _ in range(300):
+        n = int(rng.integers(1, 30))
+        L = rng.integers(1, 20, size=n + 40)
+        r = simulate_dynamic(L, 1, n)               # one slot: the stream in order
+        assert r.steps == int(L[:n].sum()) and r.accepted == list(range(n))
+        c, m = int(rng.integers(1, 9)), int(rng.integers(1, 6))
+        r = simulate_dynamic([c] * (n + m), m, n)   # equal lengths: rounds of m
+        assert r.steps == c * math.ceil(n / m)
+        assert r.accepted == list(range(n)) and r.mean_length == c
+
+
+def test_dynamic_event_driven_and_bounded_by_fifo():
+    # Independent list schedule of the stream (earliest free slot, lowest slot
+    # on ties): the accepted samples are the first `target` by (finish, slot),
+    # and the stop step is the target-th finish.  Dynamic-slot needs no more
+    # steps than FIFO over the first `target` samples: it dispatches those in
+    # the same order at the same times.
+    rng = np.random.default_rng(10)
+    for _ in range(1000):
+        target = int(rng.integers(1, 14))
+        m = int(rng.integers(1, 6))
+        L = rng.integers(1, 25, size=4 * target + 8)
+        r = simulate_dynamic(L, m, target)
+        heap = [(0, s) for s in range(m)]
+        fin = []
+        for i in range(len(L)):
+            free, s = heapq.heappop(heap)
+            fin.append((free + int(L[i]), s, i))
+            heapq.heappush(heap, (free + int(L[i]), s))
+        fin.sort()
+        assert r.steps == fin[target - 1][0]
+        assert r.accepted == [i for _, _, i in fin[:target]]
+        assert r.steps <= simulate(L[:target], m, "fifo").steps

@@ -8,7 +8,7 @@ without sharing any of the method's code.
 
 from .configs import CONFIGS, GroupConfig, get_config
 from .gen import (SCHEDULER_STUDY, Workload, bf16_bits_to_f64, f32_to_bf16_bits, scheduler_study_lengths,
-                  splitmix64)
+                  scheduler_study_stream, splitmix64)
 
 __all__ = [
     "CONFIGS",
@@ -19,5 +19,6 @@ __all__ = [
     "bf16_bits_to_f64",
     "f32_to_bf16_bits",
     "scheduler_study_lengths",
+    "scheduler_study_stream",
     "splitmix64",
 ]

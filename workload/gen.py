@@ -210,3 +210,11 @@ def scheduler_study_lengths(mu, sigma, n_groups, G, cap=1024, pred_sigma=0.2, se
     L = np.clip(np.rint(np.exp(rng.normal(mu, sigma, size=(n_groups, G)))), 1, cap).astype(np.int32)
     noise = np.random.Generator(np.random.PCG64(6000 + seed)).normal(0.0, pred_sigma, size=L.shape)
     return L, L.astype(np.float64) * np.exp(noise)
+
+
+def scheduler_study_stream(mu, sigma, L, extra, cap=1024, seed=0):
+    """Per group, a dynamic-slot stream: the group's own lengths L[n] followed
+    by `extra` more draws of the same distribution (PCG64(7000 + seed))."""
+    rng = np.random.Generator(np.random.PCG64(7000 + seed))
+    more = np.clip(np.rint(np.exp(rng.normal(mu, sigma, size=(L.shape[0], extra)))), 1, cap).astype(np.int32)
+    return np.concatenate([L, more], axis=1)
