@@ -198,7 +198,7 @@ def algorithmic_bytes(cfg, steplog):
 
 
 class Bench:
-    def __init__(self, cfg_name, split=0):
+    def __init__(self, cfg_name, split=0, reuse=0):
         import numpy as np
         import torch
 
@@ -213,15 +213,21 @@ class Bench:
         self.cfg = cfg
         t0 = time.time()
         self.wl = wl = Workload(cfg)
-        self.log = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
-        self.naive_steps = len(plan_steps(cfg, wl.L, "naive", wl.L_hat))
+        self.reuse = reuse
+        self.plog = []
+        self.log = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat, reuse=reuse, probe_log=self.plog)
+        self.naive_steps = len(plan_steps(cfg, wl.L, "naive", wl.L_hat, reuse=reuse))
         dev = DeviceInputs(wl)
         self.prefix = [[dev.prefix(l, p) for l in range(cfg.layers)] for p in range(cfg.num_prompts)]
         self.q, self.k, self.v = dev.stage(self.log, 0, len(self.log))
+        if reuse:
+            self.pq, self.pk, self.pv = dev.stage(self.plog, 0, len(self.plog))
+            self.po = torch.empty((cfg.layers,) + tuple(self.pq.shape[2:4]) + (cfg.head_dim,), dtype=torch.float32,
+                                  device="cuda")
         del dev
         torch.cuda.synchronize()
         self.stream = torch.cuda.current_stream()
-        self.ctx = context_for(cfg, stream=self.stream, split_tokens=split)
+        self.ctx = context_for(cfg, stream=self.stream, split_tokens=split, probe_tokens=reuse)
         L, S, Hq, Hkv, d, es = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.elem_bytes
         self.o = torch.empty((L, S, Hq, d), dtype=torch.float32, device="cuda")
         self.qp, self.kp, self.vp, self.op = (self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(),
@@ -230,6 +236,7 @@ class Bench:
         self.L = L
         self.tokens = wl.total_tokens
         self.alg_bytes = algorithmic_bytes(cfg, self.log)
+        self.probe_alg_bytes = algorithmic_bytes(cfg, self.plog) if reuse else 0.0
         log(f"setup {time.time() - t0:.1f}s: {len(self.log)} steps ({cfg.policy}) vs {self.naive_steps} naive, "
             f"{self.tokens} tokens, staged {(self.q.numel() + self.k.numel() + self.v.numel()) * es / 2**30:.1f} GiB")
 
@@ -237,18 +244,38 @@ class Bench:
         j = k * self.L + layer
         return (self.qp + j * self.sq, self.kp + j * self.skv, self.vp + j * self.skv, self.op + layer * self.so)
 
-    def group_decode(self):
-        """One benchmark step: prefill every layer, then decode the whole group."""
-        from paper_2506_22950_amd.group import decode_group, schedulers_for
+    def provide_probe(self, j, p, first, n, layer):
+        return (self.pq[j, layer].data_ptr(), self.pk[j, layer].data_ptr(), self.pv[j, layer].data_ptr(),
+                self.po[layer].data_ptr())
 
+    def prefill(self):
         cfg, ctx = self.cfg, self.ctx
         ctx.reset()
         for p in range(cfg.num_prompts):
             for layer in range(cfg.layers):
                 k, v = self.prefix[p][layer]
                 ctx.prefill_shared(p, layer, cfg.prompt_lens[p], k, v)
-        return decode_group(ctx, schedulers_for(cfg, cfg.policy, self.wl.L_hat), self.wl.L, cfg.layers,
-                            self.provide)
+
+    def probe(self):
+        """The probe phase of prefix reuse (nothing without it)."""
+        from paper_2506_22950_amd.group import probe_group
+
+        if self.reuse:
+            probe_group(self.ctx, self.wl.L, self.reuse, self.cfg.layers, self.provide_probe)
+
+    def decode(self):
+        from paper_2506_22950_amd.group import decode_group, schedulers_for
+
+        cfg = self.cfg
+        return decode_group(self.ctx, schedulers_for(cfg, cfg.policy, self.wl.L_hat), self.wl.L, cfg.layers,
+                            self.provide, reuse=self.reuse)
+
+    def group_decode(self):
+        """One benchmark step: prefill every layer, the probe phase (with prefix
+        reuse), then decode the whole group."""
+        self.prefill()
+        self.probe()
+        return self.decode()
 
     def check_bookkeeping(self, steps):
         np = self.np
@@ -259,13 +286,24 @@ class Bench:
     def kernel_timing(self):
         """One more whole group decode with kernel timing on: the summed device
         wall-clock time of the decode launches (first block start to last block
-        end of each), and the HIP-event time of the whole pass on the
-        library's stream."""
+        end of each), and the HIP-event time of the decode pass on the
+        library's stream.  With prefix reuse the probe launches are timed in a
+        pass of their own: returns (decode timing, probe timing or None), each
+        (ms, region_ms, launches, library alg bytes, library launches)."""
+        self.prefill()
+        probe = None
+        if self.reuse:
+            self.ctx.timing_begin()
+            self.probe()
+            ms, region_ms, n = self.ctx.timing_end()
+            st = self.ctx.get_stats()
+            probe = (ms, region_ms, n, st.alg_bytes, st.launches)
+        before = self.ctx.get_stats()
         self.ctx.timing_begin()
-        self.group_decode()
+        self.decode()
         ms, region_ms, n = self.ctx.timing_end()
         st = self.ctx.get_stats()
-        return ms, region_ms, n, st.alg_bytes, st.launches
+        return (ms, region_ms, n, st.alg_bytes - before.alg_bytes, st.launches - before.launches), probe
 
 
 def cpu_baseline(bench, budget_s=15.0):
@@ -317,6 +355,8 @@ def main():
     ap.add_argument("--split", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--reuse", type=int, default=0, metavar="K",
+                    help="prefix reuse: every sample decodes K probe tokens first (Section 4); default 0")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -340,7 +380,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         copy_calibration(torch)
-    b = Bench(args.workload, split=args.split)
+    b = Bench(args.workload, split=args.split, reuse=args.reuse)
 
     for w in range(args.warmup):
         t0 = time.time()
@@ -359,19 +399,20 @@ def main():
     ms_per_step = elapsed * 1000.0 / args.steps
     value = b.tokens * args.steps / elapsed
     log(f"timed {args.steps} group decodes: {ms_per_step:.1f} ms each, {value:.0f} tokens/s, "
-        f"end-to-end {b.alg_bytes / (ms_per_step / 1e3) / 1e9:.0f} GB/s algorithmic")
+        f"end-to-end {(b.alg_bytes + b.probe_alg_bytes) / (ms_per_step / 1e3) / 1e9:.0f} GB/s algorithmic")
 
-    roof = None
+    roof, probe = None, None
     if not args.no_kernel_timing:
-        ms, region_ms, n, alg, launches = b.kernel_timing()
+        (ms, region_ms, n, alg, launches), ptiming = b.kernel_timing()
         assert n == launches, (n, launches)
         rel = abs(alg - b.alg_bytes) / b.alg_bytes
         assert rel < 1e-9, f"library and step-log byte counts differ: {alg} vs {b.alg_bytes}"
         avg_us = ms * 1000.0 / n
         per_launch = alg / n
         achieved = per_launch / (avg_us * 1e-6) / 1e9
+        traffic = read_traffic(args.workload) if not args.reuse else None
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": read_traffic(args.workload),
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
                 "alg_bytes_per_launch": round(per_launch),
                 "timing": "device wall clock, first block start to last block end, every launch of one group decode",
@@ -379,6 +420,19 @@ def main():
                 "event_us_per_launch": round(region_ms * 1000.0 / n, 3)}
         log(f"kernel: {n} launches, avg {avg_us:.2f} us, {per_launch / 1e6:.2f} MB/launch -> {achieved:.0f} GB/s; "
             f"HIP-event region {region_ms:.1f} ms = {region_ms * 1000.0 / n:.2f} us per launch")
+        if ptiming is not None:
+            pms, pregion, pn, palg, plaunch = ptiming
+            assert pn == plaunch, (pn, plaunch)
+            assert abs(palg - b.probe_alg_bytes) <= 1e-9 * b.probe_alg_bytes, (palg, b.probe_alg_bytes)
+            pavg = pms * 1000.0 / pn
+            pper = palg / pn
+            pach = pper / (pavg * 1e-6) / 1e9
+            probe = {"kernel": "decode_kernel (probe launches, %d rows per KV head)" % (b.ctx.probe_batch *
+                                                                                      b.cfg.hpk),
+                     "probe_tokens": args.reuse, "launches": pn, "avg_launch_us": round(pavg, 3),
+                     "alg_bytes_per_launch": round(pper), "achieved": round(pach, 1), "unit": "GB/s",
+                     "frac": round(pach / PEAK_HBM_GBS, 4), "phase_ms": round(pregion, 2)}
+            log(f"probe: {pn} launches, avg {pavg:.2f} us, {pper / 1e6:.2f} MB/launch -> {pach:.0f} GB/s")
 
     cpu = None if args.no_cpu_baseline else cpu_baseline(b)
     cfg = b.cfg
@@ -402,9 +456,11 @@ def main():
             "m": cfg.slots_per_prompt, "policy": cfg.policy, "decode_steps": len(b.log),
             "naive_decode_steps": b.naive_steps, "generated_tokens": b.tokens,
             "alg_bytes_per_group": round(b.alg_bytes),
-            "end_to_end_alg_GBps": round(b.alg_bytes / (ms_per_step / 1e3) / 1e9, 1),
+            "end_to_end_alg_GBps": round((b.alg_bytes + b.probe_alg_bytes) / (ms_per_step / 1e3) / 1e9, 1),
+            "probe_tokens": args.reuse, "probe_steps": len(b.plog),
         },
         "roofline": roof,
+        "probe": probe,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define INFS_ABI_VERSION 1
+#define INFS_ABI_VERSION 2
 
 typedef enum infs_status {
     INFS_OK = 0,
@@ -99,7 +99,8 @@ typedef struct infs_config {
     int32_t max_prompt_len;      /* capacity of the shared prefix per prompt, >= 0 */
     int32_t max_suffix_len;      /* capacity of one response, >= 1 */
     int32_t page_tokens;         /* tokens per response page; 0 or 16 */
-    int32_t num_pages;           /* response page pool size; 0: enough for every slot at capacity */
+    int32_t num_pages;           /* response page pool size; 0: enough for every slot at capacity, plus
+                                    every sample's probe tokens */
     int32_t split_tokens;        /* split-K chunk length of responses in tokens; 0: 256; a multiple of 128
                                     up to 4096.  Prefixes are split in 128-token chunks when they run on
                                     MFMA tiles, else in split_tokens chunks; prefix plus response chunks
@@ -107,6 +108,8 @@ typedef struct infs_config {
     int32_t dtype;               /* infs_dtype of Q, K, V */
     float scale;                 /* softmax scale; 0: 1/sqrt(head_dim) */
     uint32_t flags;              /* INFS_FLAG_* */
+    int32_t probe_tokens;        /* prefix reuse (Section 4): k probe tokens every sample decodes before it
+                                    is dispatched (infs_probe_step); 0 = no probe phase.  In [0, max_suffix_len] */
 } infs_config;
 
 typedef struct infs_ctx infs_ctx;
@@ -114,9 +117,9 @@ typedef struct infs_ctx infs_ctx;
 /* Totals since creation or the last infs_reset (host-side counts). */
 typedef struct infs_stats {
     int64_t steps;               /* infs_end_step calls */
-    int64_t launches;            /* attention kernel launches (one per decode_step) */
-    int64_t tokens;              /* tokens generated (live slots summed over steps) */
-    double alg_bytes;            /* algorithmic HBM bytes of all decode_step launches: prefix K/V
+    int64_t launches;            /* attention kernel launches (one per decode_step or probe_step) */
+    int64_t tokens;              /* tokens generated (live slots summed over steps, probe tokens included) */
+    double alg_bytes;            /* algorithmic HBM bytes of all decode_step and probe_step launches: prefix K/V
                                     once per prompt with a live slot, each live slot's response K/V,
                                     new K/V read and append write, Q read, O write */
     double alg_flops;            /* 4 * Hq * d * (P + t) per live slot and layer */
@@ -146,13 +149,53 @@ infs_status infs_prefill_shared(infs_ctx* ctx, int32_t prompt, int32_t layer, in
                                 const void* k_dev, const void* v_dev);
 
 /* Give empty slot `slot` the sample `sample_id` of `prompt` (which must be slot / m).  The sample
-   starts with an empty response and decodes its first token at the next decode step.
+   starts with the probe tokens it decoded in the probe phase (none without probe_tokens): its
+   KV pages are reused, and it decodes its next token at the next decode step (Section 4,
+   prefix reuse: decoding resumes at token k+1).
    E_STATE: slot is live, or a step is open.  E_DUP: sample_id already dispatched for this prompt. */
 infs_status infs_refill_slot(infs_ctx* ctx, int32_t slot, int32_t prompt, int64_t sample_id);
 
 /* Release a live slot: its response pages return to the pool (the sample's buffer is recycled on
    completion, Section 3.2).  E_STATE: slot is empty, or a step is open. */
 infs_status infs_retire_slot(infs_ctx* ctx, int32_t slot);
+
+/* ---------------------------------------------------------------------------------------------
+ * Probe phase of prefix reuse (Section 4, "Prefix Reuse Optimization"; contexts with
+ * probe_tokens = k > 0).  Before the decode, every sample decodes its first k tokens against the
+ * shared prompt so that its length can be predicted from them; the KV of those tokens is kept, and
+ * a sample dispatched later resumes at token k+1 (infs_refill_slot).  A probe step decodes one
+ * token for a batch of samples of one prompt through every layer, like a decode step whose slots
+ * are the batch's samples: all n*hpk query rows of a KV head share each prefix K/V byte.
+ * ------------------------------------------------------------------------------------------- */
+
+/* One layer of a probe step for samples first_sample .. first_sample+n-1 of `prompt`.
+   live_host: n bytes, nonzero = the sample appends its next probe token (at position = its probe
+   length) and attends over [prefix ; its probe tokens]; zero = idle (O rows written 0).  NULL = all
+   live.  q_dev [n, Hq, d], k_new_dev / v_new_dev [n, Hkv, d] (context dtype), o_dev [n, Hq, d] fp32,
+   all 16-byte aligned.  1 <= n <= the probe batch (min(64, G, R / hpk) with R = 128 on MFMA tiles,
+   16 otherwise).  Every layer once per probe step, each with the same batch; close with
+   infs_end_probe_step.  E_STATE: a decode step is open, the batch differs from the open probe
+   step's, the layer was already probed, a live sample was already dispatched or released, or its
+   prompt is not prefilled for the layer.  E_CAPACITY: a live sample already has k probe tokens, or
+   the page pool is empty. */
+infs_status infs_probe_step(infs_ctx* ctx, int32_t layer, int32_t prompt, int32_t first_sample, int32_t n,
+                            const uint8_t* live_host, const void* q_dev, const void* k_new_dev,
+                            const void* v_new_dev, float* o_dev);
+
+/* Close the probe step: every live sample's probe length grows by one.  E_STATE unless every layer
+   was probed exactly once. */
+infs_status infs_end_probe_step(infs_ctx* ctx);
+
+/* Largest n of infs_probe_step (0 without a probe phase; -1 for a NULL context). */
+int32_t infs_probe_batch(const infs_ctx* ctx);
+
+/* Probe tokens decoded so far by a sample (0 without a probe phase). */
+infs_status infs_probe_state(const infs_ctx* ctx, int32_t prompt, int64_t sample_id, int32_t* probe_len);
+
+/* A sample that will not be dispatched (for instance, it finished within its probe tokens) returns
+   its probe pages to the pool and can no longer be dispatched.  E_STATE without a probe phase or
+   while a step is open; E_DUP if it was already dispatched or released. */
+infs_status infs_release_sample(infs_ctx* ctx, int32_t prompt, int64_t sample_id);
 
 /* One layer of one running step for every slot:
    live slots append this step's K/V (position = current length) to their response, then attend
@@ -182,8 +225,8 @@ infs_status infs_sync(infs_ctx* ctx);
 
 infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
 
-/* Kernel timing.  Between begin and end every decode_step launch records, on the device wall
-   clock, the start of its first work-group and the end of its last one.  infs_timing_end
+/* Kernel timing.  Between begin and end every decode_step and probe_step launch records, on the
+   device wall clock, the start of its first work-group and the end of its last one.  infs_timing_end
    synchronises and returns the summed kernel time (ms) of the timed launches, their number, and
    the time between the two calls measured by HIP events on the context's stream (region_ms,
    which also covers gaps between launches and any other work on the stream). */

@@ -104,8 +104,16 @@ class SimResult:
     finish_step: np.ndarray                  # step at which each sample produced its last token
 
 
-def simulate(L, m: int, policy: str, pred=None) -> SimResult:
-    """Simulate one prompt's group of G = len(L) samples on m slots."""
+def simulate(L, m: int, policy: str, pred=None, reuse: int = 0) -> SimResult:
+    """Simulate one prompt's group of G = len(L) samples on m slots.
+
+    reuse = k > 0: prefix reuse (Section 4).  Every sample has already decoded
+    min(L_i, k) probe tokens before the first step; a dispatched sample
+    resumes at token k+1 and holds its slot for L_i - k steps, and a sample
+    with L_i <= k finished in the probe phase: when the policy picks it, it is
+    counted as finished at once and the slot asks the policy again.  Log
+    entries carry the response length including the probe tokens.
+    """
     L = [int(x) for x in L]
     G = len(L)
     if m < 1:
@@ -114,6 +122,8 @@ def simulate(L, m: int, policy: str, pred=None) -> SimResult:
         raise ValueError("every sample has at least one token")
     if policy not in POLICIES:
         raise ValueError(f"unknown policy {policy!r}")
+    if reuse < 0:
+        raise ValueError("reuse must be >= 0")
     if policy in NEEDS_PRED:
         if pred is None:
             raise ValueError(f"{policy} needs predicted lengths")
@@ -128,64 +138,66 @@ def simulate(L, m: int, policy: str, pred=None) -> SimResult:
     started = [False] * m         # fptas_sjf: slot has had its initial fill
 
     slot_sample = [None] * m      # sample id held by each slot, or None
-    slot_len = [0] * m            # tokens generated so far by that sample
+    slot_len = [0] * m            # tokens of that sample so far (probe tokens included)
     pending = set(range(G))       # not yet dispatched
     row_next = list(range(m))     # fixed_row: next sample id of each slot
-    naive_next = 0                # naive: first id of the next micro group
+    naive = {"next": 0, "left": 0}  # naive: next id, ids left in the open micro group
     tokens = np.zeros(G, dtype=np.int64)
     finish = np.full(G, -1, dtype=np.int64)
     log = []
     dispatch = []
     step = 0
 
-    def fill():
-        nonlocal naive_next
+    def pick(s):
+        """The policy's next sample for empty slot s, or None."""
         if policy == "naive":
-            if any(x is not None for x in slot_sample) or naive_next >= G:
-                return
-            for s in range(m):
-                if naive_next < G:
-                    give(s, naive_next)
-                    naive_next += 1
-            return
-        for s in range(m):
-            if slot_sample[s] is not None:
-                continue
-            if policy == "fixed_row":
-                j = row_next[s]
-                if j >= G:
-                    continue
-                row_next[s] = j + m
-            elif policy == "fptas":
-                if bin_next[s] >= len(bins[s]):
-                    continue
-                j = bins[s][bin_next[s]]
-                bin_next[s] += 1
-            elif policy == "fifo":
-                if not pending:
-                    return
-                j = min(pending)
-            elif policy == "lpt":
-                if not pending:
-                    return
-                j = min(pending, key=lambda i: (-pred[i], i))
-            else:  # sjf, fptas_sjf
-                if not pending:
-                    return
-                j = None
-                if policy == "fptas_sjf" and not started[s]:
-                    started[s] = True
-                    if bins[s] and bins[s][0] in pending:
-                        j = bins[s][0]
-                if j is None:
-                    j = min(pending, key=lambda i: (pred[i], i))
-            give(s, j)
+            if naive["left"] == 0 and all(x is None for x in slot_sample) and naive["next"] < G:
+                naive["left"] = min(m, G - naive["next"])
+            if naive["left"] == 0:
+                return None
+            j = naive["next"]
+            naive["next"] += 1
+            naive["left"] -= 1
+            return j
+        if policy == "fixed_row":
+            j = row_next[s]
+            if j >= G:
+                return None
+            row_next[s] = j + m
+            return j
+        if policy == "fptas":
+            if bin_next[s] >= len(bins[s]):
+                return None
+            j = bins[s][bin_next[s]]
+            bin_next[s] += 1
+            return j
+        if not pending:
+            return None
+        if policy == "fifo":
+            return min(pending)
+        if policy == "lpt":
+            return min(pending, key=lambda i: (-pred[i], i))
+        if policy == "fptas_sjf" and not started[s]:
+            started[s] = True
+            if bins[s] and bins[s][0] in pending:
+                return bins[s][0]
+        return min(pending, key=lambda i: (pred[i], i))
 
-    def give(s, j):
-        pending.discard(j)
-        slot_sample[s] = j
-        slot_len[s] = 0
-        dispatch.append((step, s, j))
+    def fill():
+        for s in range(m):
+            while slot_sample[s] is None:
+                j = pick(s)
+                if j is None:
+                    break
+                pending.discard(j)
+                dispatch.append((step, s, j))
+                pre = min(L[j], reuse)
+                tokens[j] = pre
+                if pre == L[j]:          # finished within its probe tokens
+                    finish[j] = step
+                    continue
+                slot_sample[s] = j
+                slot_len[s] = pre
 
     fill()
     while any(x is not None for x in slot_sample):
@@ -209,7 +221,7 @@ def simulate(L, m: int, policy: str, pred=None) -> SimResult:
     return SimResult(steps=step, log=log, tokens=tokens, dispatch=dispatch, finish_step=finish)
 
 
-def simulate_group(L, m: int, policy: str, pred=None):
+def simulate_group(L, m: int, policy: str, pred=None, reuse: int = 0):
     """Several prompts decoded in one batch, each with its own m slots and
     pending pool.  A step advances every prompt; the batch ends when the last
     prompt's group is done.  Returns (total steps, per-prompt SimResults)."""
@@ -218,7 +230,7 @@ def simulate_group(L, m: int, policy: str, pred=None):
         L = L[None, :]
     if pred is not None:
         pred = np.asarray(pred).reshape(L.shape)
-    res = [simulate(L[p], m, policy, None if pred is None else pred[p]) for p in range(L.shape[0])]
+    res = [simulate(L[p], m, policy, None if pred is None else pred[p], reuse) for p in range(L.shape[0])]
     return max(r.steps for r in res), res
 
 

@@ -123,15 +123,18 @@ struct Shape {
   static constexpr int NB = PR / 16;               // MFMA row blocks
   static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
   static constexpr int DB = D / 16;                // MFMA 16-wide head_dim blocks
+  // More than 64 MFMA rows: each wavefront owns a quarter of the rows and
+  // walks the whole chunk, so the four need no combine.
+  static constexpr bool ROWSPLIT = MFMA && PR > 64;
   static constexpr int WAVE_NR = (!MFMA && PR > HPK) ? PR : HPK;
   static constexpr int WAVE_SMEM = 4 * WAVE_NR * (D + 2);
-  static constexpr int MFMA_SLOT = MFMA ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
+  static constexpr int MFMA_SLOT = (MFMA && !ROWSPLIT) ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
   static constexpr int MFMA_SMEM = 4 * MFMA_SLOT;
   static constexpr int SMEM = WAVE_SMEM > MFMA_SMEM ? WAVE_SMEM : MFMA_SMEM;
   // 64 MFMA rows keep 128 accumulator registers live, and 16 wavefront rows
   // as many: those shapes run 1 wavefront per SIMD rather than spill; every
   // other shape runs 2 per SIMD.
-  static constexpr int MIN_WAVES = ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
+  static constexpr int MIN_WAVES = ROWSPLIT ? 2 : ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
   static_assert(LPT >= 2 && LPT <= 64, "row size");
   static_assert(!MFMA || BF, "MFMA path is bf16");
   static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
@@ -607,6 +610,76 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
 }
 
 // ----------------------------------------------------------------------------
+// Prefix chunk on MFMA tiles with more than 64 rows (e.g. the probe phase of
+// prefix reuse, where every sample of the group shares the prefix): wavefront
+// w owns row tiles w*NBW .. w*NBW+NBW-1 and walks every 32-token block of the
+// chunk (the other wavefronts' reads of the same blocks hit the cache), then
+// stores its rows' partial directly.
+// ----------------------------------------------------------------------------
+template <class SH>
+__device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
+  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
+  constexpr int NBW = SH::NB / kWaves;
+  static_assert(SH::NB % kWaves == 0, "row tiles per wavefront");
+  using WS = Shape<true, D, HPK, true, NBW * 16>;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
+  const int plen = a.prompt[p].plen;
+  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
+  const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
+  const float sl2 = a.scale_log2;
+
+  bf16x8 bq[NBW][KB];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    const int row = (w * NBW + nb) * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
+    const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
+    const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) bq[nb][kb] = ok ? *(const bf16x8*)(qr + kb * 32 + q4 * 8) : bf16x8{};
+  }
+  f32x4 acc[NBW][DB];
+  float mrow[NBW], lrow[NBW];
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    mrow[nb] = NEG_INF;
+    lrow[nb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const uint16_t* head = (const uint16_t*)a.prefix +
+                         ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D);
+  for (int b = 0; b < nblk; ++b) {
+    bf16x8 ka[2][KB], va[DB];
+    const uint16_t* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D);
+    const uint16_t* vblk = kblk + kMfmaBlock * D;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = *(const bf16x8*)(kblk + ((mb * KB + kb) * 64 + lane) * 8);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
+    mfma_block<WS>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
+  }
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    lrow[nb] += __shfl_xor(lrow[nb], 16);
+    lrow[nb] += __shfl_xor(lrow[nb], 32);
+  }
+  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
+#pragma unroll
+  for (int nb = 0; nb < NBW; ++nb) {
+    const int64_t rec = rec0 + (w * NBW + nb) * 16 + r16;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
+    if (q4 == 0) {
+      st_coherent(a.ws_ml + rec * 2 + 0, mrow[nb]);
+      st_coherent(a.ws_ml + rec * 2 + 1, lrow[nb]);
+    }
+  }
+}
+
+// ----------------------------------------------------------------------------
 // Response chunk of one live slot (hpk rows), plus the append of this step's
 // K/V when the chunk holds the newest position.
 // ----------------------------------------------------------------------------
@@ -622,7 +695,7 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   // Page indices of this wavefront's range (lane i: the i-th 16-token group) and
   // the query rows, loaded together.
   const int npg = (wt1 - wt0 + kPageTokens - 1) / kPageTokens;
-  const int32_t* ptab = a.page_table + (int64_t)s * a.pages_per_slot + (wt0 >> 4);
+  const int32_t* ptab = a.page_table + (int64_t)sp.seq * a.pages_per_slot + (wt0 >> 4);
   const int pages = lane < npg ? ptab[lane] : 0;
   u32x4 q[HPK];
 #pragma unroll
@@ -656,7 +729,7 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
 
   if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
     const int pos = len - 1;
-    a.page_table[(int64_t)s * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
+    a.page_table[(int64_t)sp.seq * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
     if (a.count_tokens)
       __hip_atomic_fetch_add(&a.tokens[(s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -824,7 +897,9 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     while (p < a.num_prompts - 1 && !(a.prompt[p].nchunks > 0 && item < a.prompt[p].item_begin + a.prompt[p].nchunks))
       ++p;
     const int c = item - a.prompt[p].item_begin;
-    if constexpr (SH::MFMA)
+    if constexpr (SH::ROWSPLIT)
+      prefix_mfma_rows<SH>(a, p, c, g);
+    else if constexpr (SH::MFMA)
       prefix_mfma<SH>(a, p, c, g, smem);
     else
       prefix_wave<SH>(a, p, c, g, smem);
@@ -962,18 +1037,25 @@ struct Entry {
   X(true, 64, 2, false, 8)   \
   X(true, 64, 2, true, 16)   \
   X(true, 64, 2, true, 32)   \
+  X(true, 64, 2, true, 64)   \
+  X(true, 64, 2, true, 128)  \
   X(true, 128, 1, false, 8)  \
   X(true, 128, 1, true, 16)  \
+  X(true, 128, 1, true, 32)  \
+  X(true, 128, 1, true, 64)  \
   X(true, 128, 2, false, 8)  \
   X(true, 128, 2, false, 16) \
   X(true, 128, 2, true, 16)  \
   X(true, 128, 2, true, 32)  \
   X(true, 128, 2, true, 64)  \
+  X(true, 128, 2, true, 128) \
   X(true, 128, 4, false, 16) \
   X(true, 128, 4, true, 16)  \
   X(true, 128, 4, true, 32)  \
   X(true, 128, 4, true, 64)  \
-  X(true, 128, 8, true, 64)
+  X(true, 128, 4, true, 128) \
+  X(true, 128, 8, true, 64)  \
+  X(true, 128, 8, true, 128)
 
 #define INFS_ENTRY(bf, d, hpk, mf, pr) \
   {{bf, d, hpk, mf, pr}, decode_kernel<Shape<bf, d, hpk, mf, pr>>, Shape<bf, d, hpk, mf, pr>::SMEM},
@@ -991,13 +1073,15 @@ const Entry* find_entry(const KernelKey& k) {
 }  // namespace
 
 bool select_kernel(int bf16, int head_dim, int hpk, int rows, KernelKey* key) {
-  KernelKey k{bf16, head_dim, hpk, 0, 0};
-  if (bf16 && rows >= 16) {
-    k.mfma = 1;
-    k.prefix_rows = rows <= 16 ? 16 : rows <= 32 ? 32 : rows <= 64 ? 64 : 0;
-  } else {
+  return select_kernel_path(bf16, head_dim, hpk, rows, bf16 && rows >= 16, key);
+}
+
+bool select_kernel_path(int bf16, int head_dim, int hpk, int rows, int mfma, KernelKey* key) {
+  KernelKey k{bf16, head_dim, hpk, mfma && bf16 ? 1 : 0, 0};
+  if (k.mfma)
+    k.prefix_rows = rows <= 16 ? 16 : rows <= 32 ? 32 : rows <= 64 ? 64 : rows <= 128 ? 128 : 0;
+  else
     k.prefix_rows = rows <= 8 ? 8 : rows <= 16 ? 16 : 0;
-  }
   if (k.prefix_rows == 0 || !find_entry(k)) return false;
   *key = k;
   return true;

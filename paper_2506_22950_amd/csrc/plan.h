@@ -8,10 +8,11 @@
 
 namespace infs {
 
-constexpr int kMaxSlots = 64;      // S = num_prompts * slots_per_prompt
+constexpr int kMaxSlots = 64;      // S = num_prompts * slots_per_prompt; also the largest probe batch
 constexpr int kMaxPrompts = 16;
 constexpr int kPageTokens = 16;    // tokens per response page
 constexpr int kBlockThreads = 256; // 4 wavefronts of 64
+constexpr int kWaves = kBlockThreads / 64;
 constexpr int kMfmaBlock = 32;     // prefix tokens per MFMA block
 constexpr int kMfmaPrefixSplit = 4 * kMfmaBlock;  // MFMA prefix chunk: one block per wavefront
 constexpr int kMaxPartials = 128;  // prefix + response chunks merged for one slot
@@ -35,7 +36,8 @@ struct SlotPlan {
   int32_t cur_page;    // page holding position len-1 (where this step's K/V go)
   int32_t sample;      // sample id (token counters)
   int32_t target;      // response-arrival counter value once this launch's chunks of the slot arrived
-  int32_t pad_[3];
+  int32_t seq;         // page-table row of the sample's response (a sequence handle)
+  int32_t pad_[2];
 };
 
 struct PromptPlan {
@@ -54,7 +56,7 @@ struct StepArgs {
   // library buffers (already offset to this layer)
   const void* prefix;  // shared-prefix store of this layer
   void* pool;          // response page pool of this layer
-  int32_t* page_table; // [S, pages_per_slot]
+  int32_t* page_table; // [sequence handles][pages_per_slot]
   float* ws_o;         // partial outputs   [..., d]
   float* ws_ml;        // partial (max, sum) [..., 2]
   int32_t* counters;   // arrival counters, kCounterStride apart: [num_prompts][Hkv] prefix chunks,

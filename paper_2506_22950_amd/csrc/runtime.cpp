@@ -66,13 +66,34 @@ struct infs_ctx {
   std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
   std::vector<int64_t> slot_sample;                // -1: empty
   std::vector<int32_t> slot_len;
-  std::vector<std::vector<int32_t>> slot_pages;    // host copy of each slot's page list
+  // Sequence handles: each live response has a page-table row.  Without probes
+  // the handle of a slot's response is the slot; with probes (prefix reuse)
+  // it is prompt * G + sample, so a sample keeps its probe pages when it is
+  // dispatched.
+  int H = 0;
+  std::vector<int32_t> slot_handle;                // -1: empty slot
+  std::vector<std::vector<int32_t>> seq_pages;     // host copy of each handle's page list
   std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_pages;
   std::vector<std::vector<uint8_t>> dispatched;    // [prompt][G]
   // Arrivals each device counter has been sent so far (the same for every KV
   // head): prefix counters per prompt, response counters per slot.
   std::vector<uint32_t> prefix_arrivals, suffix_arrivals;
   bool step_open = false;
+  // Probe phase of prefix reuse.
+  int probe_k = 0;                                 // probe tokens per sample (0: no prefix reuse)
+  int probe_batch = 0;                             // most samples per probe launch
+  KernelKey pkey{};                                // kernel of probe launches
+  std::vector<std::vector<int32_t>> probe_len;     // [prompt][G] probe tokens decoded
+  bool probe_open = false;
+  std::vector<uint8_t> probe_layer_done;
+  int probe_layers_done = 0;
+  int pb_prompt = -1, pb_first = 0, pb_n = 0;      // the open probe step's batch
+  uint8_t pb_live[infs::kMaxSlots] = {};
+  StepArgs pplan{};
+  int pgrid = 0;
+  double pstep_bytes = 0, pstep_flops = 0;
+  uint32_t probe_prefix_arrivals = 0;
+  std::vector<uint32_t> probe_suffix_arrivals;
   std::vector<uint8_t> layer_done;
   int layers_done = 0;
   StepArgs plan{};
@@ -131,8 +152,10 @@ void free_device(infs_ctx* c) {
   (void)hipFree(c->status);
 }
 
+// Counters: decode prefix [NP][Hkv], decode response [S][Hkv], then the probe
+// launches' own prefix [1][Hkv] and response [kMaxSlots][Hkv] counters.
 size_t counter_bytes(const infs_ctx* c) {
-  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->NP + c->S) * c->Hkv;
+  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->NP + c->S + 1 + infs::kMaxSlots) * c->Hkv;
 }
 
 void reset_host(infs_ctx* c) {
@@ -140,13 +163,20 @@ void reset_host(infs_ctx* c) {
   c->prefilled.assign(c->NP, std::vector<uint8_t>(c->L, 0));
   c->slot_sample.assign(c->S, -1);
   c->slot_len.assign(c->S, 0);
-  c->slot_pages.assign(c->S, {});
+  c->slot_handle.assign(c->S, -1);
+  c->seq_pages.assign(c->H, {});
   c->free_pages = {};
   for (int i = 0; i < c->num_pages; ++i) c->free_pages.push(i);
   c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
   c->prefix_arrivals.assign(c->NP, 0);
   c->suffix_arrivals.assign(c->S, 0);
   c->step_open = false;
+  c->probe_len.assign(c->probe_k > 0 ? c->NP : 0, std::vector<int32_t>(c->G, 0));
+  c->probe_open = false;
+  c->probe_layer_done.assign(c->L, 0);
+  c->probe_layers_done = 0;
+  c->probe_prefix_arrivals = 0;
+  c->probe_suffix_arrivals.assign(infs::kMaxSlots, 0);
   c->layer_done.assign(c->L, 0);
   c->layers_done = 0;
   c->stats = infs_stats{};
@@ -197,14 +227,16 @@ infs_status open_step(infs_ctx* c) {
     }
     const int len = c->slot_len[s] + 1;
     const int pos = len - 1;
+    const int h = c->slot_handle[s];
     if (pos % infs::kPageTokens == 0) {
-      c->slot_pages[s].push_back(c->free_pages.top());
+      c->seq_pages[h].push_back(c->free_pages.top());
       c->free_pages.pop();
     }
     a.live_slot[lives++] = (int8_t)s;
     sp.len = len;
     sp.item_begin = items;
-    sp.cur_page = c->slot_pages[s][pos / infs::kPageTokens];
+    sp.seq = h;
+    sp.cur_page = c->seq_pages[h][pos / infs::kPageTokens];
     sp.sample = (int32_t)c->slot_sample[s];
     const int nch = ceil_div(len, c->split);
     items += nch;
@@ -221,6 +253,84 @@ infs_status open_step(infs_ctx* c) {
   c->step_open = true;
   std::fill(c->layer_done.begin(), c->layer_done.end(), 0);
   c->layers_done = 0;
+  return INFS_OK;
+}
+
+// Build the plan of a probe step for samples first .. first+n-1 of prompt p
+// (live[j] != 0: sample first+j decodes its next probe token).  The probe plan
+// is a one-prompt decode plan whose slots are the batch's samples; the launch
+// offsets the prefix, token-counter and counter pointers to prompt p and to
+// the probe counters.  Validates before changing anything.
+infs_status open_probe(infs_ctx* c, int p, int first, int n, const uint8_t* live) {
+  int need_pages = 0, nlive = 0;
+  for (int j = 0; j < n; ++j) {
+    if (!live[j]) continue;
+    const int i = first + j;
+    ++nlive;
+    if (c->dispatched[p][i])
+      return fail(c, INFS_E_STATE, "sample %d of prompt %d was already dispatched or released", i, p);
+    if (c->probe_len[p][i] >= c->probe_k)
+      return fail(c, INFS_E_CAPACITY, "sample %d of prompt %d already has probe_tokens=%d probe tokens", i, p,
+                  c->probe_k);
+    if (c->probe_len[p][i] % infs::kPageTokens == 0) ++need_pages;
+  }
+  if ((size_t)need_pages > c->free_pages.size())
+    return fail(c, INFS_E_CAPACITY, "page pool exhausted: need %d pages, %zu free", need_pages, c->free_pages.size());
+  if (nlive > 0 && c->plen[p] < 0) return fail(c, INFS_E_STATE, "prompt %d has no prefilled prefix", p);
+  StepArgs& a = c->pplan;
+  a = c->plan;
+  a.S = n;
+  a.m = n;
+  a.num_prompts = 1;
+  a.prefix_rows = n * c->hpk;
+  a.clock_start = a.clock_end = nullptr;
+  for (int q = 0; q < infs::kMaxPrompts; ++q) a.prompt[q] = infs::PromptPlan{};
+  const double kvrow = (double)c->Hkv * c->D * c->es;
+  double bytes = 0, flops = 0;
+  infs::PromptPlan& pp = a.prompt[0];
+  pp.plen = std::max(c->plen[p], 0);
+  pp.nchunks = nlive > 0 ? ceil_div(pp.plen, c->prefix_split) : 0;
+  pp.item_begin = 0;
+  if (nlive > 0) bytes += 2.0 * pp.plen * kvrow;
+  int items = 0, zeros = 0, lives = 0;
+  a.n_prefix_items = pp.nchunks;
+  for (int j = 0; j < n; ++j) {
+    infs::SlotPlan& sp = a.slot[j];
+    sp = infs::SlotPlan{};
+    if (!live[j]) {
+      sp.item_begin = items;
+      a.zero_slot[zeros++] = (int8_t)j;
+      continue;
+    }
+    const int i = first + j, h = p * c->G + i;
+    const int len = c->probe_len[p][i] + 1, pos = len - 1;
+    if (pos % infs::kPageTokens == 0) {
+      c->seq_pages[h].push_back(c->free_pages.top());
+      c->free_pages.pop();
+    }
+    a.live_slot[lives++] = (int8_t)j;
+    sp.len = len;
+    sp.item_begin = items;
+    sp.seq = h;
+    sp.sample = i;
+    sp.cur_page = c->seq_pages[h][pos / infs::kPageTokens];
+    items += ceil_div(len, c->split);
+    bytes += 2.0 * len * kvrow + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
+    flops += 4.0 * c->Hq * c->D * (double)(pp.plen + len);
+  }
+  a.n_suffix_items = items;
+  a.n_zero_items = zeros;
+  a.n_merge_items = lives;
+  c->pgrid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items + a.n_merge_items) * c->Hkv;
+  c->pstep_bytes = bytes;
+  c->pstep_flops = flops;
+  c->pb_prompt = p;
+  c->pb_first = first;
+  c->pb_n = n;
+  std::memcpy(c->pb_live, live, n);
+  c->probe_open = true;
+  std::fill(c->probe_layer_done.begin(), c->probe_layer_done.end(), 0);
+  c->probe_layers_done = 0;
   return INFS_OK;
 }
 
@@ -281,20 +391,20 @@ void set_targets(infs_ctx* c) {
   }
 }
 
-infs_status timed_launch(infs_ctx* c) {
-  set_targets(c);
+// Launch one decode or probe kernel; in timing mode it records its start and end.
+infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int grid) {
   Timing& t = c->timing;
-  c->plan.clock_start = c->plan.clock_end = nullptr;
+  a.clock_start = a.clock_end = nullptr;
   if (t.on) {
     if (t.used == t.capacity) {
       infs_status st = harvest_clocks(c);
       if (st != INFS_OK) return st;
     }
-    c->plan.clock_start = t.clocks + (size_t)t.used * kClockWords;
-    c->plan.clock_end = t.clocks + ((size_t)t.capacity + t.used) * kClockWords;
+    a.clock_start = t.clocks + (size_t)t.used * kClockWords;
+    a.clock_end = t.clocks + ((size_t)t.capacity + t.used) * kClockWords;
     ++t.used;
   }
-  HIP_TRY(c, infs::launch_decode(c->key, c->plan, c->grid, c->stream));
+  HIP_TRY(c, infs::launch_decode(key, a, grid, c->stream));
   return INFS_OK;
 }
 
@@ -333,14 +443,27 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   if (k.dtype != INFS_F32 && k.dtype != INFS_BF16) return fail(nullptr, INFS_E_ARG, "dtype must be INFS_F32 or INFS_BF16");
   if (!(k.scale >= 0.f) || !std::isfinite(k.scale)) return fail(nullptr, INFS_E_ARG, "scale must be finite and >= 0");
   if (k.flags & ~INFS_FLAG_DRY_RUN) return fail(nullptr, INFS_E_ARG, "unknown flags");
+  if (k.probe_tokens < 0 || k.probe_tokens > k.max_suffix_len)
+    return fail(nullptr, INFS_E_ARG, "probe_tokens must be in [0, max_suffix_len]");
 
   const int hpk = k.num_q_heads / k.num_kv_heads;
   KernelKey key{};
   if (!infs::select_kernel(k.dtype == INFS_BF16, k.head_dim, hpk, k.slots_per_prompt * hpk, &key))
     return fail(nullptr, INFS_E_ARG,
-                "no kernel for dtype=%s head_dim=%d heads_per_kv=%d prefix rows=%d (bf16 supports up to 64 rows, "
+                "no kernel for dtype=%s head_dim=%d heads_per_kv=%d prefix rows=%d (bf16 supports up to 128 rows, "
                 "fp32 up to 16)",
                 k.dtype == INFS_BF16 ? "bf16" : "f32", k.head_dim, hpk, k.slots_per_prompt * hpk);
+  // Probe launches put up to probe_batch samples' rows on one prefix work item,
+  // on the prefix path of the decode kernel (the prefix store layout is shared).
+  KernelKey pkey{};
+  int probe_batch = 0;
+  if (k.probe_tokens > 0) {
+    const int max_rows = key.mfma ? 128 : 16;
+    probe_batch = std::min({infs::kMaxSlots, max_rows / hpk, k.samples_per_prompt});
+    if (probe_batch < 1 ||
+        !infs::select_kernel_path(k.dtype == INFS_BF16, k.head_dim, hpk, probe_batch * hpk, key.mfma, &pkey))
+      return fail(nullptr, INFS_E_ARG, "no probe kernel for heads_per_kv=%d", hpk);
+  }
   {
     const int split = k.split_tokens ? k.split_tokens : 256;
     const int psplit = key.mfma ? infs::kMfmaPrefixSplit : split;
@@ -349,10 +472,11 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       return fail(nullptr, INFS_E_ARG,
                   "max_prompt_len and max_suffix_len need %d split-K chunks per slot (limit %d): raise split_tokens",
                   parts, infs::kMaxPartials);
-    const int64_t ws_bytes =
-        infs::workspace_records(key, k.num_prompts, k.num_kv_heads, std::max(1, (k.max_prompt_len + psplit - 1) / psplit),
-                                k.num_prompts * k.slots_per_prompt, (k.max_suffix_len + split - 1) / split) *
-        k.head_dim * (int64_t)sizeof(float);
+    const int pcm = std::max(1, (k.max_prompt_len + psplit - 1) / psplit), scm = (k.max_suffix_len + split - 1) / split;
+    int64_t recs = infs::workspace_records(key, k.num_prompts, k.num_kv_heads, pcm, k.num_prompts * k.slots_per_prompt, scm);
+    if (k.probe_tokens > 0)
+      recs = std::max(recs, infs::workspace_records(pkey, 1, k.num_kv_heads, pcm, probe_batch, scm));
+    const int64_t ws_bytes = recs * k.head_dim * (int64_t)sizeof(float);
     if (ws_bytes >= (int64_t(1) << 31))
       return fail(nullptr, INFS_E_ARG, "split-K workspace of %lld bytes exceeds 2 GiB: lower num_kv_heads or raise split_tokens",
                   (long long)ws_bytes);
@@ -363,6 +487,9 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->dry = (k.flags & INFS_FLAG_DRY_RUN) != 0;
   c->stream = (hipStream_t)hip_stream;
   c->key = key;
+  c->pkey = pkey;
+  c->probe_k = k.probe_tokens;
+  c->probe_batch = probe_batch;
   c->NP = k.num_prompts;
   c->m = k.slots_per_prompt;
   c->S = c->NP * c->m;
@@ -376,13 +503,23 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->split = k.split_tokens ? k.split_tokens : 256;
   c->pmax_pad = std::max(32, (k.max_prompt_len + 31) / 32 * 32);
   c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);
-  c->num_pages = k.num_pages ? k.num_pages : c->S * c->pages_per_slot;
+  c->H = c->probe_k > 0 ? c->NP * c->G : c->S;
+  if ((int64_t)c->H * c->pages_per_slot * (int64_t)sizeof(int32_t) >= (int64_t(1) << 31)) {
+    delete c;
+    return fail(nullptr, INFS_E_ARG, "page table of %d sequences x %d pages exceeds 2 GiB", c->H, c->pages_per_slot);
+  }
+  c->num_pages = k.num_pages ? k.num_pages
+                             : c->S * c->pages_per_slot +
+                                   (c->probe_k > 0 ? c->NP * c->G * ceil_div(c->probe_k, infs::kPageTokens) : 0);
   c->prefix_split = key.mfma ? infs::kMfmaPrefixSplit : c->split;
   c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->prefix_split));
   c->scmax = ceil_div(k.max_suffix_len, c->split);
   c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->es;
   c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->es;
   c->ws_records = infs::workspace_records(key, c->NP, c->Hkv, c->pcmax, c->S, c->scmax);
+  if (c->probe_k > 0)
+    c->ws_records =
+        std::max(c->ws_records, infs::workspace_records(pkey, 1, c->Hkv, c->pcmax, c->probe_batch, c->scmax));
   reset_host(c);
 
   StepArgs& a = c->plan;
@@ -417,7 +554,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     infs_status st = INFS_OK;
     if (st == INFS_OK) st = alloc((void**)&c->prefix, c->prefix_layer_bytes * c->L, "prefix store");
     if (st == INFS_OK) st = alloc((void**)&c->pool, c->pool_layer_bytes * c->L, "page pool");
-    if (st == INFS_OK) st = alloc((void**)&c->page_table, sizeof(int32_t) * c->S * c->pages_per_slot, "page table");
+    if (st == INFS_OK) st = alloc((void**)&c->page_table, sizeof(int32_t) * c->H * c->pages_per_slot, "page table");
     if (st == INFS_OK) st = alloc((void**)&c->ws_o, sizeof(float) * c->ws_records * c->D, "workspace");
     if (st == INFS_OK) st = alloc((void**)&c->ws_ml, sizeof(float) * c->ws_records * 2, "workspace");
     if (st == INFS_OK) st = alloc((void**)&c->counters, counter_bytes(c), "counters");
@@ -470,7 +607,7 @@ infs_status infs_prefill_shared(infs_ctx* c, int32_t prompt, int32_t layer, int3
     return fail(c, INFS_E_ARG, "prompt_len %d out of range [0, %d]", prompt_len, c->cfg.max_prompt_len);
   if (c->plen[prompt] >= 0 && c->plen[prompt] != prompt_len)
     return fail(c, INFS_E_ARG, "prompt %d was prefilled with %d tokens in another layer", prompt, c->plen[prompt]);
-  if (c->step_open) return fail(c, INFS_E_STATE, "prefill while a step is open");
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "prefill while a step is open");
   if (!c->dry && prompt_len > 0 && (!k_dev || !v_dev)) return fail(c, INFS_E_ARG, "null K/V pointer");
   if (!c->dry && prompt_len > 0 && (((uintptr_t)k_dev | (uintptr_t)v_dev) & 15))
     return fail(c, INFS_E_ARG, "K/V must be 16-byte aligned");
@@ -493,10 +630,16 @@ infs_status infs_refill_slot(infs_ctx* c, int32_t slot, int32_t prompt, int64_t 
   if (c->slot_sample[slot] >= 0) return fail(c, INFS_E_STATE, "slot %d is live", slot);
   if (c->dispatched[prompt][sample_id])
     return fail(c, INFS_E_DUP, "sample %lld of prompt %d was already dispatched", (long long)sample_id, prompt);
+  if (c->probe_open) return fail(c, INFS_E_STATE, "refill while a probe step is open");
   c->dispatched[prompt][sample_id] = 1;
   c->slot_sample[slot] = sample_id;
-  c->slot_len[slot] = 0;
-  c->slot_pages[slot].clear();
+  if (c->probe_k > 0) {
+    c->slot_handle[slot] = prompt * c->G + (int32_t)sample_id;
+    c->slot_len[slot] = c->probe_len[prompt][sample_id];  // decoding resumes after the probe tokens
+  } else {
+    c->slot_handle[slot] = slot;
+    c->slot_len[slot] = 0;
+  }
   return INFS_OK;
 }
 
@@ -505,10 +648,29 @@ infs_status infs_retire_slot(infs_ctx* c, int32_t slot) {
   if (slot < 0 || slot >= c->S) return fail(c, INFS_E_ARG, "slot %d out of range [0, %d)", slot, c->S);
   if (c->step_open) return fail(c, INFS_E_STATE, "retire while a step is open");
   if (c->slot_sample[slot] < 0) return fail(c, INFS_E_STATE, "slot %d is empty", slot);
-  for (int32_t pg : c->slot_pages[slot]) c->free_pages.push(pg);
-  c->slot_pages[slot].clear();
+  std::vector<int32_t>& pages = c->seq_pages[c->slot_handle[slot]];
+  for (int32_t pg : pages) c->free_pages.push(pg);
+  pages.clear();
   c->slot_sample[slot] = -1;
   c->slot_len[slot] = 0;
+  c->slot_handle[slot] = -1;
+  return INFS_OK;
+}
+
+infs_status infs_release_sample(infs_ctx* c, int32_t prompt, int64_t sample_id) {
+  CHECK_CTX(c);
+  if (c->probe_k == 0) return fail(c, INFS_E_STATE, "release_sample needs a context with probe_tokens > 0");
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range [0, %d)", prompt, c->NP);
+  if (sample_id < 0 || sample_id >= c->G)
+    return fail(c, INFS_E_ARG, "sample_id %lld out of range [0, %d)", (long long)sample_id, c->G);
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "release while a step is open");
+  if (c->dispatched[prompt][sample_id])
+    return fail(c, INFS_E_DUP, "sample %lld of prompt %d was already dispatched or released", (long long)sample_id,
+                prompt);
+  c->dispatched[prompt][sample_id] = 1;
+  std::vector<int32_t>& pages = c->seq_pages[prompt * c->G + (int32_t)sample_id];
+  for (int32_t pg : pages) c->free_pages.push(pg);
+  pages.clear();
   return INFS_OK;
 }
 
@@ -519,6 +681,7 @@ infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, cons
   if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
   if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
     return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
+  if (c->probe_open) return fail(c, INFS_E_STATE, "decode_step while a probe step is open");
   if (c->step_open && c->layer_done[layer])
     return fail(c, INFS_E_STATE, "layer %d already decoded in this step", layer);
   for (int p = 0; p < c->NP; ++p) {
@@ -540,7 +703,8 @@ infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, cons
     a.prefix = c->prefix + c->prefix_layer_bytes * layer;
     a.pool = c->pool + c->pool_layer_bytes * layer;
     a.count_tokens = layer == 0;
-    infs_status st = timed_launch(c);
+    set_targets(c);
+    infs_status st = timed_launch(c, c->key, a, c->grid);
     if (st != INFS_OK) return st;
   }
   c->layer_done[layer] = 1;
@@ -563,6 +727,90 @@ infs_status infs_end_step(infs_ctx* c) {
     }
   c->step_open = false;
   ++c->stats.steps;
+  return INFS_OK;
+}
+
+infs_status infs_probe_step(infs_ctx* c, int32_t layer, int32_t prompt, int32_t first_sample, int32_t n,
+                            const uint8_t* live_host, const void* q_dev, const void* k_new_dev, const void* v_new_dev,
+                            float* o_dev) {
+  CHECK_CTX(c);
+  if (c->probe_k == 0) return fail(c, INFS_E_STATE, "probe_step needs a context with probe_tokens > 0");
+  if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range [0, %d)", prompt, c->NP);
+  if (n < 1 || n > c->probe_batch) return fail(c, INFS_E_ARG, "n=%d out of range [1, %d]", n, c->probe_batch);
+  if (first_sample < 0 || first_sample > c->G - n)
+    return fail(c, INFS_E_ARG, "samples %d..%d out of range [0, %d)", first_sample, first_sample + n - 1, c->G);
+  if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
+  if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
+    return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
+  if (c->step_open) return fail(c, INFS_E_STATE, "probe_step while a decode step is open");
+  uint8_t live[infs::kMaxSlots];
+  for (int j = 0; j < n; ++j) live[j] = live_host ? (live_host[j] != 0) : 1;
+  if (c->probe_open) {
+    if (prompt != c->pb_prompt || first_sample != c->pb_first || n != c->pb_n || std::memcmp(live, c->pb_live, n))
+      return fail(c, INFS_E_STATE, "every layer of a probe step must decode the same batch");
+    if (c->probe_layer_done[layer]) return fail(c, INFS_E_STATE, "layer %d already probed in this step", layer);
+  }
+  bool any = false;
+  for (int j = 0; j < n; ++j) any |= live[j] != 0;
+  if (any && !c->prefilled[prompt][layer])
+    return fail(c, INFS_E_STATE, "prompt %d has no prefix for layer %d", prompt, layer);
+  if (!c->probe_open) {
+    infs_status st = open_probe(c, prompt, first_sample, n, live);
+    if (st != INFS_OK) return st;
+  }
+  if (!c->dry) {
+    StepArgs& a = c->pplan;
+    a.q = q_dev;
+    a.knew = k_new_dev;
+    a.vnew = v_new_dev;
+    a.o = o_dev;
+    a.prefix = c->prefix + c->prefix_layer_bytes * layer +
+               (size_t)prompt * c->Hkv * infs::prefix_elems_per_head(c->key, c->pmax_pad) * c->es;
+    a.pool = c->pool + c->pool_layer_bytes * layer;
+    a.tokens = c->tokens + (size_t)prompt * c->G;
+    a.counters = c->counters + (size_t)(c->NP + c->S) * c->Hkv * infs::kCounterStride;
+    a.count_tokens = layer == 0;
+    c->probe_prefix_arrivals += (uint32_t)a.prompt[0].nchunks;
+    a.prompt[0].target = (int32_t)c->probe_prefix_arrivals;
+    for (int j = 0; j < n; ++j) {
+      if (a.slot[j].len > 0) c->probe_suffix_arrivals[j] += (uint32_t)ceil_div(a.slot[j].len, c->split);
+      a.slot[j].target = (int32_t)c->probe_suffix_arrivals[j];
+    }
+    infs_status st = timed_launch(c, c->pkey, a, c->pgrid);
+    if (st != INFS_OK) return st;
+  }
+  c->probe_layer_done[layer] = 1;
+  ++c->probe_layers_done;
+  ++c->stats.launches;
+  c->stats.alg_bytes += c->pstep_bytes;
+  c->stats.alg_flops += c->pstep_flops;
+  return INFS_OK;
+}
+
+infs_status infs_end_probe_step(infs_ctx* c) {
+  CHECK_CTX(c);
+  if (!c->probe_open || c->probe_layers_done != c->L)
+    return fail(c, INFS_E_STATE, "end_probe_step needs every layer probed once (%d of %d)",
+                c->probe_open ? c->probe_layers_done : 0, c->L);
+  for (int j = 0; j < c->pb_n; ++j)
+    if (c->pb_live[j]) {
+      ++c->probe_len[c->pb_prompt][c->pb_first + j];
+      ++c->stats.tokens;
+    }
+  c->probe_open = false;
+  return INFS_OK;
+}
+
+int32_t infs_probe_batch(const infs_ctx* c) { return c ? c->probe_batch : -1; }
+
+infs_status infs_probe_state(const infs_ctx* c, int32_t prompt, int64_t sample_id, int32_t* probe_len) {
+  if (!c) return fail(nullptr, INFS_E_ARG, "null context");
+  infs_ctx* cc = const_cast<infs_ctx*>(c);
+  if (prompt < 0 || prompt >= c->NP) return fail(cc, INFS_E_ARG, "prompt %d out of range", prompt);
+  if (sample_id < 0 || sample_id >= c->G) return fail(cc, INFS_E_ARG, "sample_id out of range");
+  if (!probe_len) return fail(cc, INFS_E_ARG, "null output pointer");
+  *probe_len = c->probe_k > 0 ? c->probe_len[prompt][sample_id] : 0;
   return INFS_OK;
 }
 

@@ -13,7 +13,7 @@ from typing import Callable, List, Optional, Sequence
 from . import infs
 
 
-def context_for(cfg, stream=None, dry_run=False, split_tokens=0, num_pages=0) -> infs.Context:
+def context_for(cfg, stream=None, dry_run=False, split_tokens=0, num_pages=0, probe_tokens=0) -> infs.Context:
     """Create a context for a workload preset (workload.GroupConfig or alike)."""
     c = infs.make_config(
         num_layers=cfg.layers, num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
@@ -21,7 +21,7 @@ def context_for(cfg, stream=None, dry_run=False, split_tokens=0, num_pages=0) ->
         samples_per_prompt=cfg.samples_per_prompt, max_prompt_len=max(cfg.prompt_lens),
         max_suffix_len=cfg.max_suffix_len, page_tokens=0, num_pages=num_pages,
         split_tokens=split_tokens, dtype=infs.BF16 if cfg.dtype == "bf16" else infs.F32,
-        scale=0.0, flags=infs.FLAG_DRY_RUN if dry_run else 0)
+        scale=0.0, flags=infs.FLAG_DRY_RUN if dry_run else 0, probe_tokens=probe_tokens)
     return infs.Context(c, stream=None if dry_run else stream)
 
 
@@ -34,10 +34,48 @@ def schedulers_for(cfg, policy: str, pred=None) -> List[infs.Sched]:
     return out
 
 
+def probe_group(ctx: infs.Context, lengths, k: int, num_layers: int, provide: Callable,
+                log: Optional[list] = None, after_step: Optional[Callable] = None) -> int:
+    """Probe phase of prefix reuse (Section 4): every sample decodes its first
+    min(L_i, k) tokens against the shared prompt, in batches of up to
+    ctx.probe_batch samples of one prompt; samples that finish within their
+    probe tokens are released.  Returns the number of probe steps.
+
+    provide(step, prompt, first, n, layer) -> (q, k_new, v_new, o) device
+    buffers of that batch ([n, Hq, d], [n, Hkv, d], [n, Hkv, d], [n, Hq, d]).
+    log, if given, receives one row per probe step: per batch position
+    (prompt, sample, t) with t the probe length after this step, or None.
+    after_step(step) is called after each end_probe_step.
+    """
+    nb = ctx.probe_batch
+    steps = 0
+    for t in range(1, k + 1):
+        for p, row in enumerate(lengths):
+            G = len(row)
+            for first in range(0, G, nb):
+                n = min(nb, G - first)
+                live = [int(row[first + j]) >= t for j in range(n)]
+                if not any(live):
+                    continue
+                for layer in range(num_layers):
+                    ctx.probe_step(layer, p, first, n, live, *provide(steps, p, first, n, layer))
+                ctx.end_probe_step()
+                if after_step is not None:
+                    after_step(steps)
+                if log is not None:
+                    log.append(tuple((p, first + j, t) if live[j] else None for j in range(n)))
+                steps += 1
+    for p, row in enumerate(lengths):
+        for i, x in enumerate(row):
+            if int(x) <= k:
+                ctx.release_sample(p, i)
+    return steps
+
+
 def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_layers: int,
                  provide: Callable, after_step: Optional[Callable] = None,
                  log: Optional[list] = None, stop_after: Optional[int] = None,
-                 accepted: Optional[list] = None) -> int:
+                 accepted: Optional[list] = None, reuse: int = 0) -> int:
     """Decode every sample of every prompt; returns the number of running steps.
 
     lengths[p][i]: true length of sample i of prompt p.
@@ -50,6 +88,9 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     in ascending slot order within a step) the prompt stops: its samples still
     decoding are discarded (their slots retired) and it is not refilled.
     accepted, if given, receives per prompt the completed sample ids in order.
+    reuse = k: the samples went through a probe phase of k tokens (probe_group);
+    a dispatched sample resumes at token k+1, and one that finished within its
+    probe tokens is skipped (the scheduler is told it is done at once).
     """
     NP = len(scheds)
     m = ctx.config.slots_per_prompt
@@ -67,12 +108,16 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
             sch = scheds[p]
             for ls in range(m):
                 s = p * m + ls
-                if slot_sample[s] < 0:
+                while slot_sample[s] < 0:
                     i = sch.next(ls)
-                    if i >= 0:
-                        ctx.refill_slot(s, p, i)
-                        slot_sample[s] = i
-                        slot_len[s] = 0
+                    if i < 0:
+                        break
+                    if reuse and Ls[p][i] <= reuse:  # finished within its probe tokens
+                        sch.done(ls)
+                        continue
+                    ctx.refill_slot(s, p, i)
+                    slot_sample[s] = i
+                    slot_len[s] = reuse
 
     fill()
     step = 0
@@ -112,15 +157,19 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     return step
 
 
-def plan_steps(cfg, lengths, policy: str, pred=None, stop_after=None, accepted=None) -> list:
-    """Step log of a group decode, from a dry-run context (bookkeeping only, no GPU)."""
-    ctx = context_for(cfg, dry_run=True)
+def plan_steps(cfg, lengths, policy: str, pred=None, stop_after=None, accepted=None, reuse=0,
+               probe_log=None) -> list:
+    """Step log of a group decode, from a dry-run context (bookkeeping only, no GPU).
+    reuse = k runs the probe phase of prefix reuse first (its log into probe_log)."""
+    ctx = context_for(cfg, dry_run=True, probe_tokens=reuse)
     for p in range(cfg.num_prompts):
         for layer in range(cfg.layers):
             ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
     log = []
     nothing = (None, None, None, None)
+    if reuse:
+        probe_group(ctx, lengths, reuse, cfg.layers, lambda *a: nothing, log=probe_log)
     decode_group(ctx, schedulers_for(cfg, policy, pred), lengths, cfg.layers, lambda s, l: nothing, log=log,
-                 stop_after=stop_after, accepted=accepted)
+                 stop_after=stop_after, accepted=accepted, reuse=reuse)
     ctx.destroy()
     return log

@@ -31,7 +31,8 @@ EXPORTS = (
     "infs_refill_slot", "infs_retire_slot", "infs_decode_step", "infs_end_step", "infs_slot_state",
     "infs_sample_tokens", "infs_sync", "infs_get_stats", "infs_timing_begin", "infs_timing_end",
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
-    "infs_sched_destroy", "infs_fptas_assign",
+    "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
+    "infs_probe_state", "infs_release_sample",
 )
 
 
@@ -48,7 +49,7 @@ class Config(ctypes.Structure):
         ("samples_per_prompt", ctypes.c_int32), ("max_prompt_len", ctypes.c_int32),
         ("max_suffix_len", ctypes.c_int32), ("page_tokens", ctypes.c_int32), ("num_pages", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float),
-        ("flags", ctypes.c_uint32),
+        ("flags", ctypes.c_uint32), ("probe_tokens", ctypes.c_int32),
     ]
 
 
@@ -94,6 +95,11 @@ def load():
         "infs_sched_destroy": (None, [P]),
         "infs_fptas_assign": (I32, [I32, I32, ctypes.POINTER(ctypes.c_double), ctypes.c_double,
                                     ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+        "infs_probe_step": (I32, [P, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_uint8), P, P, P, P]),
+        "infs_end_probe_step": (I32, [P]),
+        "infs_probe_batch": (I32, [P]),
+        "infs_probe_state": (I32, [P, I32, I64, ctypes.POINTER(I32)]),
+        "infs_release_sample": (I32, [P, I32, I64]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -187,6 +193,29 @@ class Context:
 
     def sync(self):
         self._call(load().infs_sync)
+
+    @property
+    def probe_batch(self):
+        return load().infs_probe_batch(self._h)
+
+    def probe_step(self, layer, prompt, first_sample, n, live, q, k_new, v_new, o):
+        """live: n truthy values, or None for all live."""
+        buf = None
+        if live is not None:
+            buf = (ctypes.c_uint8 * n)(*[1 if x else 0 for x in live])
+        self._call(load().infs_probe_step, layer, prompt, first_sample, n, buf, _ptr(q), _ptr(k_new), _ptr(v_new),
+                   _ptr(o))
+
+    def end_probe_step(self):
+        self._call(load().infs_end_probe_step)
+
+    def probe_state(self, prompt, sample_id):
+        n = ctypes.c_int32()
+        self._call(load().infs_probe_state, prompt, sample_id, ctypes.byref(n))
+        return n.value
+
+    def release_sample(self, prompt, sample_id):
+        self._call(load().infs_release_sample, prompt, sample_id)
 
     def get_stats(self) -> Stats:
         s = Stats()

@@ -11,7 +11,7 @@ import time
 import numpy as np
 
 from oracle import attend_slot, simulate_group
-from paper_2506_22950_amd.group import context_for, decode_group, plan_steps, schedulers_for
+from paper_2506_22950_amd.group import context_for, decode_group, plan_steps, probe_group, schedulers_for
 from workload import Workload
 from workload.staging import DeviceInputs
 
@@ -21,15 +21,20 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None):
+def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
+                  probe=None):
+    """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
+    reuse first; if `probe` is a dict it receives 'log' (probe step log) and
+    'captured' (the O buffer [L, batch, Hq, d] after every probe step)."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
     wl = wl or Workload(cfg)
-    log = plan_steps(cfg, wl.L, policy, wl.L_hat, stop_after=stop_after)
+    plog = []
+    log = plan_steps(cfg, wl.L, policy, wl.L_hat, stop_after=stop_after, reuse=reuse, probe_log=plog)
     dev = DeviceInputs(wl)
     stream = torch.cuda.current_stream()
-    ctx = context_for(cfg, stream=stream, split_tokens=split)
+    ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse)
     keep = []
     for p in range(cfg.num_prompts):
         for layer in range(cfg.layers):
@@ -62,8 +67,24 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
             captured[step] = o.cpu().numpy()
 
     t0 = time.time()
+    if reuse:
+        pq, pk, pv = dev.stage(plog, 0, len(plog))
+        W = pq.shape[2]
+        po = torch.zeros((L, W, Hq, d), dtype=torch.float32, device="cuda")
+        pcap = {}
+
+        def pprovide(j, p, first, n, layer):
+            return (pq[j, layer].data_ptr(), pk[j, layer].data_ptr(), pv[j, layer].data_ptr(), po[layer].data_ptr())
+
+        def pafter(j):
+            pcap[j] = po.cpu().numpy()
+
+        nprobe = probe_group(ctx, wl.L, reuse, L, pprovide, after_step=pafter)
+        assert nprobe == len(plog)
+        if probe is not None:
+            probe["log"], probe["captured"] = plog, pcap
     steps = decode_group(ctx, schedulers_for(cfg, policy, wl.L_hat), wl.L, L, provide, after_step=after,
-                         stop_after=stop_after)
+                         stop_after=stop_after, reuse=reuse)
     torch.cuda.synchronize()
     tokens = np.stack([ctx.sample_tokens(p) for p in range(cfg.num_prompts)])
     stats = ctx.get_stats()
@@ -129,8 +150,8 @@ def oracle_dynamic_log(cfg, wl, target):
     return out
 
 
-def oracle_log(cfg, wl, policy):
-    total, res = simulate_group(wl.L, cfg.slots_per_prompt, policy, wl.L_hat)
+def oracle_log(cfg, wl, policy, reuse=0):
+    total, res = simulate_group(wl.L, cfg.slots_per_prompt, policy, wl.L_hat, reuse=reuse)
     m = cfg.slots_per_prompt
     out = []
     for k in range(total):

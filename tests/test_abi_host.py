@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     assert declared == set(infs.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.infs_abi_version() == 1
+    assert lib.infs_abi_version() == 2
 
 
 def _oracle_log(cfg, L, policy, pred):
@@ -277,3 +277,69 @@ def test_dry_run_dynamic_slot_matches_simulator():
             want.append(tuple(row))
         assert log == want, trial
         assert acc == [r.accepted for r in res], trial
+
+
+
+def _oracle_reuse_log(cfg, L, policy, pred, k):
+    total, res = simulate_group(L, cfg.slots_per_prompt, policy, pred, reuse=k)
+    m = cfg.slots_per_prompt
+    return [tuple(None if (k2 >= r.steps or r.log[k2][ls] is None) else (p, r.log[k2][ls][0], r.log[k2][ls][1])
+                  for p, r in enumerate(res) for ls in range(m)) for k2 in range(total)]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
+def test_dry_run_prefix_reuse_matches_simulator(policy):
+    # Probe phase of k tokens, then decode resuming at k+1: the library's step
+    # log equals the simulator's with the same reuse; the probe log has, per
+    # token position t <= k and batch, exactly the samples longer than t-1.
+    rng = np.random.default_rng(15)
+    for trial in range(30):
+        NP = int(rng.integers(1, 3))
+        m = int(rng.integers(1, 5))
+        G = int(rng.integers(1, 20))
+        k = int(rng.integers(1, 6))
+        cfg = get_config("tiny_f32").with_(prompt_lens=tuple(int(x) for x in rng.integers(0, 40, NP)),
+                                           samples_per_prompt=G, slots_per_prompt=m, max_suffix_len=30)
+        L = rng.integers(1, 31, size=(NP, G))
+        pred = L * np.exp(rng.normal(0, 0.3, size=L.shape))
+        plog = []
+        log = plan_steps(cfg, L, policy, pred, reuse=k, probe_log=plog)
+        assert log == _oracle_reuse_log(cfg, L, policy, pred, k), (trial, NP, m, G, k)
+        seen = {}
+        for row in plog:
+            for e in row:
+                if e is not None:
+                    p, i, t = e
+                    assert t == seen.get((p, i), 0) + 1
+                    seen[(p, i)] = t
+        assert seen == {(p, i): min(int(L[p, i]), k) for p in range(NP) for i in range(G)}
+
+
+def test_probe_state_machine_errors():
+    cfg = get_config("tiny_f32").with_(samples_per_prompt=6, slots_per_prompt=2, max_suffix_len=16)
+    ctx = context_for(cfg, dry_run=True, probe_tokens=2)
+    assert ctx.probe_batch == 6
+    ctx.prefill_shared(0, 0, cfg.prompt_lens[0], None, None)
+    nothing = (None, None, None, None)
+    assert _code(ctx.probe_step, 0, 0, 0, 7, None, *nothing) == infs.E_ARG         # batch too large
+    assert _code(ctx.probe_step, 0, 0, 3, 4, None, *nothing) == infs.E_ARG         # past the last sample
+    ctx.probe_step(0, 0, 0, 6, [1, 1, 1, 1, 0, 1], *nothing)
+    assert _code(ctx.probe_step, 0, 0, 0, 6, [1] * 6, *nothing) == infs.E_STATE    # another batch in the step
+    assert _code(ctx.decode_step, 0, *nothing) == infs.E_STATE                    # decode during a probe step
+    assert _code(ctx.refill_slot, 0, 0, 0) == infs.E_STATE                        # refill during a probe step
+    ctx.end_probe_step()
+    assert [ctx.probe_state(0, i) for i in range(6)] == [1, 1, 1, 1, 0, 1]
+    assert _code(ctx.end_probe_step) == infs.E_STATE                              # no step open
+    ctx.probe_step(0, 0, 0, 6, None, *nothing)
+    ctx.end_probe_step()
+    assert _code(ctx.probe_step, 0, 0, 0, 1, None, *nothing) == infs.E_CAPACITY   # sample 0 has its k tokens
+    ctx.refill_slot(0, 0, 0)
+    assert ctx.slot_state(0) == (0, 2)                                            # resumes after the probe tokens
+    assert _code(ctx.probe_step, 0, 0, 0, 1, None, *nothing) == infs.E_STATE      # already dispatched
+    ctx.release_sample(0, 3)
+    assert _code(ctx.release_sample, 0, 3) == infs.E_DUP
+    assert _code(ctx.refill_slot, 1, 0, 3) == infs.E_DUP
+    plain = context_for(cfg, dry_run=True)
+    assert plain.probe_batch == 0
+    assert _code(plain.probe_step, 0, 0, 0, 1, None, *nothing) == infs.E_STATE
+    assert _code(plain.release_sample, 0, 0) == infs.E_STATE

@@ -101,6 +101,43 @@ def test_bf16_dynamic_slot_stream():
     say(f"  [dynamic-slot] {steps} steps, checked {n} outputs, max abs err {worst:.3g}")
 
 
+def _prefix_reuse(cfg, policy, k, split=128):
+    wl = Workload(cfg)
+    want = oracle_log(cfg, wl, policy, reuse=k)
+    probe = {}
+    _, log, steps, captured, tokens, _ = run_gpu_group(cfg, policy, wl=wl, split=split, reuse=k, probe=probe,
+                                                       capture=lambda j: j % 3 == 0 or j == len(want) - 1)
+    assert log == want and steps == len(want)
+    assert np.array_equal(tokens, wl.L), "device token counters (probe + decode) differ from the lengths"
+    worst_p, n_p = check_against_oracle(cfg, wl, probe["log"], probe["captured"])
+    worst, n = check_against_oracle(cfg, wl, log, captured)
+    say(f"  [{cfg.name} reuse k={k}] {len(probe['log'])} probe steps ({n_p} outputs, max err {worst_p:.3g}), "
+        f"{steps} decode steps ({n} outputs, max err {worst:.3g})")
+
+
+def test_bf16_prefix_reuse_probe_rowsplit():
+    # Prefix reuse (Section 4): 40 samples decode 16 probe tokens together
+    # (80 query rows per KV head: the row-split MFMA prefix path), then SJF
+    # decode resumes each at token 17; samples shorter than 17 never take a slot.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(300,), samples_per_prompt=40,
+                                             slots_per_prompt=8, length_dist=("lognormal", 3.5, 1.0, 1, 200),
+                                             max_suffix_len=200, pool_rows=None)
+    _prefix_reuse(cfg, "sjf", 16)
+
+
+def test_bf16_prefix_reuse_hpk4():
+    # 32Q/8KV (hpk=4): probe batches of 32 samples = 128 rows per KV head.
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(200, 450), samples_per_prompt=36,
+                                                length_dist=("lognormal", 3.5, 1.0, 1, 160), max_suffix_len=160,
+                                                pool_rows=None)
+    _prefix_reuse(cfg, "fptas_sjf", 8)
+
+
+def test_f32_prefix_reuse_wave():
+    # fp32 wavefront path: probe batches of 8 samples (16 rows).
+    _prefix_reuse(get_config("tiny_f32"), "fifo", 5, split=0)
+
+
 def test_bf16_single_slot_wave_prefix():
     # m=1: 2 prefix rows, so the prefix runs on the wavefront path in bf16.
     cfg = get_config("qwen3_1p7b_l1_g32").with_(slots_per_prompt=1, samples_per_prompt=4, prompt_lens=(257,),

@@ -302,3 +302,36 @@ def test_dynamic_event_driven_and_bounded_by_fifo():
         assert r.steps == fin[target - 1][0]
         assert r.accepted == [i for _, _, i in fin[:target]]
         assert r.steps <= simulate(L[:target], m, "fifo").steps
+
+
+def test_reuse_golden_case():
+    g = json.load(open(GOLDEN))["reuse_case"]
+    r = simulate(g["L"], g["m"], g["policy"], reuse=g["k"])
+    assert r.steps == g["steps"]
+    assert r.log == [tuple(None if e is None else tuple(e) for e in row) for row in g["log"]]
+    assert list(r.tokens) == g["L"]
+
+
+def test_reuse_closed_forms():
+    # With k probe tokens a sample occupies a slot for max(L - k, 0) steps and
+    # samples with L <= k never take one: fixed-slot is the largest row sum of
+    # the remainders, naive micro groups the sum of each group's largest
+    # remainder, FIFO the FIFO schedule of the remainders in id order, and
+    # reuse 0 changes nothing.
+    rng = np.random.default_rng(13)
+    for L, m, pred in _instances(1500, seed=14):
+        k = int(rng.integers(0, 8))
+        rem = np.maximum(L - k, 0)
+        G = len(L)
+        assert simulate(L, m, "fixed_row", reuse=k).steps == max(int(rem[s::m].sum()) for s in range(m))
+        assert simulate(L, m, "naive", reuse=k).steps == sum(int(rem[n:n + m].max()) for n in range(0, G, m))
+        live = rem[rem > 0]
+        want = simulate(live, m, "fifo").steps if len(live) else 0
+        assert simulate(L, m, "fifo", reuse=k).steps == want
+        for policy in POLICIES:
+            r = simulate(L, m, policy, pred=pred, reuse=k)
+            assert list(r.tokens) == list(L), policy
+            assert sum(e is not None for row in r.log for e in row) == int(rem.sum()), policy
+            assert all(e[1] > k for row in r.log for e in row if e is not None), policy
+            if k == 0:
+                assert r.log == simulate(L, m, policy, pred=pred).log

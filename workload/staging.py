@@ -27,9 +27,11 @@ class DeviceInputs:
         return self.pool["k"][idx].contiguous(), self.pool["v"][idx].contiguous()
 
     def indices(self, log, step0, step1):
-        """Pool row indices [n, L, S] of Q and of the new K/V rows for steps [step0, step1)."""
+        """Pool row indices [n, L, S] of Q and of the new K/V rows for steps [step0, step1);
+        each log row lists, per slot (or probe batch position), (prompt, sample, t) or None."""
         c, wl = self.cfg, self.wl
-        n, S = step1 - step0, c.num_slots
+        # rows are as wide as the widest step of the window (slots, or a probe batch)
+        n, S = step1 - step0, max([c.num_slots] + [len(log[k]) for k in range(step0, step1)])
         qi = np.zeros((n, c.layers, S), dtype=np.int64)
         ki = np.zeros((n, c.layers, S), dtype=np.int64)
         # Group the (slot, step) entries by sample so each sample's rows come from one call.
