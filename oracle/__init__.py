@@ -12,6 +12,8 @@ Two parts, both plain and slow on purpose:
   concatenation of the shared prompt KV and the sample's own response KV
   (Sections 2.1, 3.1 and 3.2 of the paper: one prompt KV cache shared by the
   whole group, one private response buffer per active sample).
+* ``fp8`` -- OCP E4M3 rounding, for the FP8-stored KV cache (the paper's
+  future-work direction of KV cache compression).
 * ``simulator`` -- the step-by-step slot / refill process of naive micro
   sampling groups (Section 3.1), fixed-slot continuous sampling (Section 3.2)
   continuous refill in FIFO or shortest-job-first order (Algorithms 1
@@ -24,10 +26,15 @@ a library routine, brute force and a hand-derived worked example.
 """
 
 from .attention import attend, attend_slot, attention_weights, default_scale
+from .fp8 import E4M3_MAX, decode_e4m3, encode_e4m3, round_e4m3
 from .simulator import (FPTAS_EPSILON, POLICIES, DynamicResult, SimResult, fptas_assign, simulate,
                         simulate_dynamic, simulate_group)
 
 __all__ = [
+    "E4M3_MAX",
+    "decode_e4m3",
+    "encode_e4m3",
+    "round_e4m3",
     "attend",
     "attend_slot",
     "attention_weights",

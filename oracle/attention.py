@@ -57,13 +57,14 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, hpk: int, scale: float) 
     return out
 
 
-def attend_slot(wl, l: int, p: int, i: int, t: int, scale=None) -> np.ndarray:
+def attend_slot(wl, l: int, p: int, i: int, t: int, scale=None, kv_fp8: bool = False) -> np.ndarray:
     """Output of a live slot holding sample i of prompt p, at layer l, at the
     step where the sample's response holds t tokens (the new one included).
 
     Keys and values are prompt p's prefix followed by the sample's own t
     generated tokens; the values depend only on (l, p, i, t), never on which
-    slot or step served them.
+    slot or step served them.  kv_fp8: the KV cache holds every key and value
+    rounded to E4M3 (the query is not rounded).
     """
     if t < 1:
         raise ValueError("a live slot attends to at least its own new token")
@@ -74,4 +75,7 @@ def attend_slot(wl, l: int, p: int, i: int, t: int, scale=None) -> np.ndarray:
     ks, vs = wl.suffix_kv(l, p, i, t)
     k = np.concatenate([kp, ks], axis=0)
     v = np.concatenate([vp, vs], axis=0)
+    if kv_fp8:
+        from .fp8 import round_e4m3
+        k, v = round_e4m3(k), round_e4m3(v)
     return attend(wl.query(l, p, i, t), k, v, c.hpk, scale)
