@@ -212,6 +212,15 @@ infs_status infs_decode_step(infs_ctx* ctx, int32_t layer, const void* q_dev, co
    exactly once since the previous end_step (a step with no live slot needs no decode). */
 infs_status infs_end_step(infs_ctx* ctx);
 
+/* Read-back of the stores (synchronises; for checks and debugging).  Elements come back as stored:
+   fp32, bf16 bit patterns, or E4M3 codes for an FP8 KV cache.
+   infs_read_prefix: one prompt's prefilled K and V of one layer, [prompt_len, Hkv, d] each.
+   infs_read_response: the response K and V of a live slot's sample for one layer, [len, Hkv, d]
+   each, len = the slot's current length (infs_slot_state).  E_STATE in a dry-run context, for an
+   unprefilled prompt or empty slot, or while a step is open. */
+infs_status infs_read_prefix(infs_ctx* ctx, int32_t prompt, int32_t layer, void* k_host, void* v_host);
+infs_status infs_read_response(infs_ctx* ctx, int32_t slot, int32_t layer, void* k_host, void* v_host);
+
 /* Host mirror of a slot: *sample_id = -1 and *len = 0 when empty. */
 infs_status infs_slot_state(const infs_ctx* ctx, int32_t slot, int64_t* sample_id, int32_t* len);
 

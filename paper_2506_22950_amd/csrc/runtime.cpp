@@ -49,7 +49,8 @@ struct infs_ctx {
   KernelKey key{};
   int S = 0, m = 0, G = 0, hpk = 0, D = 0, Hkv = 0, Hq = 0, L = 0, NP = 0;
   int pmax_pad = 0, split = 0, prefix_split = 0, pages_per_slot = 0, num_pages = 0, pcmax = 0, scmax = 0;
-  size_t es = 0;
+  size_t es = 0;      // bytes per Q / K / V element handed over the ABI
+  size_t kv_es = 0;   // bytes per stored K / V element (prefix store and pages)
   size_t prefix_layer_bytes = 0, pool_layer_bytes = 0;
   int64_t ws_records = 0;
   // device memory
@@ -500,6 +501,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->Hq = k.num_q_heads;
   c->L = k.num_layers;
   c->es = k.dtype == INFS_BF16 ? 2 : 4;
+  c->kv_es = c->es;
   c->split = k.split_tokens ? k.split_tokens : 256;
   c->pmax_pad = std::max(32, (k.max_prompt_len + 31) / 32 * 32);
   c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);
@@ -514,8 +516,8 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->prefix_split = key.mfma ? infs::kMfmaPrefixSplit : c->split;
   c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->prefix_split));
   c->scmax = ceil_div(k.max_suffix_len, c->split);
-  c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->es;
-  c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->es;
+  c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->kv_es;
+  c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->kv_es;
   c->ws_records = infs::workspace_records(key, c->NP, c->Hkv, c->pcmax, c->S, c->scmax);
   if (c->probe_k > 0)
     c->ws_records =
@@ -766,7 +768,7 @@ infs_status infs_probe_step(infs_ctx* c, int32_t layer, int32_t prompt, int32_t 
     a.vnew = v_new_dev;
     a.o = o_dev;
     a.prefix = c->prefix + c->prefix_layer_bytes * layer +
-               (size_t)prompt * c->Hkv * infs::prefix_elems_per_head(c->key, c->pmax_pad) * c->es;
+               (size_t)prompt * c->Hkv * infs::prefix_elems_per_head(c->key, c->pmax_pad) * c->kv_es;
     a.pool = c->pool + c->pool_layer_bytes * layer;
     a.tokens = c->tokens + (size_t)prompt * c->G;
     a.counters = c->counters + (size_t)(c->NP + c->S) * c->Hkv * infs::kCounterStride;
@@ -811,6 +813,82 @@ infs_status infs_probe_state(const infs_ctx* c, int32_t prompt, int64_t sample_i
   if (sample_id < 0 || sample_id >= c->G) return fail(cc, INFS_E_ARG, "sample_id out of range");
   if (!probe_len) return fail(cc, INFS_E_ARG, "null output pointer");
   *probe_len = c->probe_k > 0 ? c->probe_len[prompt][sample_id] : 0;
+  return INFS_OK;
+}
+
+infs_status infs_read_prefix(infs_ctx* c, int32_t prompt, int32_t layer, void* k_host, void* v_host) {
+  CHECK_CTX(c);
+  if (c->dry) return fail(c, INFS_E_STATE, "no device memory in a dry-run context");
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range [0, %d)", prompt, c->NP);
+  if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (!c->prefilled[prompt][layer]) return fail(c, INFS_E_STATE, "prompt %d layer %d is not prefilled", prompt, layer);
+  const int P = c->plen[prompt], D = c->D, Hkv = c->Hkv;
+  if (P > 0 && (!k_host || !v_host)) return fail(c, INFS_E_ARG, "null output pointer");
+  const size_t es = c->kv_es;
+  const size_t head_elems = (size_t)infs::prefix_elems_per_head(c->key, c->pmax_pad);
+  std::vector<uint8_t> buf(head_elems * Hkv * es);
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  HIP_TRY(c, hipMemcpy(buf.data(), c->prefix + c->prefix_layer_bytes * layer + (size_t)prompt * Hkv * head_elems * es,
+                       buf.size(), hipMemcpyDeviceToHost));
+  uint8_t* out[2] = {(uint8_t*)k_host, (uint8_t*)v_host};
+  auto put = [&](int kind, int tok, int g, int d, const uint8_t* src) {
+    std::memcpy(out[kind] + (((size_t)tok * Hkv + g) * D + d) * es, src, es);
+  };
+  for (int g = 0; g < Hkv; ++g) {
+    const uint8_t* head = buf.data() + (size_t)g * head_elems * es;
+    if (!c->key.mfma) {  // [K|V][max_prompt_len][D] rows
+      for (int kind = 0; kind < 2; ++kind)
+        for (int tok = 0; tok < P; ++tok)
+          for (int d = 0; d < D; ++d) put(kind, tok, g, d, head + (((size_t)kind * c->pmax_pad + tok) * D + d) * es);
+      continue;
+    }
+    // MFMA blocks of 32 tokens: K as [2 halves][D/32][64 lanes][8], V as [D/16][64 lanes][8] (see the kernels)
+    const int KB = D / 32, DB = D / 16;
+    for (int tok = 0; tok < P; ++tok) {
+      const int b = tok / infs::kMfmaBlock, r = tok % infs::kMfmaBlock;
+      const uint8_t* blk = head + (size_t)b * 2 * infs::kMfmaBlock * D * es;
+      const int mb = r / 16, i = r % 16;
+      for (int d = 0; d < D; ++d) {
+        const int kb = d / 32, q = (d % 32) / 8, e = d % 8;
+        put(0, tok, g, d, blk + ((size_t)((mb * KB + kb) * 64 + q * 16 + i) * 8 + e) * es);
+      }
+      // token r sits at lane quarter q, element e with r = 4q+e (e < 4) or 16+4q+(e-4)
+      const int q = (r % 16) / 4, e = (r < 16 ? 0 : 4) + r % 4;
+      for (int d = 0; d < D; ++d) {
+        const int db = d / 16, j = d % 16;
+        put(1, tok, g, d, blk + ((size_t)infs::kMfmaBlock * D + (size_t)((db * 64 + q * 16 + j) * 8 + e)) * es);
+      }
+      (void)DB;
+    }
+  }
+  return INFS_OK;
+}
+
+infs_status infs_read_response(infs_ctx* c, int32_t slot, int32_t layer, void* k_host, void* v_host) {
+  CHECK_CTX(c);
+  if (c->dry) return fail(c, INFS_E_STATE, "no device memory in a dry-run context");
+  if (slot < 0 || slot >= c->S) return fail(c, INFS_E_ARG, "slot %d out of range [0, %d)", slot, c->S);
+  if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
+  if (c->slot_sample[slot] < 0) return fail(c, INFS_E_STATE, "slot %d is empty", slot);
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "read while a step is open");
+  const int len = c->slot_len[slot], D = c->D, Hkv = c->Hkv;
+  if (len > 0 && (!k_host || !v_host)) return fail(c, INFS_E_ARG, "null output pointer");
+  const size_t es = c->kv_es, rowb = (size_t)D * es, pageb = (size_t)infs::kPageTokens * rowb;
+  const std::vector<int32_t>& pages = c->seq_pages[c->slot_handle[slot]];
+  std::vector<uint8_t> buf((size_t)Hkv * 2 * pageb);
+  uint8_t* out[2] = {(uint8_t*)k_host, (uint8_t*)v_host};
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (int lp = 0; lp * infs::kPageTokens < len; ++lp) {
+    HIP_TRY(c, hipMemcpy(buf.data(), c->pool + c->pool_layer_bytes * layer + (size_t)pages[lp] * buf.size(), buf.size(),
+                         hipMemcpyDeviceToHost));
+    for (int r = 0; r < infs::kPageTokens && lp * infs::kPageTokens + r < len; ++r) {
+      const int tok = lp * infs::kPageTokens + r;
+      for (int g = 0; g < Hkv; ++g)
+        for (int kind = 0; kind < 2; ++kind)
+          std::memcpy(out[kind] + ((size_t)tok * Hkv + g) * rowb,
+                      buf.data() + ((size_t)g * 2 + kind) * pageb + (size_t)r * rowb, rowb);
+    }
+  }
   return INFS_OK;
 }
 

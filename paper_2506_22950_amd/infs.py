@@ -24,6 +24,7 @@ POLICY = {"naive": NAIVE, "fixed_row": FIXED_ROW, "fifo": FIFO, "sjf": SJF, "fpt
           "lpt": LPT}
 FPTAS_EPSILON = 0.1
 FLAG_DRY_RUN = 1
+FLAG_KV_FP8 = 2
 
 # Every symbol include/infs.h declares.
 EXPORTS = (
@@ -32,7 +33,7 @@ EXPORTS = (
     "infs_sample_tokens", "infs_sync", "infs_get_stats", "infs_timing_begin", "infs_timing_end",
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
-    "infs_probe_state", "infs_release_sample",
+    "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response",
 )
 
 
@@ -100,6 +101,8 @@ def load():
         "infs_probe_batch": (I32, [P]),
         "infs_probe_state": (I32, [P, I32, I64, ctypes.POINTER(I32)]),
         "infs_release_sample": (I32, [P, I32, I64]),
+        "infs_read_prefix": (I32, [P, I32, I32, P, P]),
+        "infs_read_response": (I32, [P, I32, I32, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -216,6 +219,30 @@ class Context:
 
     def release_sample(self, prompt, sample_id):
         self._call(load().infs_release_sample, prompt, sample_id)
+
+    def _kv_dtype(self):
+        if self.config.flags & FLAG_KV_FP8:
+            return np.uint8
+        return np.uint16 if self.config.dtype == BF16 else np.float32
+
+    def read_prefix(self, prompt, layer, prompt_len):
+        """(K, V) of a prefilled prompt as stored, numpy [prompt_len, Hkv, d]."""
+        c = self.config
+        shape = (prompt_len, c.num_kv_heads, c.head_dim)
+        k = np.zeros(shape, dtype=self._kv_dtype())
+        v = np.zeros(shape, dtype=self._kv_dtype())
+        self._call(load().infs_read_prefix, prompt, layer, k.ctypes.data, v.ctypes.data)
+        return k, v
+
+    def read_response(self, slot, layer):
+        """(K, V) of a live slot's response as stored, numpy [len, Hkv, d]."""
+        c = self.config
+        _, n = self.slot_state(slot)
+        shape = (n, c.num_kv_heads, c.head_dim)
+        k = np.zeros(shape, dtype=self._kv_dtype())
+        v = np.zeros(shape, dtype=self._kv_dtype())
+        self._call(load().infs_read_response, slot, layer, k.ctypes.data, v.ctypes.data)
+        return k, v
 
     def get_stats(self) -> Stats:
         s = Stats()

@@ -22,10 +22,12 @@ def say(*a):
 
 
 def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
-                  probe=None):
+                  probe=None, inspect=None, kv_fp8=False):
     """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
     reuse first; if `probe` is a dict it receives 'log' (probe step log) and
-    'captured' (the O buffer [L, batch, Hq, d] after every probe step)."""
+    'captured' (the O buffer [L, batch, Hq, d] after every probe step).
+    inspect(ctx, step, log) is called after every decode step; kv_fp8 stores the
+    KV cache as E4M3."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
@@ -34,7 +36,7 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
     log = plan_steps(cfg, wl.L, policy, wl.L_hat, stop_after=stop_after, reuse=reuse, probe_log=plog)
     dev = DeviceInputs(wl)
     stream = torch.cuda.current_stream()
-    ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse)
+    ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse, kv_fp8=kv_fp8)
     keep = []
     for p in range(cfg.num_prompts):
         for layer in range(cfg.layers):
@@ -65,6 +67,8 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
     def after(step):
         if capture(step):
             captured[step] = o.cpu().numpy()
+        if inspect is not None:
+            inspect(ctx, step, log)
 
     t0 = time.time()
     if reuse:
