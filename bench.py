@@ -181,24 +181,28 @@ def schedule_table(n_groups=64, G=32, m=4, cap=1024):
     return "\n".join(out)
 
 
-def algorithmic_bytes(cfg, steplog):
+def algorithmic_bytes(cfg, steplog, kv_bytes=None):
     """Algorithmic HBM bytes of all decode launches, from the step log alone:
-    prefix K/V once per prompt with a live slot, each live slot's response K/V
-    (new token included), the append write, Q read and fp32 O write."""
-    kvrow = cfg.num_kv_heads * cfg.head_dim * cfg.elem_bytes
+    prefix K/V once per prompt with a live slot, each live slot's stored
+    response K/V, the new token's K/V read and append write, Q read and fp32 O
+    write.  kv_bytes: stored bytes per K/V element (default: the input size)."""
+    kvb = cfg.elem_bytes if kv_bytes is None else kv_bytes
+    kvrow = cfg.num_kv_heads * cfg.head_dim * kvb
+    kvrow_in = cfg.num_kv_heads * cfg.head_dim * cfg.elem_bytes
     total = 0.0
     for row in steplog:
         live_prompts = {e[0] for e in row if e is not None}
         b = sum(2.0 * cfg.prompt_lens[p] * kvrow for p in live_prompts)
         for e in row:
             if e is not None:
-                b += 2.0 * e[2] * kvrow + 2.0 * kvrow + cfg.num_q_heads * cfg.head_dim * (cfg.elem_bytes + 4)
+                b += (2.0 * (e[2] - 1) * kvrow + 2.0 * kvrow_in + 2.0 * kvrow
+                      + cfg.num_q_heads * cfg.head_dim * (cfg.elem_bytes + 4))
         total += b
     return total * cfg.layers
 
 
 class Bench:
-    def __init__(self, cfg_name, split=0, reuse=0):
+    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False):
         import numpy as np
         import torch
 
@@ -227,7 +231,8 @@ class Bench:
         del dev
         torch.cuda.synchronize()
         self.stream = torch.cuda.current_stream()
-        self.ctx = context_for(cfg, stream=self.stream, split_tokens=split, probe_tokens=reuse)
+        self.ctx = context_for(cfg, stream=self.stream, split_tokens=split, probe_tokens=reuse, kv_fp8=kv_fp8)
+        self.kv_bytes = 1 if kv_fp8 else cfg.elem_bytes
         L, S, Hq, Hkv, d, es = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.elem_bytes
         self.o = torch.empty((L, S, Hq, d), dtype=torch.float32, device="cuda")
         self.qp, self.kp, self.vp, self.op = (self.q.data_ptr(), self.k.data_ptr(), self.v.data_ptr(),
@@ -235,8 +240,8 @@ class Bench:
         self.sq, self.skv, self.so = S * Hq * d * es, S * Hkv * d * es, S * Hq * d * 4
         self.L = L
         self.tokens = wl.total_tokens
-        self.alg_bytes = algorithmic_bytes(cfg, self.log)
-        self.probe_alg_bytes = algorithmic_bytes(cfg, self.plog) if reuse else 0.0
+        self.alg_bytes = algorithmic_bytes(cfg, self.log, self.kv_bytes)
+        self.probe_alg_bytes = algorithmic_bytes(cfg, self.plog, self.kv_bytes) if reuse else 0.0
         log(f"setup {time.time() - t0:.1f}s: {len(self.log)} steps ({cfg.policy}) vs {self.naive_steps} naive, "
             f"{self.tokens} tokens, staged {(self.q.numel() + self.k.numel() + self.v.numel()) * es / 2**30:.1f} GiB")
 
@@ -357,6 +362,8 @@ def main():
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--reuse", type=int, default=0, metavar="K",
                     help="prefix reuse: every sample decodes K probe tokens first (Section 4); default 0")
+    ap.add_argument("--kv-fp8", action="store_true",
+                    help="store the KV cache as E4M3 (halves the K/V bytes; not the headline configuration)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -380,7 +387,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         copy_calibration(torch)
-    b = Bench(args.workload, split=args.split, reuse=args.reuse)
+    b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8)
 
     for w in range(args.warmup):
         t0 = time.time()
@@ -410,7 +417,7 @@ def main():
         avg_us = ms * 1000.0 / n
         per_launch = alg / n
         achieved = per_launch / (avg_us * 1e-6) / 1e9
-        traffic = read_traffic(args.workload) if not args.reuse else None
+        traffic = read_traffic(args.workload) if not (args.reuse or args.kv_fp8) else None
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
@@ -458,6 +465,7 @@ def main():
             "alg_bytes_per_group": round(b.alg_bytes),
             "end_to_end_alg_GBps": round((b.alg_bytes + b.probe_alg_bytes) / (ms_per_step / 1e3) / 1e9, 1),
             "probe_tokens": args.reuse, "probe_steps": len(b.plog),
+            "kv_cache": "e4m3" if args.kv_fp8 else cfg.dtype,
         },
         "roofline": roof,
         "probe": probe,

@@ -88,6 +88,13 @@ typedef enum infs_policy {
    Lets the slot / page / step state machine run on a host without a GPU. */
 #define INFS_FLAG_DRY_RUN 1u
 
+/* Store the KV cache (prefix store and response pages) as OCP E4M3 bytes: half the bytes of bf16 per
+   token, in the direction of the KV-cache compression the paper names as future work.  K/V still
+   come in as bf16 and are rounded to nearest even (magnitudes beyond 448 saturate) when stored;
+   attention reads the stored values (the newest token included) and computes as for bf16.  Needs
+   dtype INFS_BF16, head_dim 128 and at least 16 prefix rows (slots_per_prompt * heads per KV head). */
+#define INFS_FLAG_KV_FP8 2u
+
 typedef struct infs_config {
     int32_t num_layers;          /* >= 1 */
     int32_t num_q_heads;         /* Hq, a multiple of num_kv_heads */
@@ -120,8 +127,9 @@ typedef struct infs_stats {
     int64_t launches;            /* attention kernel launches (one per decode_step or probe_step) */
     int64_t tokens;              /* tokens generated (live slots summed over steps, probe tokens included) */
     double alg_bytes;            /* algorithmic HBM bytes of all decode_step and probe_step launches: prefix K/V
-                                    once per prompt with a live slot, each live slot's response K/V,
-                                    new K/V read and append write, Q read, O write */
+                                    once per prompt with a live slot, each live slot's stored response K/V,
+                                    new K/V read and append write, Q read, O write (K/V at their stored
+                                    size) */
     double alg_flops;            /* 4 * Hq * d * (P + t) per live slot and layer */
 } infs_stats;
 

@@ -14,16 +14,17 @@ struct KernelKey {
   int hpk;         // query heads per KV head
   int mfma;        // 1: prefix rows go through MFMA tiles, 0: wavefront reductions
   int prefix_rows; // rows of one prompt's prefix work item, padded (wave: 8/16; MFMA: 16/32/64/128)
+  int kv8;         // 1: K/V stored as E4M3 (bf16 MFMA shapes of head_dim 128)
 };
 
 // Resolve the padded prefix row count and path for a shape; false if no
 // instantiation exists.
-bool select_kernel(int bf16, int head_dim, int hpk, int prefix_rows_real, KernelKey* key);
+bool select_kernel(int bf16, int head_dim, int hpk, int prefix_rows_real, int kv8, KernelKey* key);
 
 // The same with the prefix path fixed (mfma 1: MFMA tiles, 0: wavefront
 // reductions): a second kernel of a context must read the prefix store in the
 // layout its first kernel chose.
-bool select_kernel_path(int bf16, int head_dim, int hpk, int prefix_rows_real, int mfma, KernelKey* key);
+bool select_kernel_path(int bf16, int head_dim, int hpk, int prefix_rows_real, int mfma, int kv8, KernelKey* key);
 
 // Record layout of the split-K workspace for a key.
 int64_t workspace_records(const KernelKey& key, int num_prompts, int hkv, int prefix_chunks_max,

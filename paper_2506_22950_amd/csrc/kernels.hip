@@ -107,9 +107,12 @@ __device__ __forceinline__ void axpy16B(float* o, float p, const u32x4& v) {
 }
 
 // Compile-time shape of one kernel instantiation.
-template <bool BF_, int D_, int HPK_, bool MFMA_, int PR_>
+template <bool BF_, int D_, int HPK_, bool MFMA_, int PR_, bool KV8_ = false>
 struct Shape {
   static constexpr bool BF = BF_;
+  // KV8: the prefix store and the pages hold K/V as E4M3 bytes; the kernels
+  // widen them to bf16 in registers (exact) and compute as for bf16.
+  static constexpr bool KV8 = KV8_;
   static constexpr int D = D_;
   static constexpr int HPK = HPK_;
   static constexpr bool MFMA = MFMA_;
@@ -119,7 +122,10 @@ struct Shape {
   static constexpr int ROWB = D * ES;              // bytes of one K or V row of one head
   static constexpr int LPT = ROWB / 16;            // lanes per token (wavefront path)
   static constexpr int TPI = 64 / LPT;             // tokens per load instruction
-  static constexpr int PAGEB = kPageTokens * ROWB; // bytes of one page of one head, K or V
+  static constexpr int KES = KV8 ? 1 : ES;        // bytes per stored K/V element
+  static constexpr int KROWB = D * KES;            // bytes of one stored K or V row of one head
+  static constexpr int LANEB = EPL * KES;          // stored bytes behind one lane's EPL elements
+  static constexpr int PAGEB = kPageTokens * KROWB; // bytes of one page of one head, K or V
   static constexpr int NB = PR / 16;               // MFMA row blocks
   static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
   static constexpr int DB = D / 16;                // MFMA 16-wide head_dim blocks
@@ -137,6 +143,7 @@ struct Shape {
   static constexpr int MIN_WAVES = ROWSPLIT ? 2 : ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
   static_assert(LPT >= 2 && LPT <= 64, "row size");
   static_assert(!MFMA || BF, "MFMA path is bf16");
+  static_assert(!KV8 || (BF && MFMA), "FP8 KV on the bf16 MFMA shapes");
   static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
 };
 
@@ -164,6 +171,45 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t ws_rsrc(const StepArgs& a) {
 }
 __device__ __forceinline__ void st_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kCoherentPolicy);
+}
+
+// E4M3 (OCP) <-> bf16.  Widening is exact: every E4M3 value is a bf16 value.
+// Narrowing rounds to nearest even; magnitudes beyond 448 are clamped first,
+// so the conversion saturates instead of producing NaN.
+__device__ __forceinline__ u32x4 widen_e4m3(uint2 w) {
+  u32x4 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, false));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, true));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, false));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, true));
+  return r;
+}
+__device__ __forceinline__ float sat_e4m3(float x) { return fminf(fmaxf(x, -448.f), 448.f); }
+__device__ __forceinline__ uint32_t narrow4_e4m3(uint32_t lo, uint32_t hi) {  // 4 bf16 -> 4 E4M3 bytes
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(sat_e4m3(__uint_as_float(lo << 16)), sat_e4m3(__uint_as_float(lo & 0xffff0000u)),
+                                          0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(sat_e4m3(__uint_as_float(hi << 16)), sat_e4m3(__uint_as_float(hi & 0xffff0000u)),
+                                      w, true);
+  return (uint32_t)w;
+}
+__device__ __forceinline__ uint2 narrow_e4m3(const u32x4& v) {  // 8 bf16 -> 8 E4M3 bytes
+  return uint2{narrow4_e4m3(v.x, v.y), narrow4_e4m3(v.z, v.w)};
+}
+// One lane's EPL stored elements as a 16-byte register of the compute type.
+template <class SH>
+__device__ __forceinline__ u32x4 ld_kv(const char* p) {
+  if constexpr (SH::KV8)
+    return widen_e4m3(*(const uint2*)p);
+  else
+    return *(const u32x4*)p;
+}
+// Store one lane's EPL elements (given in the compute type) into a stored row.
+template <class SH>
+__device__ __forceinline__ void st_kv(char* p, const u32x4& v) {
+  if constexpr (SH::KV8)
+    *(uint2*)p = narrow_e4m3(v);
+  else
+    *(u32x4*)p = v;
 }
 
 __device__ __forceinline__ float wave_max(float x) {
@@ -228,7 +274,7 @@ __device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, con
 #pragma unroll
         for (int u = b * SB; u < b * SB + SB; ++u) {
           u32x4& dst = kind ? vv[u] : kk[u];
-          dst = *ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1);
+          dst = ld_kv<SH>(ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1));
         }
     }
 #pragma unroll
@@ -377,26 +423,26 @@ template <class SH>
 struct PrefixAddr {
   const char* base[2];
   __device__ int page(int) const { return 0; }
-  __device__ const u32x4* row(int kind, int tokbase, int, int, int end) const {
+  __device__ const char* row(int kind, int tokbase, int, int, int end) const {
     const int lane = threadIdx.x & 63;
     const int tok = min(tokbase + lane / SH::LPT, end - 1);
-    return (const u32x4*)(base[kind] + (int64_t)tok * SH::ROWB) + lane % SH::LPT;
+    return base[kind] + (int64_t)tok * SH::KROWB + (lane % SH::LPT) * SH::LANEB;
   }
 };
 
 // Addressing of a slot's stored response tokens: pages [page][kv][K|V][16][D].
 // Lane i of `pages` holds the page of the wave's i-th 16-token group.  A load
 // instruction covers TPI consecutive tokens of one page, so its address is
-// (page base) + (token in page) * ROWB + lane * 16 -- uniform plus lane offset.
+// (page base) + (token in page) * KROWB + lane * LANEB -- uniform plus lane offset.
 template <class SH>
 struct SuffixAddr {
   const char* pool;
   int pages;
   int hkv, g;
   __device__ int page(int pslot) const { return __builtin_amdgcn_readlane(pages, pslot); }
-  __device__ const u32x4* row(int kind, int tokbase, int, int pg, int) const {
+  __device__ const char* row(int kind, int tokbase, int, int pg, int) const {
     const int lane = threadIdx.x & 63;
-    return (const u32x4*)(pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tokbase & 15) * SH::ROWB) + lane;
+    return pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tokbase & 15) * SH::KROWB + lane * SH::LANEB;
   }
 };
 
@@ -425,8 +471,8 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
       q[r] = u32x4{0, 0, 0, 0};
   }
   const int64_t head = ((int64_t)p * a.Hkv + g) * 2;
-  PrefixAddr<SH> ad{{(const char*)a.prefix + head * a.max_prompt_len * SH::ROWB,
-                     (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::ROWB}};
+  PrefixAddr<SH> ad{{(const char*)a.prefix + head * a.max_prompt_len * SH::KROWB,
+                     (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::KROWB}};
   float m[PR], l[PR], o[PR][SH::EPL];
   wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
   wave_combine_groups<SH, PR>(m, l, o);
@@ -588,21 +634,22 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
     for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const uint16_t* head = (const uint16_t*)a.prefix +
-                         ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D);
+  const char* head = (const char*)a.prefix +
+                     ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
   // One 32-token block (16 KB of K and V) in flight per wavefront: the
   // register budget is kept at two wavefronts per SIMD, and the second
   // wavefront hides this one's load latency.
   for (int b = b0; b < b1; ++b) {
     bf16x8 ka[2][KB], va[DB];
-    const uint16_t* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D);
-    const uint16_t* vblk = kblk + kMfmaBlock * D;
+    const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
+    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = *(const bf16x8*)(kblk + ((mb * KB + kb) * 64 + lane) * 8);
+      for (int kb = 0; kb < KB; ++kb)
+        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
 #pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
+    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
     mfma_block<SH>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
   }
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
@@ -646,18 +693,19 @@ __device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const uint16_t* head = (const uint16_t*)a.prefix +
-                         ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D);
+  const char* head = (const char*)a.prefix +
+                     ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
   for (int b = 0; b < nblk; ++b) {
     bf16x8 ka[2][KB], va[DB];
-    const uint16_t* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D);
-    const uint16_t* vblk = kblk + kMfmaBlock * D;
+    const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
+    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = *(const bf16x8*)(kblk + ((mb * KB + kb) * 64 + lane) * 8);
+      for (int kb = 0; kb < KB; ++kb)
+        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
 #pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = *(const bf16x8*)(vblk + (db * 64 + lane) * 8);
+    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
     mfma_block<WS>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
   }
 #pragma unroll
@@ -711,6 +759,10 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   if (has_new) {
     knew = *((const u32x4*)((const char*)a.knew + newrow) + ch);
     vnew = *((const u32x4*)((const char*)a.vnew + newrow) + ch);
+    if constexpr (SH::KV8) {  // attend to the token as the cache stores it
+      knew = widen_e4m3(narrow_e4m3(knew));
+      vnew = widen_e4m3(narrow_e4m3(vnew));
+    }
   }
   SuffixAddr<SH> ad{(const char*)a.pool, pages, a.Hkv, g};
   float m[HPK], l[HPK], o[HPK][SH::EPL];
@@ -718,9 +770,10 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   if (has_new) {
     fold_token<SH, HPK>(knew, vnew, q, a.scale_log2, m, l, o);
     if (lane < SH::LPT) {
-      char* row = (char*)a.pool + (int64_t)(sp.cur_page * a.Hkv + g) * 2 * SH::PAGEB + (last & 15) * SH::ROWB;
-      *((u32x4*)row + ch) = knew;
-      *((u32x4*)(row + SH::PAGEB) + ch) = vnew;
+      char* row = (char*)a.pool + (int64_t)(sp.cur_page * a.Hkv + g) * 2 * SH::PAGEB + (last & 15) * SH::KROWB +
+                  ch * SH::LANEB;
+      st_kv<SH>(row, knew);
+      st_kv<SH>(row + SH::PAGEB, vnew);
     }
   }
   wave_combine_groups<SH, HPK>(m, l, o);
@@ -978,9 +1031,9 @@ __global__ __launch_bounds__(256) void prefill_plain_kernel(char* store, const c
 // tau(8q+e) = 4q+e for e < 4 and 16+4q+(e-4) otherwise -- the order in which
 // a lane holds probabilities after the S^T tiles.  Padding tokens are zero.
 template <class SH>
-__global__ __launch_bounds__(256) void prefill_mfma_kernel(uint16_t* store, const uint16_t* k, const uint16_t* v,
+__global__ __launch_bounds__(256) void prefill_mfma_kernel(char* store, const uint16_t* k, const uint16_t* v,
                                                           int prompt, int plen, int hkv, int pmax) {
-  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB;
+  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, KES = SH::KES;
   constexpr int KU = 2 * KB * 64, VU = DB * 64, BU = KU + VU;
   const int nblk = (plen + kMfmaBlock - 1) / kMfmaBlock;
   const int64_t units = (int64_t)hkv * nblk * BU;
@@ -989,17 +1042,16 @@ __global__ __launch_bounds__(256) void prefill_mfma_kernel(uint16_t* store, cons
     const int rem = u - (int64_t)g * nblk * BU;
     const int b = rem / BU;
     int x = rem - b * BU;
-    uint16_t* blk = store + (((int64_t)prompt * hkv + g) * (pmax / kMfmaBlock) + b) * (2 * kMfmaBlock * D);
+    char* blk = store + (((int64_t)prompt * hkv + g) * (pmax / kMfmaBlock) + b) * (2 * kMfmaBlock * D * KES);
     uint16_t vals[8];
+    char* dst;
     if (x < KU) {
       const int lane = x & 63, sub = x >> 6, mb = sub / KB, kb = sub - mb * KB;
       const int tok = b * kMfmaBlock + mb * 16 + (lane & 15);
       const int d0 = kb * 32 + (lane >> 4) * 8;
 #pragma unroll
       for (int e = 0; e < 8; ++e) vals[e] = tok < plen ? k[((int64_t)tok * hkv + g) * D + d0 + e] : 0;
-      uint16_t* dst = blk + (int64_t)x * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) dst[e] = vals[e];
+      dst = blk + (int64_t)x * 8 * KES;
     } else {
       x -= KU;
       const int lane = x & 63, db = x >> 6, qq = lane >> 4;
@@ -1009,10 +1061,14 @@ __global__ __launch_bounds__(256) void prefill_mfma_kernel(uint16_t* store, cons
         const int tok = b * kMfmaBlock + (e < 4 ? 4 * qq + e : 16 + 4 * qq + (e - 4));
         vals[e] = tok < plen ? v[((int64_t)tok * hkv + g) * D + d] : 0;
       }
-      uint16_t* dst = blk + kMfmaBlock * D + (int64_t)x * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) dst[e] = vals[e];
+      dst = blk + (int64_t)kMfmaBlock * D * KES + (int64_t)x * 8 * KES;
     }
+    u32x4 w;
+    w.x = vals[0] | ((uint32_t)vals[1] << 16);
+    w.y = vals[2] | ((uint32_t)vals[3] << 16);
+    w.z = vals[4] | ((uint32_t)vals[5] << 16);
+    w.w = vals[6] | ((uint32_t)vals[7] << 16);
+    st_kv<SH>(dst, w);
   }
 }
 
@@ -1057,27 +1113,45 @@ struct Entry {
   X(true, 128, 8, true, 64)  \
   X(true, 128, 8, true, 128)
 
-#define INFS_ENTRY(bf, d, hpk, mf, pr) \
-  {{bf, d, hpk, mf, pr}, decode_kernel<Shape<bf, d, hpk, mf, pr>>, Shape<bf, d, hpk, mf, pr>::SMEM},
+// FP8 KV cache: bf16 MFMA shapes of head_dim 128.
+#define INFS_KERNELS_KV8(X) \
+  X(128, 1, 16)             \
+  X(128, 1, 32)             \
+  X(128, 1, 64)             \
+  X(128, 2, 16)             \
+  X(128, 2, 32)             \
+  X(128, 2, 64)             \
+  X(128, 2, 128)            \
+  X(128, 4, 16)             \
+  X(128, 4, 32)             \
+  X(128, 4, 64)             \
+  X(128, 4, 128)            \
+  X(128, 8, 64)             \
+  X(128, 8, 128)
 
-const Entry kTable[] = {INFS_KERNELS(INFS_ENTRY)};
+#define INFS_ENTRY(bf, d, hpk, mf, pr) \
+  {{bf, d, hpk, mf, pr, 0}, decode_kernel<Shape<bf, d, hpk, mf, pr>>, Shape<bf, d, hpk, mf, pr>::SMEM},
+#define INFS_ENTRY_KV8(d, hpk, pr) \
+  {{1, d, hpk, 1, pr, 1}, decode_kernel<Shape<true, d, hpk, true, pr, true>>, Shape<true, d, hpk, true, pr, true>::SMEM},
+
+const Entry kTable[] = {INFS_KERNELS(INFS_ENTRY) INFS_KERNELS_KV8(INFS_ENTRY_KV8)};
 
 const Entry* find_entry(const KernelKey& k) {
   for (const Entry& e : kTable)
     if (e.key.bf16 == k.bf16 && e.key.head_dim == k.head_dim && e.key.hpk == k.hpk && e.key.mfma == k.mfma &&
-        e.key.prefix_rows == k.prefix_rows)
+        e.key.prefix_rows == k.prefix_rows && e.key.kv8 == k.kv8)
       return &e;
   return nullptr;
 }
 
 }  // namespace
 
-bool select_kernel(int bf16, int head_dim, int hpk, int rows, KernelKey* key) {
-  return select_kernel_path(bf16, head_dim, hpk, rows, bf16 && rows >= 16, key);
+bool select_kernel(int bf16, int head_dim, int hpk, int rows, int kv8, KernelKey* key) {
+  return select_kernel_path(bf16, head_dim, hpk, rows, bf16 && rows >= 16, kv8, key);
 }
 
-bool select_kernel_path(int bf16, int head_dim, int hpk, int rows, int mfma, KernelKey* key) {
-  KernelKey k{bf16, head_dim, hpk, mfma && bf16 ? 1 : 0, 0};
+bool select_kernel_path(int bf16, int head_dim, int hpk, int rows, int mfma, int kv8, KernelKey* key) {
+  KernelKey k{bf16, head_dim, hpk, mfma && bf16 ? 1 : 0, 0, kv8 ? 1 : 0};
   if (k.mfma)
     k.prefix_rows = rows <= 16 ? 16 : rows <= 32 ? 32 : rows <= 64 ? 64 : rows <= 128 ? 128 : 0;
   else
@@ -1094,6 +1168,7 @@ int64_t workspace_records(const KernelKey& key, int num_prompts, int hkv, int pr
 }
 
 int64_t prefix_elems_per_head(const KernelKey& key, int pmax_padded) {
+  // elements, whatever their size (E4M3 bytes with key.kv8)
   return (int64_t)2 * pmax_padded * key.head_dim;
 }
 
@@ -1104,11 +1179,11 @@ hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, h
   return hipGetLastError();
 }
 
-#define INFS_PREFILL_CASE(bf, d, mf)                                                                    \
-  if (key.bf16 == bf && key.head_dim == d && key.mfma == mf) {                                         \
-    using SH = Shape<bf, d, 1, mf, mf ? 16 : 8>;                                                       \
+#define INFS_PREFILL_CASE(bf, d, mf, k8)                                                               \
+  if (key.bf16 == bf && key.head_dim == d && key.mfma == mf && key.kv8 == (k8 ? 1 : 0)) {              \
+    using SH = Shape<bf, d, 1, mf, mf ? 16 : 8, k8>;                                                   \
     if constexpr (mf)                                                                                  \
-      hipLaunchKernelGGL(prefill_mfma_kernel<SH>, dim3(grid), dim3(256), 0, stream, (uint16_t*)store,  \
+      hipLaunchKernelGGL(prefill_mfma_kernel<SH>, dim3(grid), dim3(256), 0, stream, (char*)store,      \
                          (const uint16_t*)k, (const uint16_t*)v, prompt, plen, hkv, pmax);             \
     else                                                                                               \
       hipLaunchKernelGGL(prefill_plain_kernel<SH>, dim3(grid), dim3(256), 0, stream, (char*)store,     \
@@ -1121,12 +1196,13 @@ hipError_t launch_prefill(const KernelKey& key, void* store, const void* k, cons
   if (plen == 0) return hipSuccess;
   const int64_t units = (int64_t)hkv * 2 * ((plen + 31) / 32) * 32 * key.head_dim;
   const int grid = (int)((units / 8 + 255) / 256 < 4096 ? (units / 8 + 255) / 256 : 4096);
-  INFS_PREFILL_CASE(false, 64, 0)
-  INFS_PREFILL_CASE(false, 128, 0)
-  INFS_PREFILL_CASE(true, 64, 0)
-  INFS_PREFILL_CASE(true, 128, 0)
-  INFS_PREFILL_CASE(true, 64, 1)
-  INFS_PREFILL_CASE(true, 128, 1)
+  INFS_PREFILL_CASE(false, 64, 0, false)
+  INFS_PREFILL_CASE(false, 128, 0, false)
+  INFS_PREFILL_CASE(true, 64, 0, false)
+  INFS_PREFILL_CASE(true, 128, 0, false)
+  INFS_PREFILL_CASE(true, 64, 1, false)
+  INFS_PREFILL_CASE(true, 128, 1, false)
+  INFS_PREFILL_CASE(true, 128, 1, true)
   return hipErrorInvalidValue;
 }
 

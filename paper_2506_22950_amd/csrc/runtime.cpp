@@ -206,7 +206,8 @@ infs_status open_step(infs_ctx* c) {
       return fail(c, INFS_E_STATE, "prompt %d has live slots but no prefilled prefix", p);
   }
   double bytes = 0, flops = 0;
-  const double kvrow = (double)c->Hkv * c->D * c->es;
+  const double kvrow = (double)c->Hkv * c->D * c->kv_es;    // one stored K or V row, all heads
+  const double kvrow_in = (double)c->Hkv * c->D * c->es;    // one caller K or V row
   for (int p = 0; p < c->NP; ++p) {
     infs::PromptPlan& pp = a.prompt[p];
     pp.plen = std::max(c->plen[p], 0);
@@ -242,7 +243,7 @@ infs_status open_step(infs_ctx* c) {
     const int nch = ceil_div(len, c->split);
     items += nch;
     const int P = a.prompt[s / c->m].plen;
-    bytes += 2.0 * len * kvrow + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
+    bytes += 2.0 * (len - 1) * kvrow + 2.0 * kvrow_in + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
     flops += 4.0 * c->Hq * c->D * (double)(P + len);
   }
   a.n_suffix_items = items;
@@ -286,7 +287,8 @@ infs_status open_probe(infs_ctx* c, int p, int first, int n, const uint8_t* live
   a.prefix_rows = n * c->hpk;
   a.clock_start = a.clock_end = nullptr;
   for (int q = 0; q < infs::kMaxPrompts; ++q) a.prompt[q] = infs::PromptPlan{};
-  const double kvrow = (double)c->Hkv * c->D * c->es;
+  const double kvrow = (double)c->Hkv * c->D * c->kv_es;    // one stored K or V row, all heads
+  const double kvrow_in = (double)c->Hkv * c->D * c->es;    // one caller K or V row
   double bytes = 0, flops = 0;
   infs::PromptPlan& pp = a.prompt[0];
   pp.plen = std::max(c->plen[p], 0);
@@ -316,7 +318,7 @@ infs_status open_probe(infs_ctx* c, int p, int first, int n, const uint8_t* live
     sp.sample = i;
     sp.cur_page = c->seq_pages[h][pos / infs::kPageTokens];
     items += ceil_div(len, c->split);
-    bytes += 2.0 * len * kvrow + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
+    bytes += 2.0 * (len - 1) * kvrow + 2.0 * kvrow_in + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
     flops += 4.0 * c->Hq * c->D * (double)(pp.plen + len);
   }
   a.n_suffix_items = items;
@@ -443,13 +445,17 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   if (k.num_pages < 0) return fail(nullptr, INFS_E_ARG, "num_pages must be >= 0");
   if (k.dtype != INFS_F32 && k.dtype != INFS_BF16) return fail(nullptr, INFS_E_ARG, "dtype must be INFS_F32 or INFS_BF16");
   if (!(k.scale >= 0.f) || !std::isfinite(k.scale)) return fail(nullptr, INFS_E_ARG, "scale must be finite and >= 0");
-  if (k.flags & ~INFS_FLAG_DRY_RUN) return fail(nullptr, INFS_E_ARG, "unknown flags");
+  if (k.flags & ~(INFS_FLAG_DRY_RUN | INFS_FLAG_KV_FP8)) return fail(nullptr, INFS_E_ARG, "unknown flags");
+  const int kv8 = (k.flags & INFS_FLAG_KV_FP8) ? 1 : 0;
   if (k.probe_tokens < 0 || k.probe_tokens > k.max_suffix_len)
     return fail(nullptr, INFS_E_ARG, "probe_tokens must be in [0, max_suffix_len]");
 
   const int hpk = k.num_q_heads / k.num_kv_heads;
   KernelKey key{};
-  if (!infs::select_kernel(k.dtype == INFS_BF16, k.head_dim, hpk, k.slots_per_prompt * hpk, &key))
+  if (kv8 && (k.dtype != INFS_BF16 || k.head_dim != 128 || k.slots_per_prompt * hpk < 16))
+    return fail(nullptr, INFS_E_ARG,
+                "INFS_FLAG_KV_FP8 needs bf16, head_dim 128 and at least 16 prefix rows (slots_per_prompt * heads_per_kv)");
+  if (!infs::select_kernel(k.dtype == INFS_BF16, k.head_dim, hpk, k.slots_per_prompt * hpk, kv8, &key))
     return fail(nullptr, INFS_E_ARG,
                 "no kernel for dtype=%s head_dim=%d heads_per_kv=%d prefix rows=%d (bf16 supports up to 128 rows, "
                 "fp32 up to 16)",
@@ -462,7 +468,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     const int max_rows = key.mfma ? 128 : 16;
     probe_batch = std::min({infs::kMaxSlots, max_rows / hpk, k.samples_per_prompt});
     if (probe_batch < 1 ||
-        !infs::select_kernel_path(k.dtype == INFS_BF16, k.head_dim, hpk, probe_batch * hpk, key.mfma, &pkey))
+        !infs::select_kernel_path(k.dtype == INFS_BF16, k.head_dim, hpk, probe_batch * hpk, key.mfma, kv8, &pkey))
       return fail(nullptr, INFS_E_ARG, "no probe kernel for heads_per_kv=%d", hpk);
   }
   {
@@ -501,7 +507,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->Hq = k.num_q_heads;
   c->L = k.num_layers;
   c->es = k.dtype == INFS_BF16 ? 2 : 4;
-  c->kv_es = c->es;
+  c->kv_es = key.kv8 ? 1 : c->es;
   c->split = k.split_tokens ? k.split_tokens : 256;
   c->pmax_pad = std::max(32, (k.max_prompt_len + 31) / 32 * 32);
   c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);

@@ -115,8 +115,9 @@ class _PrefixCache:
         return self._wl.query(layer, p, i, t)
 
 
-def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None):
-    """Max abs error over every captured live (step, slot, layer) output; idle rows must be 0."""
+def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None, kv_fp8=False):
+    """Max abs error over every captured live (step, slot, layer) output; idle rows must be 0.
+    kv_fp8: the oracle rounds keys and values to E4M3 as the FP8 cache stores them."""
     tol = tol if tol is not None else (1e-2 if cfg.dtype == "bf16" else 1e-5)
     layers = range(cfg.layers) if layers is None else layers
     wl = _PrefixCache(wl)
@@ -129,7 +130,7 @@ def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None):
                 continue
             p, i, t = e
             for layer in layers:
-                ref = attend_slot(wl, layer, p, i, t)
+                ref = attend_slot(wl, layer, p, i, t, kv_fp8=kv_fp8)
                 err = float(np.abs(o[layer, s].astype(np.float64) - ref).max())
                 assert np.isfinite(o[layer, s]).all()
                 if err > worst:

@@ -343,3 +343,17 @@ def test_probe_state_machine_errors():
     assert plain.probe_batch == 0
     assert _code(plain.probe_step, 0, 0, 0, 1, None, *nothing) == infs.E_STATE
     assert _code(plain.release_sample, 0, 0) == infs.E_STATE
+
+
+
+def test_fp8_kv_validation():
+    # The FP8 cache needs bf16, head_dim 128 and the MFMA prefix path.
+    for name, over in (("tiny_f32", {}),                                           # fp32
+                       ("qwen3_1p7b_l1_g32", {"slots_per_prompt": 1}),            # 2 prefix rows
+                       ("qwen3_1p7b_l1_g32", {"head_dim": 64})):                   # head_dim 64
+        cfg = get_config(name).with_(**over)
+        with pytest.raises(infs.InfsError) as ei:
+            context_for(cfg, dry_run=True, kv_fp8=True)
+        assert ei.value.status == infs.E_ARG
+    ctx = context_for(get_config("qwen3_1p7b_g64"), dry_run=True, kv_fp8=True)
+    ctx.destroy()

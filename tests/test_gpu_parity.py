@@ -15,16 +15,16 @@ from workload import Workload, get_config
 pytestmark = pytest.mark.gpu
 
 
-def _run_and_check(cfg, policy, capture=None, layers=None, split=0, window=1024):
+def _run_and_check(cfg, policy, capture=None, layers=None, split=0, window=1024, kv_fp8=False):
     wl = Workload(cfg)
     want_log = oracle_log(cfg, wl, policy)
     cap = capture(want_log).__contains__ if capture else (lambda k: True)
     wl, log, steps, captured, tokens, stats = run_gpu_group(cfg, policy, capture=cap, split=split,
-                                                          window=window, wl=wl)
+                                                          window=window, wl=wl, kv_fp8=kv_fp8)
     assert log == want_log, "step log differs from the oracle simulator"
     assert steps == len(want_log)
     assert np.array_equal(tokens, wl.L), "device token counters differ from the drawn lengths"
-    worst, n = check_against_oracle(cfg, wl, log, captured, layers=layers)
+    worst, n = check_against_oracle(cfg, wl, log, captured, layers=layers, kv_fp8=kv_fp8)
     say(f"  [{cfg.name} {policy}] checked {n} (slot, layer) outputs over {len(captured)} steps, "
         f"max abs err {worst:.3g}")
     return wl, log, captured
@@ -190,3 +190,25 @@ def test_full_size_sampled(name, every, window):
     cfg = get_config(name)
     _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=every, edge=2, refills=8),
                    layers=(0, cfg.layers - 1), window=window)
+
+
+def test_fp8_kv_small_every_other_step():
+    # FP8 (E4M3) KV cache on the throughput workload's shape: the oracle rounds
+    # every key and value to E4M3; outputs within the bf16 bound.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(700,), samples_per_prompt=24,
+                                             length_dist=("lognormal", 4.0, 1.0, 1, 300), max_suffix_len=300,
+                                             pool_rows=None)
+    _run_and_check(cfg, "sjf", split=128, capture=lambda log: sample_steps(log, every=2), kv_fp8=True)
+
+
+def test_fp8_kv_hpk4_multi_prompt():
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(0, 130, 511), samples_per_prompt=20,
+                                                length_dist=("lognormal", 4.0, 1.0, 1, 260),
+                                                max_suffix_len=260, pool_rows=None)
+    _run_and_check(cfg, "fptas_sjf", split=128, capture=lambda log: sample_steps(log, every=3), kv_fp8=True)
+
+
+def test_fp8_kv_full_size_sampled():
+    cfg = get_config("qwen3_1p7b_g64")
+    _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=397, edge=2, refills=8),
+                   layers=(0, cfg.layers - 1), window=512, kv_fp8=True)

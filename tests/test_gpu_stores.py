@@ -60,3 +60,68 @@ def test_stores_round_trip(name, over):
     run_gpu_group(cfg, "fifo", capture=lambda k: False, wl=wl, inspect=inspect)
     say(f"  [{name}] {checked['prefix']} prefix and {checked['response']} response read-backs bit-exact")
     assert checked["prefix"] > 0 and checked["response"] > 0
+
+
+def test_fp8_quantization_of_every_bf16_value():
+    # The FP8 cache stores round-to-nearest-even E4M3 codes, saturating at
+    # +-448: prefill K and V with every finite bf16 bit pattern and compare the
+    # stored codes with the oracle's rounding, code by code.
+    import torch
+    from oracle import encode_e4m3, round_e4m3
+    from paper_2506_22950_amd.group import context_for
+    from workload import bf16_bits_to_f64
+
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    finite = ((bits >> 7) & 0xFF) != 0xFF
+    bits = bits[finite]
+    cfg = get_config("qwen3_1p7b_l1_g32").with_(prompt_lens=(64,), max_suffix_len=16)
+    row = cfg.num_kv_heads * cfg.head_dim
+    n = -(-len(bits) // row) * row
+    k = np.resize(bits, n)
+    v = np.resize(bits[::-1], n)
+    P = n // row
+    cfg = cfg.with_(prompt_lens=(P,))
+    ctx = context_for(cfg, stream=torch.cuda.current_stream(), kv_fp8=True)
+    kd = torch.from_numpy(k.view(np.int16).reshape(P, cfg.num_kv_heads, cfg.head_dim)).cuda()
+    vd = torch.from_numpy(v.view(np.int16).reshape(P, cfg.num_kv_heads, cfg.head_dim)).cuda()
+    ctx.prefill_shared(0, 0, P, kd, vd)
+    gk, gv = ctx.read_prefix(0, 0, P)
+    table = {}
+    for name, src, got in (("K", k, gk), ("V", v, gv)):
+        vals = bf16_bits_to_f64(src)
+        want = np.array([encode_e4m3(x) for x in round_e4m3(vals)], dtype=np.uint8)
+        bad = np.flatnonzero(got.reshape(-1) != want)
+        assert len(bad) == 0, (name, [(hex(int(src[i])), hex(int(got.reshape(-1)[i])), hex(int(want[i])))
+                                      for i in bad[:8]])
+        table[name] = len(src)
+    say(f"  E4M3 codes of {table['K']} + {table['V']} bf16 values bit-exact")
+    ctx.destroy()
+
+
+def test_fp8_append_codes():
+    # Pages written by the append hold the E4M3 codes of the new rows.
+    from oracle import encode_e4m3, round_e4m3
+    from workload import bf16_bits_to_f64
+    cfg = get_config("qwen3_1p7b_l1_g32").with_(samples_per_prompt=10, length_dist=("uniform", 1, 60),
+                                                max_suffix_len=60)
+    wl = Workload(cfg)
+    seen = [0]
+
+    def codes(kind, idx):
+        vals = bf16_bits_to_f64(wl.pool(kind)[np.asarray(idx, dtype=np.int64)])
+        return np.vectorize(encode_e4m3, otypes=[np.uint8])(round_e4m3(vals))
+
+    def inspect(ctx, step, log):
+        if step % 5 != 2:
+            return
+        for s, e in enumerate(log[step]):
+            if e is None or e[2] == wl.L[e[0], e[1]]:
+                continue
+            p, i, t = e
+            k, v = ctx.read_response(s, 0)
+            idx = wl.suffix_index(0, p, i, np.arange(t))
+            assert np.array_equal(k, codes("k", idx)) and np.array_equal(v, codes("v", idx)), (s, t)
+            seen[0] += 1
+
+    run_gpu_group(cfg, "fifo", capture=lambda j: False, wl=wl, inspect=inspect, kv_fp8=True)
+    assert seen[0] > 0
