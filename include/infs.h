@@ -15,8 +15,15 @@
  *     at once with a pending sample that starts at the next step
  *     (Section 3.2; Algorithm 1, phase 2)                  -> infs_retire_slot, infs_refill_slot
  *   - the refill order: naive micro groups (Section 3.1), fixed-slot rows
- *     (Section 3.2), FIFO, or shortest-job-first on predicted lengths
- *     (Algorithm 3)                                         -> infs_sched_*
+ *     (Section 3.2), FIFO, shortest-job-first on predicted lengths
+ *     (Algorithm 3), FPTAS grouping (Algorithm 2) alone or followed by SJF
+ *     (Algorithm 1), longest-first                          -> infs_sched_*, infs_fptas_assign
+ *   - prefix reuse: every sample first decodes k probe tokens, whose KV is
+ *     kept; a dispatched sample resumes at token k+1 (Section 4)
+ *                                                          -> infs_probe_step, infs_end_probe_step,
+ *                                                             infs_release_sample
+ *   - optionally an FP8 (E4M3) KV cache, in the direction of the KV-cache
+ *     compression the paper leaves as future work           -> INFS_FLAG_KV_FP8
  *
  * Attention computed by infs_decode_step, per live slot s holding sample i of
  * prompt p with t generated tokens (the token of this step included), per
@@ -33,12 +40,14 @@
  *     context unchanged.  A failed HIP call or kernel launch makes the
  *     context return INFS_E_DEVICE from then on.
  *   - Device work is enqueued on the HIP stream given to infs_create; no call
- *     synchronises except infs_sync, infs_sample_tokens and infs_timing_end.
+ *     synchronises except infs_sync, infs_sample_tokens, infs_timing_end,
+ *     infs_read_prefix, infs_read_response and infs_destroy.
  *   - "_dev" pointers are device (HBM) pointers owned by the caller; they
  *     must stay valid until the stream work that reads or writes them is
  *     done.  Host pointers are read or written before the call returns.
  *   - Element type of Q/K/V buffers is the context dtype (fp32, or bf16 as
- *     raw 16-bit patterns); O is always fp32.
+ *     raw 16-bit patterns); O is always fp32.  Buffers handed to kernels are
+ *     16-byte aligned.
  *   - A context must be used from one host thread at a time.
  */
 #ifndef INFS_H
@@ -57,7 +66,7 @@ typedef enum infs_status {
     INFS_E_ARG = -1,       /* invalid argument (shape, index, null pointer, unsupported shape) */
     INFS_E_STATE = -2,     /* call not allowed in the current slot / step state */
     INFS_E_CAPACITY = -3,  /* a response would exceed max_suffix_len, or the page pool is full */
-    INFS_E_DUP = -4,       /* the sample id was already dispatched in this group */
+    INFS_E_DUP = -4,       /* the sample id was already dispatched (or released) in this group */
     INFS_E_NOMEM = -5,     /* device allocation failed */
     INFS_E_DEVICE = -6     /* a HIP call failed; sticky for the context */
 } infs_status;
