@@ -249,6 +249,12 @@ infs_status infs_sample_tokens(infs_ctx* ctx, int32_t prompt, int32_t* counts_ho
    stage stopped waiting for its producers, which leaves that launch's outputs invalid (NaN). */
 infs_status infs_sync(infs_ctx* ctx);
 
+/* Bound on how many times a merge work-group polls for its producers before it gives up (default
+   2^20, far beyond any wait of a healthy launch; the work-group then writes NaN and the next
+   synchronising call returns E_DEVICE).  max_polls < 0: merges give up at once -- a way to exercise
+   that error path from the host.  E_STATE while a step is open. */
+infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
+
 infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
 
 /* Kernel timing.  Between begin and end every decode_step and probe_step launch records, on the

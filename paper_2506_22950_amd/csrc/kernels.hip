@@ -924,12 +924,15 @@ __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long*
     const int32_t* pc = prefix_counter(a, p, g);
     const int32_t* sc = suffix_counter(a, s, g);
     const int32_t pt = a.prompt[p].target, stg = a.slot[s].target;
-    int spins = 0;
-    while (!(reached(sc, stg) && reached(pc, pt)) && spins < kMergeSpins) {
-      __builtin_amdgcn_s_sleep(2);
-      ++spins;
+    bool ok = false;
+    if (a.merge_polls >= 0) {
+      ok = reached(sc, stg) && reached(pc, pt);
+      for (int spins = 0; !ok && spins < a.merge_polls; ++spins) {
+        __builtin_amdgcn_s_sleep(2);
+        ok = reached(sc, stg) && reached(pc, pt);
+      }
     }
-    *flag = spins < kMergeSpins;
+    *flag = ok;
   }
   __syncthreads();
   if (!*flag) {

@@ -81,6 +81,7 @@ struct StepArgs {
   int32_t count_tokens;       // 1 on layer 0
   float scale_log2;           // softmax scale * log2(e)
   uint32_t ws_o_bytes;        // size of ws_o (below 2^31)
+  int32_t merge_polls;        // bound on a merge block's polls of its counters (kMergeSpins; < 0: none)
   // this step
   int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;
   int32_t num_prompts;

@@ -547,6 +547,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   const float scale = k.scale > 0.f ? k.scale : 1.0f / std::sqrt((float)k.head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
   a.ws_o_bytes = (uint32_t)(c->ws_records * c->D * sizeof(float));
+  a.merge_polls = infs::kMergeSpins;
 
   if (!c->dry) {
     auto alloc = [&](void** p, size_t bytes, const char* what) -> infs_status {
@@ -811,6 +812,13 @@ infs_status infs_end_probe_step(infs_ctx* c) {
 }
 
 int32_t infs_probe_batch(const infs_ctx* c) { return c ? c->probe_batch : -1; }
+
+infs_status infs_set_merge_wait(infs_ctx* c, int32_t max_polls) {
+  CHECK_CTX(c);
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "set_merge_wait while a step is open");
+  c->plan.merge_polls = max_polls < 0 ? -1 : max_polls;
+  return INFS_OK;
+}
 
 infs_status infs_probe_state(const infs_ctx* c, int32_t prompt, int64_t sample_id, int32_t* probe_len) {
   if (!c) return fail(nullptr, INFS_E_ARG, "null context");

@@ -33,7 +33,7 @@ EXPORTS = (
     "infs_sample_tokens", "infs_sync", "infs_get_stats", "infs_timing_begin", "infs_timing_end",
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
-    "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response",
+    "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
 )
 
 
@@ -103,6 +103,7 @@ def load():
         "infs_release_sample": (I32, [P, I32, I64]),
         "infs_read_prefix": (I32, [P, I32, I32, P, P]),
         "infs_read_response": (I32, [P, I32, I32, P, P]),
+        "infs_set_merge_wait": (I32, [P, I32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -196,6 +197,9 @@ class Context:
 
     def sync(self):
         self._call(load().infs_sync)
+
+    def set_merge_wait(self, max_polls):
+        self._call(load().infs_set_merge_wait, max_polls)
 
     @property
     def probe_batch(self):

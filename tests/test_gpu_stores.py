@@ -125,3 +125,36 @@ def test_fp8_append_codes():
 
     run_gpu_group(cfg, "fifo", capture=lambda j: False, wl=wl, inspect=inspect, kv_fp8=True)
     assert seen[0] > 0
+
+
+def test_merge_timeout_is_reported():
+    # The merge's bounded wait: with the bound forced to "give up at once"
+    # from the host, every merge work-group writes NaN and returns (the
+    # producers still finish), the next synchronising call reports E_DEVICE
+    # and the context refuses further work.
+    import torch
+    from paper_2506_22950_amd import infs
+    from paper_2506_22950_amd.group import context_for
+    from workload.staging import DeviceInputs
+    cfg = get_config("tiny_f32")
+    wl = Workload(cfg)
+    dev = DeviceInputs(wl)
+    ctx = context_for(cfg, stream=torch.cuda.current_stream())
+    k, v = dev.prefix(0, 0)
+    ctx.prefill_shared(0, 0, cfg.prompt_lens[0], k, v)
+    ctx.refill_slot(0, 0, 0)
+    S = cfg.num_slots
+    q = torch.zeros((S, cfg.num_q_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
+    kn = torch.zeros((S, cfg.num_kv_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
+    o = torch.zeros((S, cfg.num_q_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
+    ctx.set_merge_wait(-1)
+    ctx.decode_step(0, q, kn, kn, o)
+    ctx.end_step()
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.sync()
+    assert ei.value.status == infs.E_DEVICE
+    assert torch.isnan(o[0]).all() and not o[1:].any()
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.retire_slot(0)
+    assert ei.value.status == infs.E_DEVICE
+    ctx.destroy()
