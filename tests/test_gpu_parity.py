@@ -58,6 +58,23 @@ def test_bf16_mfma32_small_every_step():
     _run_and_check(cfg, "sjf", split=128, capture=lambda log: sample_steps(log, every=2))
 
 
+@pytest.mark.parametrize("split", [512, 4096])
+def test_bf16_long_split_chunks(split):
+    # Longer split-K response chunks (the limit is 4096 tokens): responses span
+    # up to three chunks with ragged tails, prompt 1000 (ragged MFMA block).
+    top = 2 * split + 300
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=1, prompt_lens=(1000,), samples_per_prompt=20,
+                                             length_dist=("uniform", 1, top), max_suffix_len=top, pool_rows=None)
+    _run_and_check(cfg, "sjf", split=split,
+                   capture=lambda log: sample_steps(log, every=max(1, len(log) // 60), refills=20))
+
+
+def test_f32_wave_split_1024():
+    # fp32 wavefront path with 1024-token response chunks: responses up to 2500.
+    cfg = get_config("tiny_f32").with_(prompt_lens=(200,), length_dist=("uniform", 1, 2500), max_suffix_len=2500)
+    _run_and_check(cfg, "fifo", split=1024, capture=lambda log: sample_steps(log, every=40, refills=8))
+
+
 def test_bf16_mfma64_and_hpk4_multi_prompt():
     # Qwen3-8B shape (32Q/8KV: 4 query heads per KV head, 64 prefix rows), three
     # prompts of different lengths including an empty prefix.
