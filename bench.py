@@ -26,6 +26,11 @@ if ROOT not in sys.path:
 PEAK_HBM_GBS = 8000.0
 COPY_CAL_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_traffic_{workload}.txt")
+MFMA_FILE = os.path.join(ROOT, "profiles", "decode_kernel_mfma_{workload}.txt")
+PEAK_MFMA_BF16_TFLOPS = 2500.0
+SIMDS = 1024  # 256 compute units x 4 SIMDs
+XCDS = 8
+MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE")
 KERNEL_SOURCES = ("paper_2506_22950_amd/csrc/kernels.hip", "paper_2506_22950_amd/csrc/kernels.h",
                   "paper_2506_22950_amd/csrc/plan.h")
 METRIC = "generated tokens/sec per group decode + achieved HBM TB/s vs peak, 1 MI355X"
@@ -45,10 +50,9 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def read_traffic(workload):
-    """HBM bytes per decode launch from the committed counter summary of this
-    workload, or None when there is none or the kernel source has changed since."""
-    path = TRAFFIC_FILE.format(workload=workload)
+def _read_summary(path):
+    """key = value lines of a committed counter summary, or None when there is
+    none or the kernel source has changed since it was taken."""
     if not os.path.exists(path):
         return None
     kv = {}
@@ -59,7 +63,33 @@ def read_traffic(workload):
                 kv[k.strip()] = v.strip()
     if kv.get("kernel_source_sha256") != kernel_source_hash():
         return None
-    return float(kv["traffic_bytes_per_launch"])
+    return kv
+
+
+def read_traffic(workload):
+    """HBM bytes per decode launch from the committed counter summary of this
+    workload, or None when there is none or the kernel source has changed since."""
+    kv = _read_summary(TRAFFIC_FILE.format(workload=workload))
+    return None if kv is None else float(kv["traffic_bytes_per_launch"])
+
+
+def read_mfma(workload):
+    """MFMA counter summary of this workload's decode launches (or None)."""
+    return _read_summary(MFMA_FILE.format(workload=workload))
+
+
+def mfma_flops(cfg, steplog):
+    """MFMA flops of all decode launches of a step log: per prompt with a live
+    slot, the prefix contractions S^T = K Q^T and O^T = V^T P^T over the padded
+    row tile (m * hpk rows padded to 16/32/64) and 32-token blocks, 2 flops per
+    multiply-add, every KV head, every layer."""
+    rows = cfg.slots_per_prompt * cfg.hpk
+    pad = 16 if rows <= 16 else 32 if rows <= 32 else 64 if rows <= 64 else 128
+    per_prompt = [4 * pad * (-(-plen // 32) * 32) * cfg.head_dim * cfg.num_kv_heads for plen in cfg.prompt_lens]
+    total = 0
+    for row in steplog:
+        total += sum(per_prompt[p] for p in {e[0] for e in row if e is not None})
+    return total * cfg.layers
 
 
 def copy_calibration(torch):
@@ -136,6 +166,49 @@ def summarize_pmc(workload, fetch_dir, write_dir):
         f"traffic_bytes_per_launch = {fetch_b + write_b:.0f}",
         f"alg_bytes_per_launch = {alg:.0f}",
         f"traffic_over_alg = {(fetch_b + write_b) / alg:.3f}",
+    ]
+    return "\n".join(lines)
+
+
+def summarize_mfma(workload, pmc_dir):
+    """Text summary of one rocprofv3 --pmc run of MFMA_COUNTERS over
+    `bench.py --steps 1 --warmup 1 --no-kernel-timing --no-cpu-baseline`:
+    MFMA work and MFMA busy cycles of decode_kernel per launch.  Counter values
+    are summed over their hardware instances (shader engines, XCDs)."""
+    from paper_2506_22950_amd.group import plan_steps
+    from workload import Workload, get_config
+
+    per = {}
+    for counter in MFMA_COUNTERS:
+        vals = [float(r["Counter_Value"]) for r in _pmc_rows(pmc_dir, counter) if "decode_kernel" in r["Kernel_Name"]]
+        if not vals:
+            raise SystemExit(f"{counter}: no decode_kernel rows under {pmc_dir}")
+        per[counter] = (len(vals), sum(vals) / len(vals))
+    cfg = get_config(workload)
+    wl = Workload(cfg)
+    steplog = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
+    launches = len(steplog) * cfg.layers
+    counts = {n for n, _ in per.values()}
+    if len(counts) != 1 or next(iter(counts)) % launches:
+        raise SystemExit(f"expected whole group decodes of {launches} launches per counter, got {sorted(counts)}")
+    decodes = next(iter(counts)) // launches
+    mops = per["SQ_INSTS_VALU_MFMA_MOPS_BF16"][1]
+    busy = per["SQ_VALU_MFMA_BUSY_CYCLES"][1]
+    cu_busy_quads = per["SQ_BUSY_CU_CYCLES"][1]
+    gui = per["GRBM_GUI_ACTIVE"][1] / XCDS
+    expect = mfma_flops(cfg, steplog) / launches
+    lines = [
+        f"kernel_source_sha256 = {kernel_source_hash()}",
+        f"workload = {workload}",
+        f"decode_launches = {launches} per group decode, {decodes} group decodes profiled",
+        f"mfma_mops_bf16_per_launch = {mops:.1f}",
+        f"mfma_flops_per_launch = {mops * 512:.0f}",
+        f"expected_mfma_flops_per_launch = {expect:.0f}",
+        f"mfma_busy_cycles_per_launch = {busy:.1f}",
+        f"cu_busy_cycles_per_launch = {cu_busy_quads * 4:.1f}",
+        f"gpu_active_cycles_per_launch = {gui:.1f}",
+        f"mfma_busy_over_active_simd_cycles = {busy / (gui * SIMDS):.5f}",
+        f"mfma_busy_over_busy_cu_simd_cycles = {busy / (cu_busy_quads * 4 * 4):.5f}",
     ]
     return "\n".join(lines)
 
@@ -382,11 +455,16 @@ def main():
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the traffic summary of two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--summarize-mfma", metavar="PMC_DIR",
+                    help="print the MFMA summary of a rocprofv3 --pmc output folder and exit")
     ap.add_argument("--schedules", action="store_true",
                     help="print the running steps of the refill policies (host only, no GPU) and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
         print(summarize_pmc(args.workload, *args.summarize_pmc))
+        return
+    if args.summarize_mfma:
+        print(summarize_mfma(args.workload, args.summarize_mfma))
         return
     if args.schedules:
         print(schedule_table())
@@ -442,6 +520,14 @@ def main():
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}
+        mf = read_mfma(args.workload) if not (args.reuse or args.kv_fp8 or args.split) else None
+        if mf is not None:
+            fl = float(mf["mfma_flops_per_launch"])
+            roof["mfma"] = {"kernel": "decode_kernel (prefix contractions)", "flops_per_launch": round(fl),
+                            "tflops": round(fl / (avg_us * 1e-6) / 1e12, 2), "peak_tflops": PEAK_MFMA_BF16_TFLOPS,
+                            "frac": round(fl / (avg_us * 1e-6) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 5),
+                            "busy_over_active": float(mf["mfma_busy_over_active_simd_cycles"]),
+                            "source": os.path.relpath(MFMA_FILE.format(workload=args.workload), ROOT)}
         log(f"kernel: {n} launches, {avg_us:.2f} us per launch by HIP events, {per_launch / 1e6:.2f} MB/launch -> "
             f"{achieved:.0f} GB/s; kernel body {body_us:.2f} us (device clock)")
         if ptiming is not None:
