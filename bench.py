@@ -27,6 +27,7 @@ PEAK_HBM_GBS = 8000.0
 COPY_CAL_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_traffic_{workload}.txt")
 MFMA_FILE = os.path.join(ROOT, "profiles", "decode_kernel_mfma_{workload}.txt")
+CALIB_LIB = os.path.join(ROOT, "paper_2506_22950_amd", "libinfs_calib.so")
 PEAK_MFMA_BF16_TFLOPS = 2500.0
 SIMDS = 1024  # 256 compute units x 4 SIMDs
 XCDS = 8
@@ -90,6 +91,49 @@ def mfma_flops(cfg, steplog):
     for row in steplog:
         total += sum(per_prompt[p] for p in {e[0] for e in row if e is not None})
     return total * cfg.layers
+
+
+def read_ceiling(torch, stream, nbytes, launches=200, pool_bytes=2 << 30):
+    """The one-launch read-bandwidth reference: a plain streaming-read kernel
+    (libinfs_calib.so) over `nbytes` (rounded down to a multiple of 16 KiB),
+    launched back to back over distinct buffers of a 2 GiB pool (so no launch
+    finds its bytes in the 256 MB last-level cache), timed like the decode
+    launches: HIP events on `stream` around all launches, divided by their
+    number.  Best of 256, 512 and 1024 work-groups.
+    Returns (bytes, us per launch, work-groups)."""
+    import ctypes
+
+    if not os.path.exists(CALIB_LIB):
+        raise RuntimeError(f"{CALIB_LIB} is missing: build it with `python -m paper_2506_22950_amd.build`")
+    fn = ctypes.CDLL(CALIB_LIB).infs_calib_stream_read
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    nb = nbytes // (16 << 10) * (16 << 10)
+    nbuf = pool_bytes // nb
+    pool = torch.empty(nbuf * nb, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1024, dtype=torch.int32, device="cuda")
+    with torch.cuda.stream(stream):
+        pool.fill_(1)
+    best = None
+    for blocks in (256, 512, 1024):
+        def launch(i):
+            rc = fn(pool.data_ptr() + (i % nbuf) * nb, nb, blocks, stream.cuda_stream, sink.data_ptr())
+            if rc != 0:
+                raise RuntimeError(f"infs_calib_stream_read failed: hipError {rc}")
+
+        for i in range(5):
+            launch(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(launches):
+            launch(i)
+        e1.record(stream)
+        e1.synchronize()
+        us = e0.elapsed_time(e1) * 1000.0 / launches
+        if best is None or us < best[1]:
+            best = (nb, us, blocks)
+    del pool
+    return best
 
 
 def copy_calibration(torch):
@@ -516,7 +560,8 @@ def main():
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
                 "alg_bytes_per_launch": round(per_launch),
-                "timing": "HIP events on the kernels' stream around every decode launch of one group decode",
+                "timing": "HIP events on the kernels' stream around all decode launches of one group decode, "
+                          "divided by their number",
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}
@@ -528,6 +573,13 @@ def main():
                             "frac": round(fl / (avg_us * 1e-6) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 5),
                             "busy_over_active": float(mf["mfma_busy_over_active_simd_cycles"]),
                             "source": os.path.relpath(MFMA_FILE.format(workload=args.workload), ROOT)}
+        cb, cus, cblocks = read_ceiling(torch, b.stream, int(per_launch))
+        cgbs = cb / (cus * 1e-6) / 1e9
+        roof["read_ceiling"] = {"kernel": "plain streaming read, one launch (libinfs_calib.so)", "bytes": cb,
+                                "work_groups": cblocks, "avg_launch_us": round(cus, 3), "achieved": round(cgbs, 1),
+                                "frac": round(cgbs / PEAK_HBM_GBS, 4)}
+        roof["frac_of_read_ceiling"] = round(achieved / cgbs, 4)
+        log(f"read ceiling: {cb / 1e6:.2f} MB in {cus:.2f} us per launch ({cblocks} work-groups) -> {cgbs:.0f} GB/s")
         log(f"kernel: {n} launches, {avg_us:.2f} us per launch by HIP events, {per_launch / 1e6:.2f} MB/launch -> "
             f"{achieved:.0f} GB/s; kernel body {body_us:.2f} us (device clock)")
         if ptiming is not None:

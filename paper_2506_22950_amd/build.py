@@ -1,7 +1,9 @@
-"""Build libinfs.so (HIP kernels + host runtime + scheduler) for gfx950 with hipcc.
+"""Build libinfs.so (HIP kernels + host runtime + scheduler) for gfx950 with hipcc,
+and libinfs_calib.so (a streaming-read kernel that bench.py uses as the
+one-launch read-bandwidth reference; not part of the decode path).
 
 Usage: python -m paper_2506_22950_amd.build   (or call build()).
-The library is written next to this file so that it travels with the source tree.
+The libraries are written next to this file so that they travel with the source tree.
 """
 
 import os
@@ -15,9 +17,11 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libinfs.so")
+CALIB_LIB = os.path.join(HERE, "libinfs_calib.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
 SOURCES = ["kernels.hip", "runtime.cpp", "sched.cpp"]
+CALIB_SOURCES = ["calib.hip"]
 
 
 def _hipcc():
@@ -60,14 +64,15 @@ def build(verbose: bool = False) -> str:
             print("\n".join(msgs))
         return obj
 
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError("linking libinfs.so failed:\n" + r.stderr)
-    os.replace(tmp, LIB)
+    with ThreadPoolExecutor(max_workers=len(SOURCES) + len(CALIB_SOURCES)) as ex:
+        objs = list(ex.map(compile_one, SOURCES + CALIB_SOURCES))
+    for lib, part in ((LIB, objs[:len(SOURCES)]), (CALIB_LIB, objs[len(SOURCES):])):
+        tmp = lib + ".tmp"
+        cmd = [hipcc, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *part]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"linking {os.path.basename(lib)} failed:\n" + r.stderr)
+        os.replace(tmp, lib)
     return LIB
 
 

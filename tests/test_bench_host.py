@@ -72,3 +72,17 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_calibration_library_exports():
+    import ctypes
+
+    assert os.path.exists(bench.CALIB_LIB), "build the libraries first (python -m paper_2506_22950_amd.build)"
+    lib = ctypes.CDLL(bench.CALIB_LIB)
+    fn = lib.infs_calib_stream_read
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    # Argument errors are refused on the host, before any launch.
+    assert fn(None, 1 << 20, 256, None, None) != 0
+    assert fn(ctypes.c_void_p(256), 1000, 256, None, ctypes.c_void_p(256)) != 0
+    assert fn(ctypes.c_void_p(8), 1 << 20, 256, None, ctypes.c_void_p(256)) != 0
