@@ -257,6 +257,19 @@ infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
 
 infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
 
+/* The decode kernel instantiation a context runs, fixed by infs_create from the element type, head
+   size, heads per KV head and m * hpk prefix rows: bf16 (0: fp32 Q/K/V, 1: bf16), head_dim, hpk,
+   mfma (1: the prefix contractions run on 16x16x32 MFMA tiles, 0: on wavefront dot products),
+   prefix_rows (the row tile, padded: 8/16 on the wavefront path, 16/32/64/128 on MFMA tiles),
+   kv_fp8 (1: K/V stored as E4M3).  probe_* describe the kernel of infs_probe_step launches
+   (probe_prefix_rows = 0 without a probe phase).  For diagnostics and tests; dry-run contexts
+   answer too. */
+typedef struct infs_kernel_info {
+    int32_t bf16, head_dim, hpk, mfma, prefix_rows, kv_fp8;
+    int32_t probe_mfma, probe_prefix_rows;
+} infs_kernel_info;
+infs_status infs_get_kernel_info(const infs_ctx* ctx, infs_kernel_info* out);
+
 /* Kernel timing.  Between begin and end every decode_step and probe_step launch records, on the
    device wall clock, the start of its first work-group and the end of its last one.  infs_timing_end
    synchronises and returns the summed kernel time (ms) of the timed launches, their number, and

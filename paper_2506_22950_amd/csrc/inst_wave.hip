@@ -1,0 +1,48 @@
+// Decode kernel instantiations: fp32 Q/K/V, and bf16 with fewer than 16 prefix rows (wavefront reductions); head_dim 64 and 128, 1/2/4/8 query heads per KV head, 8 or 16 padded rows.
+#include "decode.h"
+
+namespace infs {
+namespace {
+
+#define INFS_ENTRY(bf, d, hpk, mf, pr) {{bf, d, hpk, mf, pr, 0}, decode_kernel<Shape<bf, d, hpk, mf, pr>>},
+
+const KernelEntry kEntries[] = {
+    INFS_ENTRY(false, 64, 1, false, 8)
+    INFS_ENTRY(false, 64, 1, false, 16)
+    INFS_ENTRY(false, 64, 2, false, 8)
+    INFS_ENTRY(false, 64, 2, false, 16)
+    INFS_ENTRY(false, 64, 4, false, 8)
+    INFS_ENTRY(false, 64, 4, false, 16)
+    INFS_ENTRY(false, 64, 8, false, 8)
+    INFS_ENTRY(false, 64, 8, false, 16)
+    INFS_ENTRY(false, 128, 1, false, 8)
+    INFS_ENTRY(false, 128, 1, false, 16)
+    INFS_ENTRY(false, 128, 2, false, 8)
+    INFS_ENTRY(false, 128, 2, false, 16)
+    INFS_ENTRY(false, 128, 4, false, 8)
+    INFS_ENTRY(false, 128, 4, false, 16)
+    INFS_ENTRY(false, 128, 8, false, 8)
+    INFS_ENTRY(false, 128, 8, false, 16)
+    INFS_ENTRY(true, 64, 1, false, 8)
+    INFS_ENTRY(true, 64, 1, false, 16)
+    INFS_ENTRY(true, 64, 2, false, 8)
+    INFS_ENTRY(true, 64, 2, false, 16)
+    INFS_ENTRY(true, 64, 4, false, 8)
+    INFS_ENTRY(true, 64, 4, false, 16)
+    INFS_ENTRY(true, 64, 8, false, 8)
+    INFS_ENTRY(true, 64, 8, false, 16)
+    INFS_ENTRY(true, 128, 1, false, 8)
+    INFS_ENTRY(true, 128, 1, false, 16)
+    INFS_ENTRY(true, 128, 2, false, 8)
+    INFS_ENTRY(true, 128, 2, false, 16)
+    INFS_ENTRY(true, 128, 4, false, 8)
+    INFS_ENTRY(true, 128, 4, false, 16)
+    INFS_ENTRY(true, 128, 8, false, 8)
+    INFS_ENTRY(true, 128, 8, false, 16)
+};
+
+}  // namespace
+
+KernelTable kernels_wave() { return {kEntries, (int)(sizeof(kEntries) / sizeof(kEntries[0]))}; }
+
+}  // namespace infs

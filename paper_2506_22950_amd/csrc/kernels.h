@@ -35,6 +35,23 @@ int64_t prefix_elems_per_head(const KernelKey& key, int max_prompt_len_padded);
 
 hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream);
 
+// The decode kernel instantiations, spread over several translation units
+// (inst_*.hip) so that they compile in parallel.
+struct KernelEntry {
+  KernelKey key;
+  void (*decode)(const StepArgs);
+};
+struct KernelTable {
+  const KernelEntry* entries;
+  int count;
+};
+KernelTable kernels_wave();        // fp32, and bf16 below 16 prefix rows (wavefront reductions)
+KernelTable kernels_mfma_d64();    // bf16, head_dim 64, MFMA prefix tiles
+KernelTable kernels_mfma_d128a();  // bf16, head_dim 128, hpk 1 and 2
+KernelTable kernels_mfma_d128b();  // bf16, head_dim 128, hpk 4 and 8
+KernelTable kernels_kv8a();        // E4M3 K/V, head_dim 128, hpk 1 and 2
+KernelTable kernels_kv8b();        // E4M3 K/V, head_dim 128, hpk 4 and 8
+
 // Copy one prompt's K/V [plen, Hkv, D] into the shared-prefix store (layout chosen by key).
 hipError_t launch_prefill(const KernelKey& key, void* prefix_layer, const void* k, const void* v,
                           int prompt, int plen, int hkv, int max_prompt_len_padded, hipStream_t stream);

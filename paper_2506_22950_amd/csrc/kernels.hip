@@ -1,1149 +1,22 @@
-// HIP kernels for gfx950 (CDNA4): shared-prefix continuous-sampling decode.
-//
-// One launch per layer-step does all the device work of that layer:
-//   * append: each live slot's new K/V row goes into its response pages;
-//   * split-K attention over the shared prefix: one work-group per
-//     (prompt, KV head, chunk of `split` prefix tokens).  Every K/V byte of the
-//     chunk is read from HBM once and used by all m * hpk query rows of that
-//     KV head -- the rows of every live slot of the prompt.  With >= 16 rows
-//     the two contractions run on MFMA tiles (v_mfma_f32_16x16x32_bf16);
-//     below that, on wavefront dot products;
-//   * split-K attention over each live slot's private response (hpk rows per
-//     KV byte, wavefront dot products);
-//   * log-sum-exp merge: one work-group per live (slot, KV head), placed at
-//     the end of the grid, waits (bounded) until every chunk of that slot has
-//     published its partial, combines the partial softmaxes and writes O.
-// Idle slots get O = 0.
-//
-// A partial over a key set J is (M, L, O) with scores in log2 units
-// (s_j = scale * log2(e) * q.k_j): M = max_j s_j, L = sum_j 2^(s_j - M),
-// O = sum_j 2^(s_j - M) v_j.  Two partials combine exactly as
-// M = max(M1, M2), L = 2^(M1-M) L1 + 2^(M2-M) L2, O likewise, and the result
-// is O / L.
-#include <hip/hip_runtime.h>
-#include <stdint.h>
-
-#include "kernels.h"
+// Host side of the decode kernels: the instantiation registry, kernel
+// selection, the launches, and the prefill kernels.  The device code (and what
+// the kernels compute) is in decode.h; the decode kernel instantiations are in
+// inst_*.hip.
+#include "decode.h"
 
 namespace infs {
 namespace {
 
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-
-#define NEG_INF (-__builtin_huge_valf())
-
-__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
-__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Lane permutations inside 16-lane DPP rows (row_mask = bank_mask = all).
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over each aligned group of N consecutive lanes; every lane gets its group's sum.
-template <int N>
-__device__ __forceinline__ float group_sum(float x) {
-  static_assert(N == 2 || N == 4 || N == 8 || N == 16 || N == 32 || N == 64, "group size");
-  x += dpp<0xB1>(x);                       // quad_perm [1,0,3,2]: lane ^ 1
-  if constexpr (N >= 4) x += dpp<0x4E>(x); // quad_perm [2,3,0,1]: lane ^ 2
-  if constexpr (N == 8) x += dpp<0x141>(x);  // row_half_mirror: quad 0 <-> quad 1
-  if constexpr (N >= 16) {
-    x += dpp<0x124>(x);                    // row_ror:4
-    x += dpp<0x128>(x);                    // row_ror:8
-  }
-  if constexpr (N >= 32) x += __shfl_xor(x, 16);
-  if constexpr (N >= 64) x += __shfl_xor(x, 32);
-  return x;
-}
-
-// Combine partial (m2, l2) into (m, l); returns the weights of the old and new parts.
-__device__ __forceinline__ void lse_combine(float& m, float& l, float m2, float l2, float& a, float& b) {
-  const float mn = fmaxf(m, m2);
-  const float mu = (mn == NEG_INF) ? 0.f : mn;
-  a = exp2_fast(m - mu);
-  b = exp2_fast(m2 - mu);
-  l = l * a + l2 * b;
-  m = mn;
-}
-
-// 16-byte chunk helpers: 8 bf16 or 4 fp32 elements.
-template <bool BF>
-__device__ __forceinline__ float dot16B(const u32x4& k, const u32x4& q) {
-  if constexpr (BF) {
-    // Pairs are taken with shufflevector from a whole-vector cast: casting the
-    // individual 32-bit lanes to bf16x2 is mis-lowered by this compiler (all
-    // four dots read the same dword).
-    const bf16x8 kv = __builtin_bit_cast(bf16x8, k), qv = __builtin_bit_cast(bf16x8, q);
-    float s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 0, 1), __builtin_shufflevector(qv, qv, 0, 1), 0.f, false);
-    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 2, 3), __builtin_shufflevector(qv, qv, 2, 3), s, false);
-    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 4, 5), __builtin_shufflevector(qv, qv, 4, 5), s, false);
-    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(kv, kv, 6, 7), __builtin_shufflevector(qv, qv, 6, 7), s, false);
-    return s;
-  } else {
-    float s = __uint_as_float(k.x) * __uint_as_float(q.x);
-    s = fmaf(__uint_as_float(k.y), __uint_as_float(q.y), s);
-    s = fmaf(__uint_as_float(k.z), __uint_as_float(q.z), s);
-    s = fmaf(__uint_as_float(k.w), __uint_as_float(q.w), s);
-    return s;
-  }
-}
-
-template <bool BF>
-__device__ __forceinline__ void axpy16B(float* o, float p, const u32x4& v) {
-  if constexpr (BF) {
-    o[0] = fmaf(p, bf_lo(v.x), o[0]); o[1] = fmaf(p, bf_hi(v.x), o[1]);
-    o[2] = fmaf(p, bf_lo(v.y), o[2]); o[3] = fmaf(p, bf_hi(v.y), o[3]);
-    o[4] = fmaf(p, bf_lo(v.z), o[4]); o[5] = fmaf(p, bf_hi(v.z), o[5]);
-    o[6] = fmaf(p, bf_lo(v.w), o[6]); o[7] = fmaf(p, bf_hi(v.w), o[7]);
-  } else {
-    o[0] = fmaf(p, __uint_as_float(v.x), o[0]); o[1] = fmaf(p, __uint_as_float(v.y), o[1]);
-    o[2] = fmaf(p, __uint_as_float(v.z), o[2]); o[3] = fmaf(p, __uint_as_float(v.w), o[3]);
-  }
-}
-
-// Compile-time shape of one kernel instantiation.
-template <bool BF_, int D_, int HPK_, bool MFMA_, int PR_, bool KV8_ = false>
-struct Shape {
-  static constexpr bool BF = BF_;
-  // KV8: the prefix store and the pages hold K/V as E4M3 bytes; the kernels
-  // widen them to bf16 in registers (exact) and compute as for bf16.
-  static constexpr bool KV8 = KV8_;
-  static constexpr int D = D_;
-  static constexpr int HPK = HPK_;
-  static constexpr bool MFMA = MFMA_;
-  static constexpr int PR = PR_;                  // prefix rows per record group (padded)
-  static constexpr int ES = BF ? 2 : 4;            // element bytes
-  static constexpr int EPL = 16 / ES;              // elements per lane chunk
-  static constexpr int ROWB = D * ES;              // bytes of one K or V row of one head
-  static constexpr int LPT = ROWB / 16;            // lanes per token (wavefront path)
-  static constexpr int TPI = 64 / LPT;             // tokens per load instruction
-  static constexpr int KES = KV8 ? 1 : ES;        // bytes per stored K/V element
-  static constexpr int KROWB = D * KES;            // bytes of one stored K or V row of one head
-  static constexpr int LANEB = EPL * KES;          // stored bytes behind one lane's EPL elements
-  static constexpr int PAGEB = kPageTokens * KROWB; // bytes of one page of one head, K or V
-  static constexpr int NB = PR / 16;               // MFMA row blocks
-  static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
-  static constexpr int DB = D / 16;                // MFMA 16-wide head_dim blocks
-  // More than 64 MFMA rows: each wavefront owns a quarter of the rows and
-  // walks the whole chunk, so the four need no combine.
-  static constexpr bool ROWSPLIT = MFMA && PR > 64;
-  static constexpr int WAVE_NR = (!MFMA && PR > HPK) ? PR : HPK;
-  static constexpr int WAVE_SMEM = 4 * WAVE_NR * (D + 2);
-  static constexpr int MFMA_SLOT = (MFMA && !ROWSPLIT) ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
-  static constexpr int MFMA_SMEM = 4 * MFMA_SLOT;
-  static constexpr int SMEM = WAVE_SMEM > MFMA_SMEM ? WAVE_SMEM : MFMA_SMEM;
-  // 64 MFMA rows keep 128 accumulator registers live, and 16 wavefront rows
-  // as many: those shapes run 1 wavefront per SIMD rather than spill; every
-  // other shape runs 2 per SIMD.
-  static constexpr int MIN_WAVES = ROWSPLIT ? 2 : ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
-  static_assert(LPT >= 2 && LPT <= 64, "row size");
-  static_assert(!MFMA || BF, "MFMA path is bf16");
-  static_assert(!KV8 || (BF && MFMA), "FP8 KV on the bf16 MFMA shapes");
-  static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
-};
-
-// ----------------------------------------------------------------------------
-// Partials are exchanged between work-groups through agent-scope atomic
-// stores and loads (coherent across the XCDs' L2 caches), ordered by waiting
-// for the stores to complete before the arrival counter is bumped.  This
-// avoids the whole-cache write-back and invalidate of an agent-scope fence.
-// ----------------------------------------------------------------------------
-__device__ __forceinline__ void st_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// 16-byte store into the partial-output workspace with the cache policy of
-// the agent-scope atomic store above (write through to the coherence point),
-// so that a lane's four consecutive floats leave as one write instead of
-// four partial-line writes.  The workspace is addressed by a raw buffer
-// resource over its whole size; byte_off must be below ws_o_bytes.
-constexpr int kCoherentPolicy = 16;  // sc1
-constexpr int kRawBufferWord3 = 0x00020000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t ws_rsrc(const StepArgs& a) {
-  return __builtin_amdgcn_make_buffer_rsrc(a.ws_o, 0, (int)a.ws_o_bytes, kRawBufferWord3);
-}
-__device__ __forceinline__ void st_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kCoherentPolicy);
-}
-
-// E4M3 (OCP) <-> bf16.  Widening is exact: every E4M3 value is a bf16 value.
-// Narrowing rounds to nearest even; magnitudes beyond 448 are clamped first,
-// so the conversion saturates instead of producing NaN.
-__device__ __forceinline__ u32x4 widen_e4m3(uint2 w) {
-  u32x4 r;
-  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, false));
-  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.x, 1.0f, true));
-  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, false));
-  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w.y, 1.0f, true));
-  return r;
-}
-__device__ __forceinline__ float sat_e4m3(float x) { return fminf(fmaxf(x, -448.f), 448.f); }
-__device__ __forceinline__ uint32_t narrow4_e4m3(uint32_t lo, uint32_t hi) {  // 4 bf16 -> 4 E4M3 bytes
-  int w = __builtin_amdgcn_cvt_pk_fp8_f32(sat_e4m3(__uint_as_float(lo << 16)), sat_e4m3(__uint_as_float(lo & 0xffff0000u)),
-                                          0, false);
-  w = __builtin_amdgcn_cvt_pk_fp8_f32(sat_e4m3(__uint_as_float(hi << 16)), sat_e4m3(__uint_as_float(hi & 0xffff0000u)),
-                                      w, true);
-  return (uint32_t)w;
-}
-__device__ __forceinline__ uint2 narrow_e4m3(const u32x4& v) {  // 8 bf16 -> 8 E4M3 bytes
-  return uint2{narrow4_e4m3(v.x, v.y), narrow4_e4m3(v.z, v.w)};
-}
-// One lane's EPL stored elements as a 16-byte register of the compute type.
-template <class SH>
-__device__ __forceinline__ u32x4 ld_kv(const char* p) {
-  if constexpr (SH::KV8)
-    return widen_e4m3(*(const uint2*)p);
-  else
-    return *(const u32x4*)p;
-}
-// Store one lane's EPL elements (given in the compute type) into a stored row.
-template <class SH>
-__device__ __forceinline__ void st_kv(char* p, const u32x4& v) {
-  if constexpr (SH::KV8)
-    *(uint2*)p = narrow_e4m3(v);
-  else
-    *(u32x4*)p = v;
-}
-
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) x = fmaxf(x, __shfl_xor(x, s));
-  return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int s = 1; s < 64; s <<= 1) x += __shfl_xor(x, s);
-  return x;
-}
-
-// ----------------------------------------------------------------------------
-// Wavefront path: NR query rows over the token range [t0, t1) of one KV head.
-// LPT consecutive lanes hold one token's row (16 B each), so a load
-// instruction covers TPI tokens; U loads per lane for K and for V are issued
-// together before any arithmetic.  Each token group keeps its own running
-// (m, l, o); the groups are combined at the end.  t0 must be a multiple of 16
-// (page-aligned) so that every load instruction stays inside one page.
-// ----------------------------------------------------------------------------
-template <class SH, int NR>
-struct WaveCfg {
-  // Loads per lane per iteration, sized so that K/V buffers, scores and
-  // accumulators of NR rows stay within the two-wavefronts-per-SIMD budget.
-  static constexpr int UMAX = NR <= 2 ? 16 : NR <= 4 ? 8 : 4;
-  static constexpr int U = (64 / SH::TPI) < UMAX ? (64 / SH::TPI) : UMAX;
-  static_assert(16 % SH::TPI == 0, "a load instruction must not straddle a page");
-};
-
-template <class SH, int NR, class Addr>
-__device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, const u32x4 (&q)[NR], float sl2,
-                                             float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
-  constexpr int LPT = SH::LPT, TPI = SH::TPI, EPL = SH::EPL, U = WaveCfg<SH, NR>::U;
-  // Loads are issued in sub-blocks of SB per lane (K, then V) and the online
-  // softmax runs per sub-block, so the arithmetic on early sub-blocks overlaps
-  // the arrival of later ones.  Every load is unconditional: tokens past t1
-  // read a valid row (Addr keeps addresses in bounds) and are masked to -inf.
-  constexpr int SB = U >= 8 ? 4 : U;
-  constexpr int NSB = U / SB;
-  static_assert(U % SB == 0 && SB % 2 == 0, "sub-blocks of token pairs");
-  const int lane = threadIdx.x & 63, ts = lane / LPT;
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    m[r] = NEG_INF;
-    l[r] = 0.f;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) o[r][e] = 0.f;
-  }
-  constexpr int PGI = (U * TPI + 15) / 16;  // 16-token pages touched per iteration
-  for (int base = t0; base < t1; base += U * TPI) {
-    // Page numbers first, in straight-line code: the compiler then waits for
-    // the page-table load once instead of before every K/V load.
-    int pg[PGI];
-#pragma unroll
-    for (int i = 0; i < PGI; ++i) pg[i] = ad.page(((base - t0) >> 4) + i);
-    u32x4 kk[U], vv[U];
-#pragma unroll
-    for (int b = 0; b < NSB; ++b) {
-#pragma unroll
-      for (int kind = 0; kind < 2; ++kind)
-#pragma unroll
-        for (int u = b * SB; u < b * SB + SB; ++u) {
-          u32x4& dst = kind ? vv[u] : kk[u];
-          dst = ld_kv<SH>(ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1));
-        }
+const KernelEntry* find_entry(const KernelKey& k) {
+  static const KernelTable tables[] = {kernels_wave(),      kernels_mfma_d64(), kernels_mfma_d128a(),
+                                       kernels_mfma_d128b(), kernels_kv8a(),     kernels_kv8b()};
+  for (const KernelTable& t : tables)
+    for (int i = 0; i < t.count; ++i) {
+      const KernelEntry& e = t.entries[i];
+      if (e.key.bf16 == k.bf16 && e.key.head_dim == k.head_dim && e.key.hpk == k.hpk && e.key.mfma == k.mfma &&
+          e.key.prefix_rows == k.prefix_rows && e.key.kv8 == k.kv8)
+        return &e;
     }
-#pragma unroll
-    for (int b = 0; b < NSB; ++b) {
-      float s[SB][NR];
-#pragma unroll
-      for (int x = 0; x < SB; ++x) {
-        const int u = b * SB + x;
-        const bool ok = base + u * TPI + ts < t1;
-#pragma unroll
-        for (int r = 0; r < NR; ++r) {
-          const float y = group_sum<LPT>(dot16B<SH::BF>(kk[u], q[r])) * sl2;
-          s[x][r] = ok ? y : NEG_INF;
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < NR; ++r) {
-        float mb = s[0][r];
-#pragma unroll
-        for (int x = 1; x < SB; ++x) mb = fmaxf(mb, s[x][r]);
-        const float mn = fmaxf(m[r], mb);
-        const float mu = (mn == NEG_INF) ? 0.f : mn;
-        const float corr = exp2_fast(m[r] - mu);
-        m[r] = mn;
-        l[r] *= corr;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) o[r][e] *= corr;
-        if constexpr (SH::BF) {
-          // P.V two tokens at a time with bf16 dot products: the probabilities
-          // are rounded to bf16 and the normaliser sums the same rounded values.
-#pragma unroll
-          for (int x = 0; x < SB; x += 2) {
-            const int u = b * SB + x;
-            const __bf16 h0 = (__bf16)exp2_fast(s[x][r] - mu), h1 = (__bf16)exp2_fast(s[x + 1][r] - mu);
-            l[r] += (float)h0 + (float)h1;
-            const bf16x2 pb = {h0, h1};
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-              const uint32_t lo = __builtin_amdgcn_perm(vv[u + 1][k], vv[u][k], 0x05040100u);  // elems 2k
-              const uint32_t hi = __builtin_amdgcn_perm(vv[u + 1][k], vv[u][k], 0x07060302u);  // elems 2k+1
-              o[r][2 * k] = __builtin_amdgcn_fdot2_f32_bf16(pb, __builtin_bit_cast(bf16x2, lo), o[r][2 * k], false);
-              o[r][2 * k + 1] = __builtin_amdgcn_fdot2_f32_bf16(pb, __builtin_bit_cast(bf16x2, hi), o[r][2 * k + 1], false);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int x = 0; x < SB; ++x) {
-            const float p = exp2_fast(s[x][r] - mu);
-            l[r] += p;
-            axpy16B<false>(o[r], p, vv[b * SB + x]);
-          }
-        }
-      }
-    }
-  }
-}
-
-// Fold one token (K row chunk k, V row chunk v held by every token group) into
-// token group 0's running partial.  All lanes take part in the reduction.
-template <class SH, int NR>
-__device__ __forceinline__ void fold_token(const u32x4& k, const u32x4& v, const u32x4 (&q)[NR], float sl2,
-                                           float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
-  const bool mine = (threadIdx.x & 63) < SH::LPT;
-#pragma unroll
-  for (int r = 0; r < NR; ++r) {
-    const float x = group_sum<SH::LPT>(dot16B<SH::BF>(k, q[r])) * sl2;
-    if (mine) {
-      const float mn = fmaxf(m[r], x);
-      const float corr = exp2_fast(m[r] - mn);
-      const float p = exp2_fast(x - mn);
-      m[r] = mn;
-      l[r] = l[r] * corr + p;
-#pragma unroll
-      for (int e = 0; e < SH::EPL; ++e) o[r][e] *= corr;
-      axpy16B<SH::BF>(o[r], p, v);
-    }
-  }
-}
-
-// Combine the TPI token groups of a wavefront (lanes ch, ch+LPT, ...).
-template <class SH, int NR>
-__device__ __forceinline__ void wave_combine_groups(float (&m)[NR], float (&l)[NR], float (&o)[NR][SH::EPL]) {
-#pragma unroll
-  for (int mask = SH::LPT; mask < 64; mask <<= 1) {
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      const float m2 = __shfl_xor(m[r], mask);
-      const float l2 = __shfl_xor(l[r], mask);
-      float a, b;
-      lse_combine(m[r], l[r], m2, l2, a, b);
-#pragma unroll
-      for (int e = 0; e < SH::EPL; ++e) o[r][e] = o[r][e] * a + __shfl_xor(o[r][e], mask) * b;
-    }
-  }
-}
-
-// Combine the four wavefronts' partials through LDS and store the block's
-// partial rows [0, NR) at records rec0 + r.
-template <class SH, int NR>
-__device__ __forceinline__ void block_store_partial(float* smem, const float (&m)[NR], const float (&l)[NR],
-                                                    const float (&o)[NR][SH::EPL], float* ws_o, float* ws_ml,
-                                                    int64_t rec0) {
-  constexpr int D = SH::D, EPL = SH::EPL;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* so = smem;                   // [4][NR][D]
-  float* sml = smem + 4 * NR * D;     // [4][NR][2]
-  if (lane < SH::LPT) {
-#pragma unroll
-    for (int r = 0; r < NR; ++r)
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) so[(w * NR + r) * D + lane * EPL + e] = o[r][e];
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-      sml[(w * NR + r) * 2 + 0] = m[r];
-      sml[(w * NR + r) * 2 + 1] = l[r];
-    }
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < NR * D; idx += kBlockThreads) {
-    const int r = idx / D, d = idx - r * D;
-    float M = NEG_INF;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, sml[(v * NR + r) * 2]);
-    const float Mu = (M == NEG_INF) ? 0.f : M;
-    float L = 0.f, O = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const float wgt = exp2_fast(sml[(v * NR + r) * 2] - Mu);
-      L += wgt * sml[(v * NR + r) * 2 + 1];
-      O += wgt * so[(v * NR + r) * D + d];
-    }
-    st_coherent(ws_o + (rec0 + r) * D + d, O);
-    if (d == 0) {
-      st_coherent(ws_ml + (rec0 + r) * 2 + 0, M);
-      st_coherent(ws_ml + (rec0 + r) * 2 + 1, L);
-    }
-  }
-}
-
-// Addressing of the plain prefix store: [prompt][kv][K|V][max_prompt_len][D].
-// Row of token tokbase + (lane / LPT), clamped below `end` so that masked
-// tokens still read inside this head's region.
-template <class SH>
-struct PrefixAddr {
-  const char* base[2];
-  __device__ int page(int) const { return 0; }
-  __device__ const char* row(int kind, int tokbase, int, int, int end) const {
-    const int lane = threadIdx.x & 63;
-    const int tok = min(tokbase + lane / SH::LPT, end - 1);
-    return base[kind] + (int64_t)tok * SH::KROWB + (lane % SH::LPT) * SH::LANEB;
-  }
-};
-
-// Addressing of a slot's stored response tokens: pages [page][kv][K|V][16][D].
-// Lane i of `pages` holds the page of the wave's i-th 16-token group.  A load
-// instruction covers TPI consecutive tokens of one page, so its address is
-// (page base) + (token in page) * KROWB + lane * LANEB -- uniform plus lane offset.
-template <class SH>
-struct SuffixAddr {
-  const char* pool;
-  int pages;
-  int hkv, g;
-  __device__ int page(int pslot) const { return __builtin_amdgcn_readlane(pages, pslot); }
-  __device__ const char* row(int kind, int tokbase, int, int pg, int) const {
-    const int lane = threadIdx.x & 63;
-    return pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tokbase & 15) * SH::KROWB + lane * SH::LANEB;
-  }
-};
-
-__device__ __forceinline__ int64_t prefix_records(const StepArgs& a, int pr) {
-  return (int64_t)a.num_prompts * a.prefix_chunks_max * a.Hkv * pr;
-}
-
-// ----------------------------------------------------------------------------
-// Prefix chunk, wavefront path (fewer than 16 rows): rows r = slot_in_prompt * hpk + j.
-// ----------------------------------------------------------------------------
-template <class SH>
-__device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem) {
-  constexpr int PR = SH::PR, HPK = SH::HPK;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
-  const int plen = a.prompt[p].plen;
-  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
-  const int sub = a.prefix_split / 4;
-  const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
-  u32x4 q[PR];
-#pragma unroll
-  for (int r = 0; r < PR; ++r) {
-    const int si = r / HPK, j = r - si * HPK, s = p * a.m + min(si, a.m - 1);
-    if (r < a.prefix_rows && a.slot[s].len > 0)
-      q[r] = *((const u32x4*)((const char*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * SH::ROWB) + ch);
-    else
-      q[r] = u32x4{0, 0, 0, 0};
-  }
-  const int64_t head = ((int64_t)p * a.Hkv + g) * 2;
-  PrefixAddr<SH> ad{{(const char*)a.prefix + head * a.max_prompt_len * SH::KROWB,
-                     (const char*)a.prefix + (head + 1) * a.max_prompt_len * SH::KROWB}};
-  float m[PR], l[PR], o[PR][SH::EPL];
-  wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
-  wave_combine_groups<SH, PR>(m, l, o);
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * PR;
-  block_store_partial<SH, PR>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
-}
-
-// ----------------------------------------------------------------------------
-// Prefix chunk, MFMA path (R = NB*16 rows).  Per 32-token block:
-//   S^T[tok][row] = K[tok][:] . Q[row][:]     (A = K block, B = Q^T; 2 x NB tiles of 16x16)
-//   O^T[d][row]  += V^T[d][tok] P^T[tok][row] (A = V^T, B = P^T; NB x DB tiles)
-// With S^T, O^T and the running (m, l) all indexed by row = lane % 16, the
-// online-softmax rescale needs no cross-lane transpose.  The P^T operand takes
-// the 8 probabilities a lane already holds; the contraction index (token) is
-// the same permutation on both operands, and the prefix store keeps V in that
-// order (see prefill_mfma_kernel).  Each wavefront keeps one block in flight
-// (the accumulators of 32+ rows leave no registers for a second).
-// ----------------------------------------------------------------------------
-template <class SH>
-__device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const bf16x8 (&va)[SH::DB],
-                                           const bf16x8 (&bq)[SH::NB][SH::KB], int tb, int t1, float sl2,
-                                           f32x4 (&acc)[SH::NB][SH::DB], float (&mrow)[SH::NB],
-                                           float (&lrow)[SH::NB]) {
-  constexpr int NB = SH::NB, KB = SH::KB, DB = SH::DB;
-  const int lane = threadIdx.x & 63, q4 = lane >> 4;
-  f32x4 st[2][NB];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      f32x4 t = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb) t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[mb][kb], bq[nb][kb], t, 0, 0, 0);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int tok = tb + mb * 16 + q4 * 4 + e;
-        t[e] = (tok < t1) ? t[e] * sl2 : NEG_INF;
-      }
-      st[mb][nb] = t;
-    }
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    float mb_ = fmaxf(fmaxf(fmaxf(st[0][nb][0], st[0][nb][1]), fmaxf(st[0][nb][2], st[0][nb][3])),
-                      fmaxf(fmaxf(st[1][nb][0], st[1][nb][1]), fmaxf(st[1][nb][2], st[1][nb][3])));
-    mb_ = fmaxf(mb_, __shfl_xor(mb_, 16));
-    mb_ = fmaxf(mb_, __shfl_xor(mb_, 32));
-    const float mn = fmaxf(mrow[nb], mb_);
-    const float mu = (mn == NEG_INF) ? 0.f : mn;
-    const float corr = exp2_fast(mrow[nb] - mu);
-    mrow[nb] = mn;
-    lrow[nb] *= corr;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[nb][db] *= corr;
-    bf16x8 pb;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const __bf16 h = (__bf16)exp2_fast(st[mb][nb][e] - mu);
-        pb[mb * 4 + e] = h;
-        lrow[nb] += (float)h;
-      }
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[db], pb, acc[nb][db], 0, 0, 0);
-  }
-}
-
-// Combine the four wavefronts' MFMA partials of one chunk (same rows, disjoint
-// token ranges) and store rows 0 .. nrows-1 as records rec0 + row.  Every
-// wavefront publishes its fragments to LDS; after one barrier each combines
-// the four for a quarter of the head dimension and stores it.
-template <class XS>
-__device__ void mfma_combine_store(const StepArgs& a, float* smem, f32x4 (&acc)[XS::NB][XS::DB],
-                                   float (&mrow)[XS::NB], float (&lrow)[XS::NB], int64_t rec0, int nrows) {
-  constexpr int NB = XS::NB, DB = XS::DB, D = XS::D;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    lrow[nb] += __shfl_xor(lrow[nb], 16);
-    lrow[nb] += __shfl_xor(lrow[nb], 32);
-  }
-  constexpr int OFL = NB * DB * 64 * 4;
-  {
-    float* sl = smem + w * XS::MFMA_SLOT;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-      for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
-      sl[OFL + nb * 64 + lane] = mrow[nb];
-      sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
-    }
-  }
-  __syncthreads();
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
-  constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
-  static_assert(DB % 4 == 0, "head_dim blocks per wave");
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    if (nb * 16 + r16 >= nrows) continue;
-    float M = NEG_INF;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane]);
-    const float Mu = (M == NEG_INF) ? 0.f : M;
-    float wv[4], L = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      wv[v] = exp2_fast(smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane] - Mu);
-      L += wv[v] * smem[v * XS::MFMA_SLOT + OFL + NB * 64 + nb * 64 + lane];
-    }
-    const int64_t rec = rec0 + nb * 16 + r16;
-#pragma unroll
-    for (int x = 0; x < DBW; ++x) {
-      const int db = w * DBW + x;
-      f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * XS::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
-      st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
-    }
-    if (w == 0 && q4 == 0) {
-      st_coherent(a.ws_ml + rec * 2 + 0, M);
-      st_coherent(a.ws_ml + rec * 2 + 1, L);
-    }
-  }
-}
-
-template <class SH>
-__device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
-  constexpr int D = SH::D, NB = SH::NB, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
-  const int plen = a.prompt[p].plen;
-  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
-  const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
-  const int bpw = a.prefix_split / kMfmaBlock / 4;
-  const int b0 = w * bpw, b1 = min(b0 + bpw, nblk);
-  const float sl2 = a.scale_log2;
-
-  bf16x8 bq[NB][KB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int row = nb * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
-    const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
-    const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      if (ok)
-        bq[nb][kb] = *(const bf16x8*)(qr + kb * 32 + q4 * 8);
-      else
-        bq[nb][kb] = bf16x8{};
-    }
-  }
-
-  f32x4 acc[NB][DB];
-  float mrow[NB], lrow[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    mrow[nb] = NEG_INF;
-    lrow[nb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  const char* head = (const char*)a.prefix +
-                     ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
-  // One 32-token block (16 KB of K and V) in flight per wavefront: the
-  // register budget is kept at two wavefronts per SIMD, and the second
-  // wavefront hides this one's load latency.
-  for (int b = b0; b < b1; ++b) {
-    bf16x8 ka[2][KB], va[DB];
-    const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
-    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
-#pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
-    mfma_block<SH>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
-  }
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
-  mfma_combine_store<SH>(a, smem, acc, mrow, lrow, rec0, SH::PR);
-}
-
-// ----------------------------------------------------------------------------
-// Prefix chunk on MFMA tiles with more than 64 rows (e.g. the probe phase of
-// prefix reuse, where every sample of the group shares the prefix): wavefront
-// w owns row tiles w*NBW .. w*NBW+NBW-1 and walks every 32-token block of the
-// chunk (the other wavefronts' reads of the same blocks hit the cache), then
-// stores its rows' partial directly.
-// ----------------------------------------------------------------------------
-template <class SH>
-__device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
-  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
-  constexpr int NBW = SH::NB / kWaves;
-  static_assert(SH::NB % kWaves == 0, "row tiles per wavefront");
-  using WS = Shape<true, D, HPK, true, NBW * 16>;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
-  const int plen = a.prompt[p].plen;
-  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
-  const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
-  const float sl2 = a.scale_log2;
-
-  bf16x8 bq[NBW][KB];
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    const int row = (w * NBW + nb) * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
-    const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
-    const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) bq[nb][kb] = ok ? *(const bf16x8*)(qr + kb * 32 + q4 * 8) : bf16x8{};
-  }
-  f32x4 acc[NBW][DB];
-  float mrow[NBW], lrow[NBW];
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    mrow[nb] = NEG_INF;
-    lrow[nb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  const char* head = (const char*)a.prefix +
-                     ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
-  for (int b = 0; b < nblk; ++b) {
-    bf16x8 ka[2][KB], va[DB];
-    const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
-    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
-#pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
-    mfma_block<WS>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
-  }
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    lrow[nb] += __shfl_xor(lrow[nb], 16);
-    lrow[nb] += __shfl_xor(lrow[nb], 32);
-  }
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
-#pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    const int64_t rec = rec0 + (w * NBW + nb) * 16 + r16;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
-    if (q4 == 0) {
-      st_coherent(a.ws_ml + rec * 2 + 0, mrow[nb]);
-      st_coherent(a.ws_ml + rec * 2 + 1, lrow[nb]);
-    }
-  }
-}
-
-// ----------------------------------------------------------------------------
-// Response chunk of one live slot (hpk rows), plus the append of this step's
-// K/V when the chunk holds the newest position.
-// ----------------------------------------------------------------------------
-template <class SH>
-__device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem) {
-  constexpr int HPK = SH::HPK;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
-  const SlotPlan& sp = a.slot[s];
-  const int len = sp.len;
-  const int t0 = c * a.split, t1 = min(t0 + a.split, len);
-  const int sub = a.split / 4;
-  const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
-  // Page indices of this wavefront's range (lane i: the i-th 16-token group) and
-  // the query rows, loaded together.
-  const int npg = (wt1 - wt0 + kPageTokens - 1) / kPageTokens;
-  const int32_t* ptab = a.page_table + (int64_t)sp.seq * a.pages_per_slot + (wt0 >> 4);
-  const int pages = lane < npg ? ptab[lane] : 0;
-  u32x4 q[HPK];
-#pragma unroll
-  for (int r = 0; r < HPK; ++r)
-    q[r] = *((const u32x4*)((const char*)a.q + ((int64_t)s * a.Hq + g * HPK + r) * SH::ROWB) + ch);
-  // The newest token (position len-1) comes from the caller's rows: the wave
-  // whose range holds it loads it up front, folds it in after the stored
-  // tokens, and stores it into its page.
-  const int last = len - 1;
-  const bool has_new = last >= wt0 && last < wt1;
-  const int64_t newrow = ((int64_t)s * a.Hkv + g) * SH::ROWB;
-  u32x4 knew = u32x4{0, 0, 0, 0}, vnew = u32x4{0, 0, 0, 0};
-  if (has_new) {
-    knew = *((const u32x4*)((const char*)a.knew + newrow) + ch);
-    vnew = *((const u32x4*)((const char*)a.vnew + newrow) + ch);
-    if constexpr (SH::KV8) {  // attend to the token as the cache stores it
-      knew = widen_e4m3(narrow_e4m3(knew));
-      vnew = widen_e4m3(narrow_e4m3(vnew));
-    }
-  }
-  SuffixAddr<SH> ad{(const char*)a.pool, pages, a.Hkv, g};
-  float m[HPK], l[HPK], o[HPK][SH::EPL];
-  wave_partial<SH, HPK>(ad, wt0, has_new ? last : wt1, q, a.scale_log2, m, l, o);
-  if (has_new) {
-    fold_token<SH, HPK>(knew, vnew, q, a.scale_log2, m, l, o);
-    if (lane < SH::LPT) {
-      char* row = (char*)a.pool + (int64_t)(sp.cur_page * a.Hkv + g) * 2 * SH::PAGEB + (last & 15) * SH::KROWB +
-                  ch * SH::LANEB;
-      st_kv<SH>(row, knew);
-      st_kv<SH>(row + SH::PAGEB, vnew);
-    }
-  }
-  wave_combine_groups<SH, HPK>(m, l, o);
-  const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.suffix_chunks_max + c) * a.Hkv + g) * HPK;
-  block_store_partial<SH, HPK>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
-
-  if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
-    const int pos = len - 1;
-    a.page_table[(int64_t)sp.seq * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
-    if (a.count_tokens)
-      __hip_atomic_fetch_add(&a.tokens[(s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
-
-// ----------------------------------------------------------------------------
-// Merge all partials of (slot s, KV head g) and write O rows g*hpk .. +hpk-1
-// (the log-sum-exp combination of split-K partial softmaxes).  Partial c < nP
-// is prefix chunk c, then the response chunks.  The hpk*d outputs are cut into
-// 4-float vectors, one per lane (MV vectors per lane when they exceed 64); the
-// partials are dealt round-robin to the four wavefronts, each of which loads a
-// round of MCU partials at once (16-byte loads, no load waits on another) and
-// folds them into a running (max, sum, output); the four wavefronts' results
-// are then combined through LDS.
-// ----------------------------------------------------------------------------
-template <class SH>
-struct MergeShape {
-  static constexpr int OPP = SH::HPK * SH::D;          // outputs per partial
-  static constexpr int NVEC = OPP / 4;                 // 4-float vectors per partial
-  static constexpr int MV = (NVEC + 63) / 64;          // vectors per lane
-  static constexpr int MCU = MV == 1 ? 8 : 4;          // partials per load round and wavefront
-  static constexpr int SMEM = 4 * 64 * MV * 8;         // per wave and lane vector: max, sum, 2 pad, 4 outputs
-  static_assert(SH::D % 4 == 0, "vectors");
-};
-
-template <class SH>
-__device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
-  using MS = MergeShape<SH>;
-  constexpr int D = SH::D, HPK = SH::HPK, MV = MS::MV, MCU = MS::MCU;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int p = s / a.m, si = s - p * a.m;
-  const int nP = a.prompt[p].nchunks;
-  const int n = nP + (a.slot[s].len + a.split - 1) / a.split;
-  const int64_t pbase = ((int64_t)p * a.prefix_chunks_max * a.Hkv + g) * SH::PR + si * HPK;
-  const int64_t pstride = (int64_t)a.Hkv * SH::PR;
-  const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
-  const int64_t sstride = (int64_t)a.Hkv * HPK;
-  auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + c * pstride : sbase + (c - nP) * sstride) + j; };
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
-
-  float M[MV], L[MV];
-  f32x4 O[MV];
-#pragma unroll
-  for (int v = 0; v < MV; ++v) {
-    M[v] = NEG_INF;
-    L[v] = 0.f;
-    O[v] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  for (int c0 = w; c0 < n; c0 += 4 * MCU) {
-    uint64_t ml[MCU][MV];
-    f32x4 ov[MCU][MV];
-#pragma unroll
-    for (int u = 0; u < MCU; ++u) {
-      const int c = c0 + 4 * u;
-#pragma unroll
-      for (int v = 0; v < MV; ++v) {
-        const int x = (v * 64 + lane) * 4, j = x / D, d = x - j * D;
-        if (c < n && x < MS::OPP) {
-          const int64_t r = rec(c, j);
-          ml[u][v] = __hip_atomic_load((const uint64_t*)(a.ws_ml + r * 2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          ov[u][v] = __builtin_bit_cast(
-              f32x4, __builtin_amdgcn_raw_buffer_load_b128(wsr, (uint32_t)((r * D + d) * 4), 0, kCoherentPolicy));
-        } else {
-          ml[u][v] = (uint64_t)__float_as_uint(NEG_INF);
-          ov[u][v] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < MCU; ++u)
-#pragma unroll
-      for (int v = 0; v < MV; ++v) {
-        const float mc = __uint_as_float((uint32_t)ml[u][v]), lc = __uint_as_float((uint32_t)(ml[u][v] >> 32));
-        const float nm = fmaxf(M[v], mc);
-        const float base = nm == NEG_INF ? 0.f : nm;
-        const float al = exp2_fast(M[v] - base), be = mc == NEG_INF ? 0.f : exp2_fast(mc - base);
-        L[v] = L[v] * al + lc * be;
-        O[v] = O[v] * al + ov[u][v] * be;
-        M[v] = nm;
-      }
-  }
-#pragma unroll
-  for (int v = 0; v < MV; ++v) {
-    float* e = smem + ((w * MV + v) * 64 + lane) * 8;
-    e[0] = M[v];
-    e[1] = L[v];
-    *(f32x4*)(e + 4) = O[v];
-  }
-  __syncthreads();
-  for (int t = threadIdx.x; t < MS::NVEC; t += kBlockThreads) {
-    const int v = t >> 6, ln = t & 63;
-    float mw[4], mx = NEG_INF;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      mw[q] = smem[((q * MV + v) * 64 + ln) * 8];
-      mx = fmaxf(mx, mw[q]);
-    }
-    const float base = mx == NEG_INF ? 0.f : mx;
-    float Lt = 0.f;
-    f32x4 Ot = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float* e = smem + ((q * MV + v) * 64 + ln) * 8;
-      const float wq = mw[q] == NEG_INF ? 0.f : exp2_fast(mw[q] - base);
-      Lt += wq * e[1];
-      Ot += *(const f32x4*)(e + 4) * wq;
-    }
-    const int x = t * 4, j = x / D, d = x - j * D;
-    *(f32x4*)(a.o + ((int64_t)s * a.Hq + g * HPK + j) * D + d) = Ot * (1.f / Lt);
-  }
-}
-
-// A producer block has stored its partial: once every thread's stores have
-// completed, count one arrival on `ctr`.
-__device__ __forceinline__ void arrive(int32_t* ctr) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
-  __syncthreads();                // ... and so have every thread's
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ int32_t* prefix_counter(const StepArgs& a, int p, int g) {
-  return a.counters + (int64_t)(p * a.Hkv + g) * kCounterStride;
-}
-__device__ __forceinline__ int32_t* suffix_counter(const StepArgs& a, int s, int g) {
-  return a.counters + (int64_t)((a.num_prompts + s) * a.Hkv + g) * kCounterStride;
-}
-// Counters wrap: `reached` compares by the sign of the difference.
-__device__ __forceinline__ bool reached(const int32_t* ctr, int32_t target) {
-  const int32_t v = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return (int32_t)((uint32_t)v - (uint32_t)target) >= 0;
-}
-
-// Merge block of (slot s, KV head g): wait until the prefix chunks of its
-// prompt and its own response chunks have all arrived (bounded), then merge.
-template <class SH>
-__device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag, float* smem) {
-  if (threadIdx.x == 0) {
-    const int p = s / a.m;
-    const int32_t* pc = prefix_counter(a, p, g);
-    const int32_t* sc = suffix_counter(a, s, g);
-    const int32_t pt = a.prompt[p].target, stg = a.slot[s].target;
-    bool ok = false;
-    if (a.merge_polls >= 0) {
-      ok = reached(sc, stg) && reached(pc, pt);
-      for (int spins = 0; !ok && spins < a.merge_polls; ++spins) {
-        __builtin_amdgcn_s_sleep(2);
-        ok = reached(sc, stg) && reached(pc, pt);
-      }
-    }
-    *flag = ok;
-  }
-  __syncthreads();
-  if (!*flag) {
-    if (threadIdx.x == 0) __hip_atomic_store(a.status, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
-    for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = __builtin_nanf("");
-    return;
-  }
-  merge_outputs<SH>(a, s, g, smem);
-}
-
-template <class SH>
-__device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, unsigned long long* flagp) {
-  const int item = blockIdx.x / a.Hkv;
-  const int g = blockIdx.x - item * a.Hkv;
-  if (item < a.n_prefix_items) {
-    int p = 0;
-    while (p < a.num_prompts - 1 && !(a.prompt[p].nchunks > 0 && item < a.prompt[p].item_begin + a.prompt[p].nchunks))
-      ++p;
-    const int c = item - a.prompt[p].item_begin;
-    if constexpr (SH::ROWSPLIT)
-      prefix_mfma_rows<SH>(a, p, c, g);
-    else if constexpr (SH::MFMA)
-      prefix_mfma<SH>(a, p, c, g, smem);
-    else
-      prefix_wave<SH>(a, p, c, g, smem);
-    arrive(prefix_counter(a, p, g));
-    return;
-  }
-  int it = item - a.n_prefix_items;
-  if (it < a.n_suffix_items) {
-    const int lane = threadIdx.x & 63;
-    bool hit = false;
-    if (lane < a.S) {
-      const int len = a.slot[lane].len, b = a.slot[lane].item_begin;
-      hit = len > 0 && it >= b && it < b + (len + a.split - 1) / a.split;
-    }
-    const int s = __ffsll((long long)__ballot(hit)) - 1;
-    if (s < 0) return;  // unreachable with a consistent plan
-    const int c = it - a.slot[s].item_begin;
-    suffix_chunk<SH>(a, s, c, g, smem);
-    arrive(suffix_counter(a, s, g));
-    return;
-  }
-  it -= a.n_suffix_items;
-  if (it < a.n_zero_items) {
-    const int s = a.zero_slot[it];
-    float* o = a.o + ((int64_t)s * a.Hq + g * SH::HPK) * SH::D;
-    for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = 0.f;
-    return;
-  }
-  it -= a.n_zero_items;
-  merge_block<SH>(a, a.live_slot[it], g, flagp, smem);
-}
-
-// Timing mode (a.clock_start != null): every block folds its start and end
-// time (device wall clock) into one of this launch's start / end slots.
-template <class SH>
-__global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(const StepArgs a) {
-  constexpr int SMEM = SH::SMEM > MergeShape<SH>::SMEM ? SH::SMEM : MergeShape<SH>::SMEM;
-  __shared__ __attribute__((aligned(16))) float smem[SMEM];
-  __shared__ unsigned long long flag;
-  const int cs = (blockIdx.x % kClockSlots) * kClockStride;
-  if (a.clock_start && threadIdx.x == 0)
-    __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-  decode_block<SH>(a, smem, &flag);
-  if (a.clock_start) {
-    __syncthreads();
-    if (threadIdx.x == 0)
-      __hip_atomic_fetch_max(a.clock_end + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
-
-// ----------------------------------------------------------------------------
-// Prefill: [plen, Hkv, D] -> prefix store.  One thread per 16-byte unit.
-// ----------------------------------------------------------------------------
-template <class SH>
-__global__ __launch_bounds__(256) void prefill_plain_kernel(char* store, const char* k, const char* v, int prompt,
-                                                           int plen, int hkv, int pmax) {
-  const int64_t units = (int64_t)hkv * 2 * plen * SH::LPT;
-  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < units; u += (int64_t)gridDim.x * blockDim.x) {
-    const int ch = u % SH::LPT;
-    const int64_t r = u / SH::LPT;
-    const int j = r % plen;
-    const int kind = (r / plen) % 2;
-    const int g = r / (2 * plen);
-    const u32x4* src = (const u32x4*)((kind ? v : k) + ((int64_t)j * hkv + g) * SH::ROWB) + ch;
-    char* dst = store + (((int64_t)prompt * hkv + g) * 2 + kind) * pmax * SH::ROWB + (int64_t)j * SH::ROWB;
-    *((u32x4*)dst + ch) = *src;
-  }
-}
-
-// MFMA layout per (prompt, kv head), per 32-token block: a K block of
-// [2 token halves][KB][64 lanes][8] and a V block of [DB][64 lanes][8].
-// K unit (mb, kb, lane): tokens mb*16 + lane%16, dims kb*32 + 8*(lane/16) + e.
-// V unit (db, lane): dim db*16 + lane%16, tokens tau(8*(lane/16) + e) where
-// tau(8q+e) = 4q+e for e < 4 and 16+4q+(e-4) otherwise -- the order in which
-// a lane holds probabilities after the S^T tiles.  Padding tokens are zero.
-template <class SH>
-__global__ __launch_bounds__(256) void prefill_mfma_kernel(char* store, const uint16_t* k, const uint16_t* v,
-                                                          int prompt, int plen, int hkv, int pmax) {
-  constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, KES = SH::KES;
-  constexpr int KU = 2 * KB * 64, VU = DB * 64, BU = KU + VU;
-  const int nblk = (plen + kMfmaBlock - 1) / kMfmaBlock;
-  const int64_t units = (int64_t)hkv * nblk * BU;
-  for (int64_t u = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; u < units; u += (int64_t)gridDim.x * blockDim.x) {
-    const int g = u / ((int64_t)nblk * BU);
-    const int rem = u - (int64_t)g * nblk * BU;
-    const int b = rem / BU;
-    int x = rem - b * BU;
-    char* blk = store + (((int64_t)prompt * hkv + g) * (pmax / kMfmaBlock) + b) * (2 * kMfmaBlock * D * KES);
-    uint16_t vals[8];
-    char* dst;
-    if (x < KU) {
-      const int lane = x & 63, sub = x >> 6, mb = sub / KB, kb = sub - mb * KB;
-      const int tok = b * kMfmaBlock + mb * 16 + (lane & 15);
-      const int d0 = kb * 32 + (lane >> 4) * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) vals[e] = tok < plen ? k[((int64_t)tok * hkv + g) * D + d0 + e] : 0;
-      dst = blk + (int64_t)x * 8 * KES;
-    } else {
-      x -= KU;
-      const int lane = x & 63, db = x >> 6, qq = lane >> 4;
-      const int d = db * 16 + (lane & 15);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int tok = b * kMfmaBlock + (e < 4 ? 4 * qq + e : 16 + 4 * qq + (e - 4));
-        vals[e] = tok < plen ? v[((int64_t)tok * hkv + g) * D + d] : 0;
-      }
-      dst = blk + (int64_t)kMfmaBlock * D * KES + (int64_t)x * 8 * KES;
-    }
-    u32x4 w;
-    w.x = vals[0] | ((uint32_t)vals[1] << 16);
-    w.y = vals[2] | ((uint32_t)vals[3] << 16);
-    w.z = vals[4] | ((uint32_t)vals[5] << 16);
-    w.w = vals[6] | ((uint32_t)vals[7] << 16);
-    st_kv<SH>(dst, w);
-  }
-}
-
-// ----------------------------------------------------------------------------
-// Instantiation table.
-// ----------------------------------------------------------------------------
-struct Entry {
-  KernelKey key;
-  void (*decode)(const StepArgs);
-  int smem_floats;
-};
-
-#define INFS_KERNELS(X)      \
-  X(false, 64, 1, false, 8)  \
-  X(false, 64, 2, false, 8)  \
-  X(false, 64, 2, false, 16) \
-  X(false, 64, 4, false, 16) \
-  X(false, 128, 1, false, 8) \
-  X(false, 128, 2, false, 8) \
-  X(false, 128, 2, false, 16) \
-  X(false, 128, 4, false, 16) \
-  X(true, 64, 2, false, 8)   \
-  X(true, 64, 2, true, 16)   \
-  X(true, 64, 2, true, 32)   \
-  X(true, 64, 2, true, 64)   \
-  X(true, 64, 2, true, 128)  \
-  X(true, 128, 1, false, 8)  \
-  X(true, 128, 1, true, 16)  \
-  X(true, 128, 1, true, 32)  \
-  X(true, 128, 1, true, 64)  \
-  X(true, 128, 2, false, 8)  \
-  X(true, 128, 2, false, 16) \
-  X(true, 128, 2, true, 16)  \
-  X(true, 128, 2, true, 32)  \
-  X(true, 128, 2, true, 64)  \
-  X(true, 128, 2, true, 128) \
-  X(true, 128, 4, false, 16) \
-  X(true, 128, 4, true, 16)  \
-  X(true, 128, 4, true, 32)  \
-  X(true, 128, 4, true, 64)  \
-  X(true, 128, 4, true, 128) \
-  X(true, 128, 8, true, 64)  \
-  X(true, 128, 8, true, 128)
-
-// FP8 KV cache: bf16 MFMA shapes of head_dim 128.
-#define INFS_KERNELS_KV8(X) \
-  X(128, 1, 16)             \
-  X(128, 1, 32)             \
-  X(128, 1, 64)             \
-  X(128, 2, 16)             \
-  X(128, 2, 32)             \
-  X(128, 2, 64)             \
-  X(128, 2, 128)            \
-  X(128, 4, 16)             \
-  X(128, 4, 32)             \
-  X(128, 4, 64)             \
-  X(128, 4, 128)            \
-  X(128, 8, 64)             \
-  X(128, 8, 128)
-
-#define INFS_ENTRY(bf, d, hpk, mf, pr) \
-  {{bf, d, hpk, mf, pr, 0}, decode_kernel<Shape<bf, d, hpk, mf, pr>>, Shape<bf, d, hpk, mf, pr>::SMEM},
-#define INFS_ENTRY_KV8(d, hpk, pr) \
-  {{1, d, hpk, 1, pr, 1}, decode_kernel<Shape<true, d, hpk, true, pr, true>>, Shape<true, d, hpk, true, pr, true>::SMEM},
-
-const Entry kTable[] = {INFS_KERNELS(INFS_ENTRY) INFS_KERNELS_KV8(INFS_ENTRY_KV8)};
-
-const Entry* find_entry(const KernelKey& k) {
-  for (const Entry& e : kTable)
-    if (e.key.bf16 == k.bf16 && e.key.head_dim == k.head_dim && e.key.hpk == k.hpk && e.key.mfma == k.mfma &&
-        e.key.prefix_rows == k.prefix_rows && e.key.kv8 == k.kv8)
-      return &e;
   return nullptr;
 }
 
@@ -1176,7 +49,7 @@ int64_t prefix_elems_per_head(const KernelKey& key, int pmax_padded) {
 }
 
 hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream) {
-  const Entry* e = find_entry(key);
+  const KernelEntry* e = find_entry(key);
   if (!e) return hipErrorInvalidValue;
   hipLaunchKernelGGL(e->decode, dim3(grid), dim3(kBlockThreads), 0, stream, args);
   return hipGetLastError();

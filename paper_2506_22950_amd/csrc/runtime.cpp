@@ -938,6 +938,13 @@ infs_status infs_get_stats(const infs_ctx* c, infs_stats* out) {
   return INFS_OK;
 }
 
+infs_status infs_get_kernel_info(const infs_ctx* c, infs_kernel_info* out) {
+  if (!c || !out) return fail(nullptr, INFS_E_ARG, "null argument");
+  *out = infs_kernel_info{c->key.bf16, c->key.head_dim, c->key.hpk, c->key.mfma, c->key.prefix_rows, c->key.kv8,
+                          c->probe_batch > 0 ? c->pkey.mfma : 0, c->probe_batch > 0 ? c->pkey.prefix_rows : 0};
+  return INFS_OK;
+}
+
 infs_status infs_timing_begin(infs_ctx* c) {
   CHECK_CTX(c);
   if (c->dry) return fail(c, INFS_E_STATE, "no timing in a dry-run context");

@@ -34,6 +34,7 @@ EXPORTS = (
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
+    "infs_get_kernel_info",
 )
 
 
@@ -52,6 +53,11 @@ class Config(ctypes.Structure):
         ("split_tokens", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float),
         ("flags", ctypes.c_uint32), ("probe_tokens", ctypes.c_int32),
     ]
+
+
+class KernelInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("bf16", "head_dim", "hpk", "mfma", "prefix_rows", "kv_fp8",
+                                             "probe_mfma", "probe_prefix_rows")]
 
 
 class Stats(ctypes.Structure):
@@ -85,6 +91,7 @@ def load():
         "infs_sample_tokens": (I32, [P, I32, ctypes.POINTER(I32), I32]),
         "infs_sync": (I32, [P]),
         "infs_get_stats": (I32, [P, ctypes.POINTER(Stats)]),
+        "infs_get_kernel_info": (I32, [P, ctypes.POINTER(KernelInfo)]),
         "infs_timing_begin": (I32, [P]),
         "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(I64)]),
@@ -252,6 +259,12 @@ class Context:
         s = Stats()
         self._call(load().infs_get_stats, ctypes.byref(s))
         return s
+
+    def kernel_info(self) -> dict:
+        """The decode (and probe) kernel instantiation this context runs."""
+        k = KernelInfo()
+        self._call(load().infs_get_kernel_info, ctypes.byref(k))
+        return {n: getattr(k, n) for n, _ in KernelInfo._fields_}
 
     def timing_begin(self):
         self._call(load().infs_timing_begin)

@@ -15,6 +15,9 @@ import pytest
 from oracle import POLICIES, simulate, simulate_group
 from paper_2506_22950_amd import infs
 from paper_2506_22950_amd.group import context_for, decode_group, plan_steps, schedulers_for
+from tests.shape_table import ENTRIES as SHAPE_ENTRIES
+from tests.shape_table import case_for
+from tests.shape_table import case_id as shape_case_id
 from workload import CONFIGS, Workload, get_config
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "infs.h")
@@ -357,3 +360,14 @@ def test_fp8_kv_validation():
         assert ei.value.status == infs.E_ARG
     ctx = context_for(get_config("qwen3_1p7b_g64"), dry_run=True, kv_fp8=True)
     ctx.destroy()
+
+
+@pytest.mark.parametrize("entry", SHAPE_ENTRIES, ids=shape_case_id)
+def test_kernel_selection_reaches_every_instantiation(entry):
+    # Each instantiation is selected by its small workload (dry run, no GPU).
+    cfg, probe, want = case_for(entry)
+    ctx = context_for(cfg, dry_run=True, probe_tokens=probe, kv_fp8=entry[5])
+    got = ctx.kernel_info()
+    ctx.destroy()
+    for k, v in want.items():
+        assert got[k] == v, (k, got)
