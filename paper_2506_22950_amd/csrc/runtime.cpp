@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <functional>
@@ -102,6 +103,7 @@ struct infs_ctx {
   double step_bytes = 0, step_flops = 0;
   infs_stats stats{};
   bool dead = false;
+  std::string dead_msg;  // the device error that made the context unusable
   std::string err = "no error";
   Timing timing;
 };
@@ -122,9 +124,13 @@ infs_status fail(infs_ctx* c, infs_status st, const char* fmt, ...) {
 }
 
 infs_status device_fail(infs_ctx* c, hipError_t e, const char* what) {
-  if (c) c->dead = true;
-  return fail(c, e == hipErrorOutOfMemory ? INFS_E_NOMEM : INFS_E_DEVICE, "%s failed: %s", what,
-              hipGetErrorString(e));
+  const infs_status st = fail(c, e == hipErrorOutOfMemory ? INFS_E_NOMEM : INFS_E_DEVICE, "%s failed: %s", what,
+                              hipGetErrorString(e));
+  if (c) {
+    c->dead = true;
+    c->dead_msg = c->err;
+  }
+  return st;
 }
 
 #define HIP_TRY(ctx, expr)                                  \
@@ -136,7 +142,7 @@ infs_status device_fail(infs_ctx* c, hipError_t e, const char* what) {
 #define CHECK_CTX(c)                                                                  \
   do {                                                                                \
     if (!(c)) return fail(nullptr, INFS_E_ARG, "null context");                      \
-    if ((c)->dead) return fail(c, INFS_E_DEVICE, "context unusable after a device error: %s", (c)->err.c_str()); \
+    if ((c)->dead) return fail(c, INFS_E_DEVICE, "context unusable after a device error: %s", (c)->dead_msg.c_str()); \
   } while (0)
 
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -375,8 +381,10 @@ infs_status check_status(infs_ctx* c) {
   int32_t st = 0;
   HIP_TRY(c, hipMemcpy(&st, c->status, sizeof st, hipMemcpyDeviceToHost));
   if (st != 0) {
+    fail(c, INFS_E_DEVICE, "a merge work-group gave up waiting for its producers; outputs are invalid");
     c->dead = true;
-    return fail(c, INFS_E_DEVICE, "a merge work-group gave up waiting for its producers; outputs are invalid");
+    c->dead_msg = c->err;
+    return INFS_E_DEVICE;
   }
   return INFS_OK;
 }
@@ -516,9 +524,17 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     delete c;
     return fail(nullptr, INFS_E_ARG, "page table of %d sequences x %d pages exceeds 2 GiB", c->H, c->pages_per_slot);
   }
-  c->num_pages = k.num_pages ? k.num_pages
-                             : c->S * c->pages_per_slot +
-                                   (c->probe_k > 0 ? c->NP * c->G * ceil_div(c->probe_k, infs::kPageTokens) : 0);
+  {
+    const int64_t pages = k.num_pages ? (int64_t)k.num_pages
+                                      : (int64_t)c->S * c->pages_per_slot +
+                                            (c->probe_k > 0 ? (int64_t)c->NP * c->G * ceil_div(c->probe_k, infs::kPageTokens)
+                                                            : 0);
+    if (pages > INT32_MAX) {
+      delete c;
+      return fail(nullptr, INFS_E_ARG, "a page pool of %lld pages is beyond the page index range", (long long)pages);
+    }
+    c->num_pages = (int)pages;
+  }
   c->prefix_split = key.mfma ? infs::kMfmaPrefixSplit : c->split;
   c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->prefix_split));
   c->scmax = ceil_div(k.max_suffix_len, c->split);
