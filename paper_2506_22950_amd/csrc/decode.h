@@ -133,22 +133,28 @@ struct Shape {
   static constexpr int NB = PR / 16;               // MFMA row blocks
   static constexpr int KB = D / 32;                // MFMA k-blocks over head_dim
   static constexpr int DB = D / 16;                // MFMA 16-wide head_dim blocks
-  // More than 64 MFMA rows: each wavefront owns a quarter of the rows and
-  // walks the whole chunk, so the four need no combine.
-  static constexpr bool ROWSPLIT = MFMA && PR > 64;
+  // MFMA prefix work split over the four wavefronts: RG row groups of NBW
+  // 16-row tiles times TG token groups of BPW 32-token blocks of the chunk
+  // (16 rows: 1 x 4, 32 rows: 2 x 2, 64 rows: 4 x 1, 128 rows: 4 x 1 with two
+  // tiles per wavefront).  Token groups of one row group combine through LDS.
+  static constexpr int NBW = NB >= 8 ? 2 : 1;
+  static constexpr int RG = MFMA ? NB / NBW : 1;
+  static constexpr int TG = kWaves / RG;
+  static constexpr int BPW = (kMfmaPrefixSplit / kMfmaBlock) / TG;
   static constexpr int WAVE_NR = (!MFMA && PR > HPK) ? PR : HPK;
   static constexpr int WAVE_SMEM = 4 * WAVE_NR * (D + 2);
-  static constexpr int MFMA_SLOT = (MFMA && !ROWSPLIT) ? (NB * DB * 64 * 4 + 2 * NB * 64) : 0;
-  static constexpr int MFMA_SMEM = 4 * MFMA_SLOT;
+  static constexpr int MFMA_SLOT = (MFMA && TG > 1) ? (NBW * DB * 64 * 4 + 2 * NBW * 64) : 0;
+  static constexpr int MFMA_SMEM = kWaves * MFMA_SLOT;
   static constexpr int SMEM = WAVE_SMEM > MFMA_SMEM ? WAVE_SMEM : MFMA_SMEM;
-  // 64 MFMA rows keep 128 accumulator registers live, and 16 wavefront rows
-  // as many: those shapes run 1 wavefront per SIMD rather than spill; every
-  // other shape runs 2 per SIMD.
-  static constexpr int MIN_WAVES = ROWSPLIT ? 2 : ((MFMA && NB > 2) || (!MFMA && PR >= 16)) ? 1 : 2;
+  // 16 wavefront rows keep as many accumulators live as fill a SIMD's
+  // registers at two wavefronts: that shape runs one per SIMD rather than
+  // spill; every other shape runs (at least) two per SIMD.
+  static constexpr int MIN_WAVES = (!MFMA && PR >= 16) ? 1 : 2;
   static_assert(LPT >= 2 && LPT <= 64, "row size");
   static_assert(!MFMA || BF, "MFMA path is bf16");
   static_assert(!KV8 || (BF && MFMA), "FP8 KV on the bf16 MFMA shapes");
   static_assert(!MFMA || (PR % 16 == 0), "MFMA rows");
+  static_assert(!MFMA || (NB % NBW == 0 && kWaves % RG == 0 && DB % TG == 0 && BPW >= 1), "MFMA work split");
 };
 
 // ----------------------------------------------------------------------------
@@ -544,145 +550,34 @@ __device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const 
   }
 }
 
-// Combine the four wavefronts' MFMA partials of one chunk (same rows, disjoint
-// token ranges) and store rows 0 .. nrows-1 as records rec0 + row.  Every
-// wavefront publishes its fragments to LDS; after one barrier each combines
-// the four for a quarter of the head dimension and stores it.
-template <class XS>
-__device__ void mfma_combine_store(const StepArgs& a, float* smem, f32x4 (&acc)[XS::NB][XS::DB],
-                                   float (&mrow)[XS::NB], float (&lrow)[XS::NB], int64_t rec0, int nrows) {
-  constexpr int NB = XS::NB, DB = XS::DB, D = XS::D;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    lrow[nb] += __shfl_xor(lrow[nb], 16);
-    lrow[nb] += __shfl_xor(lrow[nb], 32);
-  }
-  constexpr int OFL = NB * DB * 64 * 4;
-  {
-    float* sl = smem + w * XS::MFMA_SLOT;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-      for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
-      sl[OFL + nb * 64 + lane] = mrow[nb];
-      sl[OFL + NB * 64 + nb * 64 + lane] = lrow[nb];
-    }
-  }
-  __syncthreads();
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
-  constexpr int DBW = DB / 4;  // head-dim blocks stored by each wave
-  static_assert(DB % 4 == 0, "head_dim blocks per wave");
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    if (nb * 16 + r16 >= nrows) continue;
-    float M = NEG_INF;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) M = fmaxf(M, smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane]);
-    const float Mu = (M == NEG_INF) ? 0.f : M;
-    float wv[4], L = 0.f;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      wv[v] = exp2_fast(smem[v * XS::MFMA_SLOT + OFL + nb * 64 + lane] - Mu);
-      L += wv[v] * smem[v * XS::MFMA_SLOT + OFL + NB * 64 + nb * 64 + lane];
-    }
-    const int64_t rec = rec0 + nb * 16 + r16;
-#pragma unroll
-    for (int x = 0; x < DBW; ++x) {
-      const int db = w * DBW + x;
-      f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc4 += *(const f32x4*)(smem + v * XS::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[v];
-      st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
-    }
-    if (w == 0 && q4 == 0) {
-      st_coherent(a.ws_ml + rec * 2 + 0, M);
-      st_coherent(a.ws_ml + rec * 2 + 1, L);
-    }
-  }
-}
-
+// ----------------------------------------------------------------------------
+// Prefix chunk on MFMA tiles.  Wavefront w takes row group rg = w % RG (its
+// NBW 16-row tiles) and token group tg = w / RG (BPW consecutive 32-token
+// blocks of the chunk), walking its blocks with the next block's loads in
+// flight while the current one is multiplied (with two tiles per wavefront,
+// only the next K).  With one token group the
+// wavefront stores its rows' partial directly; otherwise the token groups of
+// a row group publish their partials to LDS and, after one barrier, each
+// combines DB / TG of the head-dimension blocks of its row group and stores
+// them.
+// ----------------------------------------------------------------------------
 template <class SH>
 __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
-  constexpr int D = SH::D, NB = SH::NB, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
-  const int plen = a.prompt[p].plen;
-  const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
-  const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
-  const int bpw = a.prefix_split / kMfmaBlock / 4;
-  const int b0 = w * bpw, b1 = min(b0 + bpw, nblk);
-  const float sl2 = a.scale_log2;
-
-  bf16x8 bq[NB][KB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const int row = nb * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
-    const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
-    const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      if (ok)
-        bq[nb][kb] = *(const bf16x8*)(qr + kb * 32 + q4 * 8);
-      else
-        bq[nb][kb] = bf16x8{};
-    }
-  }
-
-  f32x4 acc[NB][DB];
-  float mrow[NB], lrow[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    mrow[nb] = NEG_INF;
-    lrow[nb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) acc[nb][db] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  const char* head = (const char*)a.prefix +
-                     ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
-  // One 32-token block (16 KB of K and V) in flight per wavefront: the
-  // register budget is kept at two wavefronts per SIMD, and the second
-  // wavefront hides this one's load latency.
-  for (int b = b0; b < b1; ++b) {
-    bf16x8 ka[2][KB], va[DB];
-    const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
-    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
-#pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
-    mfma_block<SH>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
-  }
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
-  mfma_combine_store<SH>(a, smem, acc, mrow, lrow, rec0, SH::PR);
-}
-
-// ----------------------------------------------------------------------------
-// Prefix chunk on MFMA tiles with more than 64 rows (e.g. the probe phase of
-// prefix reuse, where every sample of the group shares the prefix): wavefront
-// w owns row tiles w*NBW .. w*NBW+NBW-1 and walks every 32-token block of the
-// chunk (the other wavefronts' reads of the same blocks hit the cache), then
-// stores its rows' partial directly.
-// ----------------------------------------------------------------------------
-template <class SH>
-__device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
   constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
-  constexpr int NBW = SH::NB / kWaves;
-  static_assert(SH::NB % kWaves == 0, "row tiles per wavefront");
+  constexpr int NBW = SH::NBW, RG = SH::RG, TG = SH::TG, BPW = SH::BPW;
   using WS = Shape<true, D, HPK, true, NBW * 16>;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, q4 = lane >> 4, r16 = lane & 15;
+  const int rg = w % RG, tg = w / RG;
   const int plen = a.prompt[p].plen;
   const int t0 = c * a.prefix_split, t1 = min(t0 + a.prefix_split, plen);
   const int nblk = (t1 - t0 + kMfmaBlock - 1) / kMfmaBlock;
+  const int b0 = tg * BPW, b1 = min(b0 + BPW, nblk);
   const float sl2 = a.scale_log2;
 
   bf16x8 bq[NBW][KB];
 #pragma unroll
   for (int nb = 0; nb < NBW; ++nb) {
-    const int row = (w * NBW + nb) * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
+    const int row = (rg * NBW + nb) * 16 + r16, si = row / HPK, j = row - si * HPK, s = p * a.m + min(si, a.m - 1);
     const bool ok = row < a.prefix_rows && a.slot[s].len > 0;
     const uint16_t* qr = (const uint16_t*)a.q + ((int64_t)s * a.Hq + g * HPK + j) * D;
 #pragma unroll
@@ -699,18 +594,48 @@ __device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
   }
   const char* head = (const char*)a.prefix +
                      ((int64_t)(p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);
-  for (int b = 0; b < nblk; ++b) {
-    bf16x8 ka[2][KB], va[DB];
+  auto fetch_k = [&](int b, bf16x8 (&ka)[2][KB]) {
     const char* kblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES);
-    const char* vblk = kblk + kMfmaBlock * D * SH::KES;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
         ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
+  };
+  auto fetch_v = [&](int b, bf16x8 (&va)[DB]) {
+    const char* vblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES) +
+                       kMfmaBlock * D * SH::KES;
 #pragma unroll
     for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
-    mfma_block<WS>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
+  };
+  // With two tiles per wavefront the accumulators leave room to prefetch only
+  // the next block's K; its V is fetched once the current block is done.
+  constexpr bool PREFETCH_V = NBW == 1;
+  if (b0 < b1) {
+    bf16x8 ka[2][KB], va[DB];
+    fetch_k(b0, ka);
+    fetch_v(b0, va);
+    for (int b = b0; b < b1; ++b) {
+      const bool more = b + 1 < b1;
+      bf16x8 kn[2][KB], vn[DB];
+      if (more) {
+        fetch_k(b + 1, kn);
+        if constexpr (PREFETCH_V) fetch_v(b + 1, vn);
+      }
+      mfma_block<WS>(ka, va, bq, t0 + b * kMfmaBlock, t1, sl2, acc, mrow, lrow);
+      if (more) {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int kb = 0; kb < KB; ++kb) ka[mb][kb] = kn[mb][kb];
+        if constexpr (PREFETCH_V) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db) va[db] = vn[db];
+        } else {
+          fetch_v(b + 1, va);
+        }
+      }
+    }
   }
 #pragma unroll
   for (int nb = 0; nb < NBW; ++nb) {
@@ -719,14 +644,58 @@ __device__ void prefix_mfma_rows(const StepArgs& a, int p, int c, int g) {
   }
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
   const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
+  if constexpr (TG == 1) {
 #pragma unroll
-  for (int nb = 0; nb < NBW; ++nb) {
-    const int64_t rec = rec0 + (w * NBW + nb) * 16 + r16;
+    for (int nb = 0; nb < NBW; ++nb) {
+      const int64_t rec = rec0 + (rg * NBW + nb) * 16 + r16;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
-    if (q4 == 0) {
-      st_coherent(a.ws_ml + rec * 2 + 0, mrow[nb]);
-      st_coherent(a.ws_ml + rec * 2 + 1, lrow[nb]);
+      for (int db = 0; db < DB; ++db) st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
+      if (q4 == 0) {
+        st_coherent(a.ws_ml + rec * 2 + 0, mrow[nb]);
+        st_coherent(a.ws_ml + rec * 2 + 1, lrow[nb]);
+      }
+    }
+  } else {
+    constexpr int OFL = NBW * DB * 64 * 4;
+    {
+      float* sl = smem + w * SH::MFMA_SLOT;
+#pragma unroll
+      for (int nb = 0; nb < NBW; ++nb) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) *(f32x4*)(sl + ((nb * DB + db) * 64 + lane) * 4) = acc[nb][db];
+        sl[OFL + nb * 64 + lane] = mrow[nb];
+        sl[OFL + NBW * 64 + nb * 64 + lane] = lrow[nb];
+      }
+    }
+    __syncthreads();
+    constexpr int DBW = DB / TG;  // head-dim blocks this wavefront combines and stores
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+      float M = NEG_INF;
+#pragma unroll
+      for (int t = 0; t < TG; ++t) M = fmaxf(M, smem[(t * RG + rg) * SH::MFMA_SLOT + OFL + nb * 64 + lane]);
+      const float Mu = (M == NEG_INF) ? 0.f : M;
+      float wv[TG], L = 0.f;
+#pragma unroll
+      for (int t = 0; t < TG; ++t) {
+        const float* sl = smem + (t * RG + rg) * SH::MFMA_SLOT;
+        wv[t] = exp2_fast(sl[OFL + nb * 64 + lane] - Mu);
+        L += wv[t] * sl[OFL + NBW * 64 + nb * 64 + lane];
+      }
+      const int64_t rec = rec0 + (rg * NBW + nb) * 16 + r16;
+#pragma unroll
+      for (int x = 0; x < DBW; ++x) {
+        const int db = tg * DBW + x;
+        f32x4 acc4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < TG; ++t)
+          acc4 += *(const f32x4*)(smem + (t * RG + rg) * SH::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[t];
+        st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
+      }
+      if (tg == 0 && q4 == 0) {
+        st_coherent(a.ws_ml + rec * 2 + 0, M);
+        st_coherent(a.ws_ml + rec * 2 + 1, L);
+      }
     }
   }
 }
@@ -957,9 +926,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     while (p < a.num_prompts - 1 && !(a.prompt[p].nchunks > 0 && item < a.prompt[p].item_begin + a.prompt[p].nchunks))
       ++p;
     const int c = item - a.prompt[p].item_begin;
-    if constexpr (SH::ROWSPLIT)
-      prefix_mfma_rows<SH>(a, p, c, g);
-    else if constexpr (SH::MFMA)
+    if constexpr (SH::MFMA)
       prefix_mfma<SH>(a, p, c, g, smem);
     else
       prefix_wave<SH>(a, p, c, g, smem);
