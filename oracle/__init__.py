@@ -6,7 +6,7 @@ anything in this package.  The GPU library never calls it, and it shares no
 code with the GPU library: the two meet only at the seeded input generator in
 ``workload/``.
 
-Two parts, both plain and slow on purpose:
+Three parts, all plain and slow on purpose:
 
 * ``attention`` -- float64 softmax attention of a decode query over the
   concatenation of the shared prompt KV and the sample's own response KV
