@@ -132,9 +132,9 @@ def _prefix_reuse(cfg, policy, k, split=128):
         f"{steps} decode steps ({n} outputs, max err {worst:.3g})")
 
 
-def test_bf16_prefix_reuse_probe_rowsplit():
+def test_bf16_prefix_reuse_probe_128_row_tiles():
     # Prefix reuse (Section 4): 40 samples decode 16 probe tokens together
-    # (80 query rows per KV head: the row-split MFMA prefix path), then SJF
+    # (80 query rows per KV head: 128-row MFMA tiles, two per wavefront), then SJF
     # decode resumes each at token 17; samples shorter than 17 never take a slot.
     cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(300,), samples_per_prompt=40,
                                              slots_per_prompt=8, length_dist=("lognormal", 3.5, 1.0, 1, 200),
