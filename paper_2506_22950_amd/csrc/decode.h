@@ -3,8 +3,9 @@
 // One launch per layer-step does all the device work of that layer:
 //   * append: each live slot's new K/V row goes into its response pages;
 //   * split-K attention over the shared prefix: one work-group per
-//     (prompt, KV head, chunk of `split` prefix tokens).  Every K/V byte of the
-//     chunk is read from HBM once and used by all m * hpk query rows of that
+//     (prompt, KV head, prefix chunk: 128 tokens on MFMA tiles, `split`
+//     tokens otherwise).  Every K/V byte of the chunk is read from HBM once
+//     and used by all m * hpk query rows of that
 //     KV head -- the rows of every live slot of the prompt.  With >= 16 rows
 //     the two contractions run on MFMA tiles (v_mfma_f32_16x16x32_bf16);
 //     below that, on wavefront dot products;
