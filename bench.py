@@ -517,6 +517,9 @@ def main():
                     help="prefix reuse: every sample decodes K probe tokens first (Section 4); default 0")
     ap.add_argument("--kv-fp8", action="store_true",
                     help="store the KV cache as E4M3 (halves the K/V bytes; not the headline configuration)")
+    ap.add_argument("--exchange", type=int, choices=(0, 1), default=None,
+                    help="partial exchange: 0 through the coherence point, 1 through the XCD's L2 "
+                         "(default: the library's choice)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -546,6 +549,8 @@ def main():
     if args.copy_calibration:
         copy_calibration(torch)
     b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8)
+    if args.exchange is not None:
+        b.ctx.set_exchange(args.exchange)
 
     for w in range(args.warmup):
         t0 = time.time()
@@ -577,7 +582,7 @@ def main():
         body_us = ms * 1000.0 / n
         per_launch = alg / n
         achieved = per_launch / (avg_us * 1e-6) / 1e9
-        traffic = read_traffic(args.workload) if not (args.reuse or args.kv_fp8) else None
+        traffic = read_traffic(args.workload) if not (args.reuse or args.kv_fp8 or args.exchange is not None) else None
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
@@ -644,6 +649,7 @@ def main():
             "probe_tokens": args.reuse, "probe_steps": len(b.plog),
             "kv_cache": "e4m3" if args.kv_fp8 else cfg.dtype,
             "staged_steps": b.window,
+            "exchange": {0: "coherence point", 1: "xcd l2"}[b.ctx.exchange_mode()],
         },
         "roofline": roof,
         "probe": probe,

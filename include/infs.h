@@ -255,6 +255,21 @@ infs_status infs_sync(infs_ctx* ctx);
    that error path from the host.  E_STATE while a step is open. */
 infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
 
+/* How work-groups of one decode launch hand their split-K partials to the merging work-group.
+   mode 0: stores written through to the device coherence point, loads from it: correct wherever
+           work-groups run.
+   mode 1: through the L2 of the XCD that runs a KV head's work-groups (fewer trips to the
+           coherence point).  Available when infs_create saw, in a probe launch, work-group b run on
+           XCD b % n for the device's n XCDs and num_kv_heads is a multiple of n; then it is the
+           default.  Every work-group checks its XCD again; a mismatch makes the next synchronising
+           call return E_DEVICE (outputs of that launch are invalid).
+   mode 2: mode 1 with every work-group's check made to fail, so the error path can be tested.
+   E_STATE while a step is open or when mode 1/2 is unavailable (always on dry-run contexts). */
+infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
+
+/* The current exchange mode (0, 1 or 2); -1 for a NULL context. */
+int32_t infs_exchange_mode(const infs_ctx* ctx);
+
 infs_status infs_get_stats(const infs_ctx* ctx, infs_stats* out);
 
 /* The decode kernel instantiation a context runs, fixed by infs_create from the element type, head

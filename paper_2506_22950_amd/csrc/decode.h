@@ -37,6 +37,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
 #define NEG_INF (-__builtin_huge_valf())
 
@@ -159,30 +160,56 @@ struct Shape {
 };
 
 // ----------------------------------------------------------------------------
-// Partials are exchanged between work-groups through agent-scope atomic
-// stores and loads (coherent across the XCDs' L2 caches), ordered by waiting
-// for the stores to complete before the arrival counter is bumped.  This
-// avoids the whole-cache write-back and invalidate of an agent-scope fence.
+// Partial exchange between work-groups.  Producers store their partials, wait
+// until the stores have completed and count an arrival; a merge reads them
+// once its counters show every arrival.  Two cache policies:
+//  * coherent: stores write through to the device coherence point and loads
+//    bypass the XCD's L2 (the policy of agent-scope atomic stores and loads),
+//    for producers and merges on any XCDs;
+//  * XCD-local (StepArgs::l2_xcds > 0): stores stop in the XCD's L2 and loads
+//    only miss the CU's L1.  Valid when every work-group of a KV head runs on
+//    one XCD: work-group b on XCD b % l2_xcds with Hkv a multiple of l2_xcds,
+//    which the host verified when it created the context and which every
+//    work-group checks again (a mismatch sets the status word).
+// Neither needs an agent-scope fence (on this chip one writes back the whole
+// L2).  Raw buffer resources over the workspace let a lane's 16 bytes leave
+// as one write; offsets are in bytes and below ws_o_bytes / ws_ml_bytes.  The
+// policy is a template parameter: the kernel picks one instantiation of its
+// work-group body per launch, so no load or store waits behind a branch.
 // ----------------------------------------------------------------------------
-__device__ __forceinline__ void st_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// 16-byte store into the partial-output workspace with the cache policy of
-// the agent-scope atomic store above (write through to the coherence point),
-// so that a lane's four consecutive floats leave as one write instead of
-// four partial-line writes.  The workspace is addressed by a raw buffer
-// resource over its whole size; byte_off must be below ws_o_bytes.
-constexpr int kCoherentPolicy = 16;  // sc1
 constexpr int kRawBufferWord3 = 0x00020000;
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t ws_rsrc(const StepArgs& a) {
-  return __builtin_amdgcn_make_buffer_rsrc(a.ws_o, 0, (int)a.ws_o_bytes, kRawBufferWord3);
-}
-__device__ __forceinline__ void st_coherent4(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, f32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, byte_off, 0, kCoherentPolicy);
-}
+constexpr int kStoreThrough = 16;  // sc1
+constexpr int kLoadCoherent = 16;  // sc1
+constexpr int kStoreL2 = 0;
+constexpr int kLoadL2 = 1;         // sc0: miss the CU's L1, hit the XCD's L2
+constexpr int kXccIdReg = 20 | (3 << 11);  // s_getreg operand: HW_REG_XCC_ID bits 3:0
+
+template <bool L2>
+struct Exchange {
+  static constexpr int kStore = L2 ? kStoreL2 : kStoreThrough;
+  static constexpr int kLoad = L2 ? kLoadL2 : kLoadCoherent;
+  __amdgpu_buffer_rsrc_t o, ml;
+  __device__ explicit Exchange(const StepArgs& a)
+      : o(__builtin_amdgcn_make_buffer_rsrc(a.ws_o, 0, (int)a.ws_o_bytes, kRawBufferWord3)),
+        ml(__builtin_amdgcn_make_buffer_rsrc(a.ws_ml, 0, (int)a.ws_ml_bytes, kRawBufferWord3)) {}
+  __device__ void store(uint32_t off, float v) const {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), o, off, 0, kStore);
+  }
+  __device__ void store4(uint32_t off, f32x4 v) const {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), o, off, 0, kStore);
+  }
+  // (M, L) of record rec.
+  __device__ void store_ml(int64_t rec, float m, float l) const {
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(m), __float_as_uint(l)}, ml, (uint32_t)(rec * 8), 0,
+                                          kStore);
+  }
+  __device__ f32x4 load4(uint32_t off) const {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(o, off, 0, kLoad));
+  }
+  __device__ u32x2 load_ml(int64_t rec) const {
+    return __builtin_amdgcn_raw_buffer_load_b64(ml, (uint32_t)(rec * 8), 0, kLoad);
+  }
+};
 
 // E4M3 (OCP) <-> bf16.  Widening is exact: every E4M3 value is a bf16 value.
 // Narrowing rounds to nearest even; magnitudes beyond 448 are clamped first,
@@ -384,9 +411,9 @@ __device__ __forceinline__ void wave_combine_groups(float (&m)[NR], float (&l)[N
 
 // Combine the four wavefronts' partials through LDS and store the block's
 // partial rows [0, NR) at records rec0 + r.
-template <class SH, int NR>
+template <class SH, int NR, bool L2>
 __device__ __forceinline__ void block_store_partial(float* smem, const float (&m)[NR], const float (&l)[NR],
-                                                    const float (&o)[NR][SH::EPL], float* ws_o, float* ws_ml,
+                                                    const float (&o)[NR][SH::EPL], const Exchange<L2>& ex,
                                                     int64_t rec0) {
   constexpr int D = SH::D, EPL = SH::EPL;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -419,11 +446,8 @@ __device__ __forceinline__ void block_store_partial(float* smem, const float (&m
       L += wgt * sml[(v * NR + r) * 2 + 1];
       O += wgt * so[(v * NR + r) * D + d];
     }
-    st_coherent(ws_o + (rec0 + r) * D + d, O);
-    if (d == 0) {
-      st_coherent(ws_ml + (rec0 + r) * 2 + 0, M);
-      st_coherent(ws_ml + (rec0 + r) * 2 + 1, L);
-    }
+    ex.store((uint32_t)(((rec0 + r) * D + d) * 4), O);
+    if (d == 0) ex.store_ml(rec0 + r, M, L);
   }
 }
 
@@ -464,7 +488,7 @@ __device__ __forceinline__ int64_t prefix_records(const StepArgs& a, int pr) {
 // ----------------------------------------------------------------------------
 // Prefix chunk, wavefront path (fewer than 16 rows): rows r = slot_in_prompt * hpk + j.
 // ----------------------------------------------------------------------------
-template <class SH>
+template <class SH, bool L2>
 __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem) {
   constexpr int PR = SH::PR, HPK = SH::HPK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
@@ -488,7 +512,7 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
   wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
   wave_combine_groups<SH, PR>(m, l, o);
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * PR;
-  block_store_partial<SH, PR>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
+  block_store_partial<SH, PR, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
 }
 
 // ----------------------------------------------------------------------------
@@ -562,7 +586,7 @@ __device__ __forceinline__ void mfma_block(const bf16x8 (&ka)[2][SH::KB], const 
 // combines DB / TG of the head-dimension blocks of its row group and stores
 // them.
 // ----------------------------------------------------------------------------
-template <class SH>
+template <class SH, bool L2>
 __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem) {
   constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, HPK = SH::HPK;
   constexpr int NBW = SH::NBW, RG = SH::RG, TG = SH::TG, BPW = SH::BPW;
@@ -644,17 +668,14 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
     lrow[nb] += __shfl_xor(lrow[nb], 32);
   }
   const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
+  const Exchange<L2> ex(a);
   if constexpr (TG == 1) {
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
       const int64_t rec = rec0 + (rg * NBW + nb) * 16 + r16;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
-      if (q4 == 0) {
-        st_coherent(a.ws_ml + rec * 2 + 0, mrow[nb]);
-        st_coherent(a.ws_ml + rec * 2 + 1, lrow[nb]);
-      }
+      for (int db = 0; db < DB; ++db) ex.store4((uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc[nb][db]);
+      if (q4 == 0) ex.store_ml(rec, mrow[nb], lrow[nb]);
     }
   } else {
     constexpr int OFL = NBW * DB * 64 * 4;
@@ -691,12 +712,9 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
 #pragma unroll
         for (int t = 0; t < TG; ++t)
           acc4 += *(const f32x4*)(smem + (t * RG + rg) * SH::MFMA_SLOT + ((nb * DB + db) * 64 + lane) * 4) * wv[t];
-        st_coherent4(wsr, (uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
+        ex.store4((uint32_t)((rec * D + db * 16 + q4 * 4) * 4), acc4);
       }
-      if (tg == 0 && q4 == 0) {
-        st_coherent(a.ws_ml + rec * 2 + 0, M);
-        st_coherent(a.ws_ml + rec * 2 + 1, L);
-      }
+      if (tg == 0 && q4 == 0) ex.store_ml(rec, M, L);
     }
   }
 }
@@ -705,7 +723,7 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
 // Response chunk of one live slot (hpk rows), plus the append of this step's
 // K/V when the chunk holds the newest position.
 // ----------------------------------------------------------------------------
-template <class SH>
+template <class SH, bool L2>
 __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem) {
   constexpr int HPK = SH::HPK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
@@ -752,7 +770,7 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   }
   wave_combine_groups<SH, HPK>(m, l, o);
   const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.suffix_chunks_max + c) * a.Hkv + g) * HPK;
-  block_store_partial<SH, HPK>(smem, m, l, o, a.ws_o, a.ws_ml, rec0);
+  block_store_partial<SH, HPK, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
 
   if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
     const int pos = len - 1;
@@ -782,7 +800,7 @@ struct MergeShape {
   static_assert(SH::D % 4 == 0, "vectors");
 };
 
-template <class SH>
+template <class SH, bool L2>
 __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
   using MS = MergeShape<SH>;
   constexpr int D = SH::D, HPK = SH::HPK, MV = MS::MV, MCU = MS::MCU;
@@ -795,7 +813,7 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
   const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
   const int64_t sstride = (int64_t)a.Hkv * HPK;
   auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + c * pstride : sbase + (c - nP) * sstride) + j; };
-  const __amdgpu_buffer_rsrc_t wsr = ws_rsrc(a);
+  const Exchange<L2> ex(a);
 
   float M[MV], L[MV];
   f32x4 O[MV];
@@ -806,7 +824,7 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
     O[v] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   for (int c0 = w; c0 < n; c0 += 4 * MCU) {
-    uint64_t ml[MCU][MV];
+    u32x2 ml[MCU][MV];
     f32x4 ov[MCU][MV];
 #pragma unroll
     for (int u = 0; u < MCU; ++u) {
@@ -816,11 +834,10 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
         const int x = (v * 64 + lane) * 4, j = x / D, d = x - j * D;
         if (c < n && x < MS::OPP) {
           const int64_t r = rec(c, j);
-          ml[u][v] = __hip_atomic_load((const uint64_t*)(a.ws_ml + r * 2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          ov[u][v] = __builtin_bit_cast(
-              f32x4, __builtin_amdgcn_raw_buffer_load_b128(wsr, (uint32_t)((r * D + d) * 4), 0, kCoherentPolicy));
+          ml[u][v] = ex.load_ml(r);
+          ov[u][v] = ex.load4((uint32_t)((r * D + d) * 4));
         } else {
-          ml[u][v] = (uint64_t)__float_as_uint(NEG_INF);
+          ml[u][v] = u32x2{__float_as_uint(NEG_INF), 0u};
           ov[u][v] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
       }
@@ -829,7 +846,7 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
     for (int u = 0; u < MCU; ++u)
 #pragma unroll
       for (int v = 0; v < MV; ++v) {
-        const float mc = __uint_as_float((uint32_t)ml[u][v]), lc = __uint_as_float((uint32_t)(ml[u][v] >> 32));
+        const float mc = __uint_as_float(ml[u][v].x), lc = __uint_as_float(ml[u][v].y);
         const float nm = fmaxf(M[v], mc);
         const float base = nm == NEG_INF ? 0.f : nm;
         const float al = exp2_fast(M[v] - base), be = mc == NEG_INF ? 0.f : exp2_fast(mc - base);
@@ -891,7 +908,7 @@ __device__ __forceinline__ bool reached(const int32_t* ctr, int32_t target) {
 
 // Merge block of (slot s, KV head g): wait until the prefix chunks of its
 // prompt and its own response chunks have all arrived (bounded), then merge.
-template <class SH>
+template <class SH, bool L2>
 __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag, float* smem) {
   if (threadIdx.x == 0) {
     const int p = s / a.m;
@@ -915,22 +932,25 @@ __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long*
     for (int idx = threadIdx.x; idx < SH::HPK * SH::D; idx += kBlockThreads) o[idx] = __builtin_nanf("");
     return;
   }
-  merge_outputs<SH>(a, s, g, smem);
+  merge_outputs<SH, L2>(a, s, g, smem);
 }
 
-template <class SH>
+template <class SH, bool L2>
 __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, unsigned long long* flagp) {
   const int item = blockIdx.x / a.Hkv;
   const int g = blockIdx.x - item * a.Hkv;
+  if (L2 && threadIdx.x == 0 &&
+      (__builtin_amdgcn_s_getreg(kXccIdReg) & 15) != (int)((blockIdx.x + a.l2_check_shift) % a.l2_xcds))
+    __hip_atomic_store(a.status, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (item < a.n_prefix_items) {
     int p = 0;
     while (p < a.num_prompts - 1 && !(a.prompt[p].nchunks > 0 && item < a.prompt[p].item_begin + a.prompt[p].nchunks))
       ++p;
     const int c = item - a.prompt[p].item_begin;
     if constexpr (SH::MFMA)
-      prefix_mfma<SH>(a, p, c, g, smem);
+      prefix_mfma<SH, L2>(a, p, c, g, smem);
     else
-      prefix_wave<SH>(a, p, c, g, smem);
+      prefix_wave<SH, L2>(a, p, c, g, smem);
     arrive(prefix_counter(a, p, g));
     return;
   }
@@ -945,7 +965,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     const int s = __ffsll((long long)__ballot(hit)) - 1;
     if (s < 0) return;  // unreachable with a consistent plan
     const int c = it - a.slot[s].item_begin;
-    suffix_chunk<SH>(a, s, c, g, smem);
+    suffix_chunk<SH, L2>(a, s, c, g, smem);
     arrive(suffix_counter(a, s, g));
     return;
   }
@@ -957,12 +977,14 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     return;
   }
   it -= a.n_zero_items;
-  merge_block<SH>(a, a.live_slot[it], g, flagp, smem);
+  merge_block<SH, L2>(a, a.live_slot[it], g, flagp, smem);
 }
 
-// Timing mode (a.clock_start != null): every block folds its start and end
-// time (device wall clock) into one of this launch's start / end slots.
-template <class SH>
+// One kernel per shape and exchange policy (L2: partials through the XCD's
+// L2; the host launches the one that matches StepArgs::l2_xcds).  Timing mode
+// (a.clock_start != null): every block folds its start and end time (device
+// wall clock) into one of this launch's start / end slots.
+template <class SH, bool L2>
 __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(const StepArgs a) {
   constexpr int SMEM = SH::SMEM > MergeShape<SH>::SMEM ? SH::SMEM : MergeShape<SH>::SMEM;
   __shared__ __attribute__((aligned(16))) float smem[SMEM];
@@ -971,7 +993,7 @@ __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void decode_kernel(co
   if (a.clock_start && threadIdx.x == 0)
     __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-  decode_block<SH>(a, smem, &flag);
+  decode_block<SH, L2>(a, smem, &flag);
   if (a.clock_start) {
     __syncthreads();
     if (threadIdx.x == 0)

@@ -39,7 +39,7 @@ hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, h
 // (inst_*.hip) so that they compile in parallel.
 struct KernelEntry {
   KernelKey key;
-  void (*decode)(const StepArgs);
+  void (*decode[2])(const StepArgs);  // [0]: partials through the coherence point, [1]: through the XCD's L2
 };
 struct KernelTable {
   const KernelEntry* entries;
@@ -51,6 +51,9 @@ KernelTable kernels_mfma_d128a();  // bf16, head_dim 128, hpk 1 and 2
 KernelTable kernels_mfma_d128b();  // bf16, head_dim 128, hpk 4 and 8
 KernelTable kernels_kv8a();        // E4M3 K/V, head_dim 128, hpk 1 and 2
 KernelTable kernels_kv8b();        // E4M3 K/V, head_dim 128, hpk 4 and 8
+
+// Record the XCD each of `blocks` work-groups runs on: out[b] = XCC id of work-group b.
+hipError_t launch_xcd_probe(int32_t* out, int blocks, hipStream_t stream);
 
 // Copy one prompt's K/V [plen, Hkv, D] into the shared-prefix store (layout chosen by key).
 hipError_t launch_prefill(const KernelKey& key, void* prefix_layer, const void* k, const void* v,

@@ -51,7 +51,7 @@ int64_t prefix_elems_per_head(const KernelKey& key, int pmax_padded) {
 hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream) {
   const KernelEntry* e = find_entry(key);
   if (!e) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(e->decode, dim3(grid), dim3(kBlockThreads), 0, stream, args);
+  hipLaunchKernelGGL(e->decode[args.l2_xcds > 0 ? 1 : 0], dim3(grid), dim3(kBlockThreads), 0, stream, args);
   return hipGetLastError();
 }
 
@@ -66,6 +66,17 @@ hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, h
                          (const char*)k, (const char*)v, prompt, plen, hkv, pmax);                     \
     return hipGetLastError();                                                                          \
   }
+
+namespace {
+__global__ __launch_bounds__(64) void xcd_probe_kernel(int32_t* out) {
+  if (threadIdx.x == 0) out[blockIdx.x] = __builtin_amdgcn_s_getreg(kXccIdReg) & 15;
+}
+}  // namespace
+
+hipError_t launch_xcd_probe(int32_t* out, int blocks, hipStream_t stream) {
+  hipLaunchKernelGGL(xcd_probe_kernel, dim3(blocks), dim3(64), 0, stream, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_prefill(const KernelKey& key, void* store, const void* k, const void* v, int prompt, int plen,
                           int hkv, int pmax, hipStream_t stream) {

@@ -63,7 +63,8 @@ struct StepArgs {
                        // then [S][Hkv] response chunks.  They only grow (wrapping); each launch
                        // carries the values they reach once its producers have all arrived.
   int32_t* tokens;     // [num_prompts, G] per-sample token counters
-  int32_t* status;     // device status word: nonzero after a merge wait hit its bound
+  int32_t* status;     // device status word: 1 after a merge wait hit its bound, 2 after a work-group
+                       // of an XCD-local exchange ran on another XCD than planned
   // Timing mode (else null): kClockSlots start/end slots of this launch,
   // kClockStride apart; block b folds its start into the minimum of slot
   // b % kClockSlots and its end into the maximum of that slot (spread over
@@ -81,6 +82,10 @@ struct StepArgs {
   int32_t count_tokens;       // 1 on layer 0
   float scale_log2;           // softmax scale * log2(e)
   uint32_t ws_o_bytes;        // size of ws_o (below 2^31)
+  uint32_t ws_ml_bytes;       // size of ws_ml
+  int32_t l2_xcds;            // > 0: partials exchanged through the XCD's L2; work-group b runs on XCD
+                              // b % l2_xcds (0: written through to the device coherence point)
+  int32_t l2_check_shift;     // 0; 1 makes every work-group's XCD check fail (error-path tests)
   int32_t merge_polls;        // bound on a merge block's polls of its counters (kMergeSpins; < 0: none)
   // this step
   int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;

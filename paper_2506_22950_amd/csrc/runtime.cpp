@@ -50,6 +50,7 @@ struct infs_ctx {
   KernelKey key{};
   int S = 0, m = 0, G = 0, hpk = 0, D = 0, Hkv = 0, Hq = 0, L = 0, NP = 0;
   int pmax_pad = 0, split = 0, prefix_split = 0, pages_per_slot = 0, num_pages = 0, pcmax = 0, scmax = 0;
+  int l2_xcds = 0;    // > 0: work-group b was seen on XCD b % l2_xcds and Hkv is a multiple of it
   size_t es = 0;      // bytes per Q / K / V element handed over the ABI
   size_t kv_es = 0;   // bytes per stored K / V element (prefix store and pages)
   size_t prefix_layer_bytes = 0, pool_layer_bytes = 0;
@@ -381,7 +382,9 @@ infs_status check_status(infs_ctx* c) {
   int32_t st = 0;
   HIP_TRY(c, hipMemcpy(&st, c->status, sizeof st, hipMemcpyDeviceToHost));
   if (st != 0) {
-    fail(c, INFS_E_DEVICE, "a merge work-group gave up waiting for its producers; outputs are invalid");
+    fail(c, INFS_E_DEVICE, st == 2 ? "a work-group ran on another XCD than the XCD-local exchange of partials "
+                                     "assumes; outputs are invalid (infs_set_exchange(ctx, 0) avoids it)"
+                                   : "a merge work-group gave up waiting for its producers; outputs are invalid");
     c->dead = true;
     c->dead_msg = c->err;
     return INFS_E_DEVICE;
@@ -416,6 +419,29 @@ infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int gri
     ++t.used;
   }
   HIP_TRY(c, infs::launch_decode(key, a, grid, c->stream));
+  return INFS_OK;
+}
+
+// Where work-groups run: a probe launch of kProbeBlocks work-groups records
+// each one's XCD.  If work-group b ran on XCD b % n for n distinct XCDs and Hkv
+// is a multiple of n, every KV head's work-groups share one XCD (item * Hkv + g
+// is g modulo n), and partials can be exchanged through that XCD's L2.
+infs_status probe_xcds(infs_ctx* c) {
+  constexpr int kProbeBlocks = 4096;
+  c->l2_xcds = 0;
+  int32_t* d = nullptr;
+  hipError_t e = hipMalloc((void**)&d, sizeof(int32_t) * kProbeBlocks);
+  if (e != hipSuccess) return device_fail(nullptr, e, "hipMalloc(XCD probe)");
+  std::vector<int32_t> h(kProbeBlocks);
+  e = infs::launch_xcd_probe(d, kProbeBlocks, c->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+  if (e == hipSuccess) e = hipMemcpy(h.data(), d, sizeof(int32_t) * kProbeBlocks, hipMemcpyDeviceToHost);
+  (void)hipFree(d);
+  if (e != hipSuccess) return device_fail(nullptr, e, "XCD probe");
+  const int n = *std::max_element(h.begin(), h.end()) + 1;
+  bool ok = n >= 1 && c->Hkv % n == 0;
+  for (int b = 0; ok && b < kProbeBlocks; ++b) ok = h[b] == b % n;
+  if (ok) c->l2_xcds = n;
   return INFS_OK;
 }
 
@@ -563,6 +589,7 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   const float scale = k.scale > 0.f ? k.scale : 1.0f / std::sqrt((float)k.head_dim);
   a.scale_log2 = scale * 1.4426950408889634f;
   a.ws_o_bytes = (uint32_t)(c->ws_records * c->D * sizeof(float));
+  a.ws_ml_bytes = (uint32_t)(c->ws_records * 2 * sizeof(float));
   a.merge_polls = infs::kMergeSpins;
 
   if (!c->dry) {
@@ -590,6 +617,13 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       delete c;
       return st;
     }
+    st = probe_xcds(c);
+    if (st != INFS_OK) {
+      free_device(c);
+      delete c;
+      return st;
+    }
+    a.l2_xcds = c->l2_xcds;
     a.page_table = c->page_table;
     a.ws_o = c->ws_o;
     a.ws_ml = c->ws_ml;
@@ -834,6 +868,23 @@ infs_status infs_set_merge_wait(infs_ctx* c, int32_t max_polls) {
   if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "set_merge_wait while a step is open");
   c->plan.merge_polls = max_polls < 0 ? -1 : max_polls;
   return INFS_OK;
+}
+
+infs_status infs_set_exchange(infs_ctx* c, int32_t mode) {
+  CHECK_CTX(c);
+  if (mode < 0 || mode > 2) return fail(c, INFS_E_ARG, "exchange mode must be 0, 1 or 2");
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "set_exchange while a step is open");
+  if (mode > 0 && c->l2_xcds == 0)
+    return fail(c, INFS_E_STATE, "no XCD-local exchange: %s",
+                c->dry ? "dry-run context" : "work-groups of one KV head do not share an XCD on this device");
+  c->plan.l2_xcds = mode > 0 ? c->l2_xcds : 0;
+  c->plan.l2_check_shift = mode == 2 ? 1 : 0;
+  return INFS_OK;
+}
+
+int32_t infs_exchange_mode(const infs_ctx* c) {
+  if (!c) return -1;
+  return c->plan.l2_xcds == 0 ? 0 : c->plan.l2_check_shift ? 2 : 1;
 }
 
 infs_status infs_probe_state(const infs_ctx* c, int32_t prompt, int64_t sample_id, int32_t* probe_len) {

@@ -34,7 +34,7 @@ EXPORTS = (
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
-    "infs_get_kernel_info",
+    "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode",
 )
 
 
@@ -92,6 +92,8 @@ def load():
         "infs_sync": (I32, [P]),
         "infs_get_stats": (I32, [P, ctypes.POINTER(Stats)]),
         "infs_get_kernel_info": (I32, [P, ctypes.POINTER(KernelInfo)]),
+        "infs_set_exchange": (I32, [P, I32]),
+        "infs_exchange_mode": (I32, [P]),
         "infs_timing_begin": (I32, [P]),
         "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(I64)]),
@@ -259,6 +261,14 @@ class Context:
         s = Stats()
         self._call(load().infs_get_stats, ctypes.byref(s))
         return s
+
+    def set_exchange(self, mode: int):
+        """0: partials through the device coherence point; 1: through the XCD's L2
+        (the default where available); 2: as 1 with the XCD check forced to fail."""
+        self._call(load().infs_set_exchange, mode)
+
+    def exchange_mode(self) -> int:
+        return load().infs_exchange_mode(self._h)
 
     def kernel_info(self) -> dict:
         """The decode (and probe) kernel instantiation this context runs."""

@@ -371,3 +371,15 @@ def test_kernel_selection_reaches_every_instantiation(entry):
     ctx.destroy()
     for k, v in want.items():
         assert got[k] == v, (k, got)
+
+
+def test_exchange_mode_on_dry_run():
+    # A dry-run context has no device, so no XCD-local exchange of partials.
+    cfg, ctx = _dry()
+    assert ctx.exchange_mode() == 0
+    assert _code(ctx.set_exchange, 1) == infs.E_STATE
+    assert _code(ctx.set_exchange, 2) == infs.E_STATE
+    assert _code(ctx.set_exchange, 3) == infs.E_ARG
+    ctx.set_exchange(0)
+    assert ctx.exchange_mode() == 0
+    ctx.destroy()

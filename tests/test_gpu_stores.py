@@ -5,7 +5,7 @@ and the MFMA-swizzled prefix layouts and for pages written by the append."""
 import numpy as np
 import pytest
 
-from tests.gpu_harness import run_gpu_group, say
+from tests.gpu_harness import check_against_oracle, run_gpu_group, say
 from workload import Workload, get_config
 
 pytestmark = pytest.mark.gpu
@@ -160,4 +160,65 @@ def test_merge_timeout_is_reported():
         assert ei.value.status == infs.E_DEVICE
         msg = str(ei.value)
         assert msg.count("gave up waiting") == 1 and msg.count("unusable") == 1, msg
+    ctx.destroy()
+
+
+def test_exchange_modes_agree_bitwise():
+    # The XCD-local exchange of partials (the default for 8 KV heads on this
+    # device) and the exchange through the coherence point move the same
+    # values: every output agrees bit for bit, and both match the oracle.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(700,), samples_per_prompt=24,
+                                             length_dist=("lognormal", 4.0, 1.0, 1, 300), max_suffix_len=300,
+                                             pool_rows=None)
+    wl = Workload(cfg)
+    modes = {}
+
+    def seen(ctx, step, log):
+        modes.setdefault("default", ctx.exchange_mode())
+
+    _, log, _, cap_default, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, inspect=seen)
+    assert modes["default"] == 1, "8 KV heads on this device should exchange partials through the XCD's L2"
+    _, log0, _, cap0, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, exchange=0)
+    assert log == log0 and cap_default.keys() == cap0.keys()
+    for k in cap0:
+        assert np.array_equal(cap_default[k], cap0[k]), k
+    check_against_oracle(cfg, wl, log0, {k: cap0[k] for k in list(cap0)[::5]})
+
+
+def test_exchange_mode_guard():
+    # Two KV heads span several XCDs: no XCD-local exchange.  With 8 heads,
+    # mode 2 makes every work-group's XCD check fail: the next synchronising
+    # call reports E_DEVICE and the context refuses further work.
+    import torch
+    from paper_2506_22950_amd import infs
+    from paper_2506_22950_amd.group import context_for
+    from workload.staging import DeviceInputs
+    ctx = context_for(get_config("tiny_f32"), stream=torch.cuda.current_stream())
+    assert ctx.exchange_mode() == 0
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.set_exchange(1)
+    assert ei.value.status == infs.E_STATE
+    ctx.destroy()
+
+    cfg = get_config("qwen3_1p7b_l1_g32")
+    wl = Workload(cfg)
+    dev = DeviceInputs(wl)
+    ctx = context_for(cfg, stream=torch.cuda.current_stream())
+    k, v = dev.prefix(0, 0)
+    ctx.prefill_shared(0, 0, cfg.prompt_lens[0], k, v)
+    ctx.refill_slot(0, 0, 0)
+    S = cfg.num_slots
+    q = torch.zeros((S, cfg.num_q_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+    kn = torch.zeros((S, cfg.num_kv_heads, cfg.head_dim), dtype=torch.bfloat16, device="cuda")
+    o = torch.zeros((S, cfg.num_q_heads, cfg.head_dim), dtype=torch.float32, device="cuda")
+    ctx.set_exchange(2)
+    assert ctx.exchange_mode() == 2
+    ctx.decode_step(0, q, kn, kn, o)
+    ctx.end_step()
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.sync()
+    assert ei.value.status == infs.E_DEVICE and "another XCD" in str(ei.value)
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.retire_slot(0)
+    assert ei.value.status == infs.E_DEVICE
     ctx.destroy()
