@@ -887,18 +887,20 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
 }
 
 // A producer block has stored its partial: once every thread's stores have
-// completed, count one arrival on `ctr`.
-__device__ __forceinline__ void arrive(int32_t* ctr) {
+// completed, count one arrival on the counter of each live slot among slots
+// first .. first + n - 1 (lane i adds for slot first + i; n <= 64).  A
+// response chunk counts on its own slot, a prefix chunk on every live slot of
+// its prompt, so a merge waits on a single counter that no other merge polls.
+__device__ __forceinline__ void arrive(const StepArgs& a, int first, int n, int g) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
   __syncthreads();                // ... and so have every thread's
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((int)threadIdx.x < n && a.slot[first + threadIdx.x].len > 0)
+    __hip_atomic_fetch_add(a.counters + (int64_t)((first + threadIdx.x) * a.Hkv + g) * kCounterStride, 1,
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ int32_t* prefix_counter(const StepArgs& a, int p, int g) {
-  return a.counters + (int64_t)(p * a.Hkv + g) * kCounterStride;
-}
-__device__ __forceinline__ int32_t* suffix_counter(const StepArgs& a, int s, int g) {
-  return a.counters + (int64_t)((a.num_prompts + s) * a.Hkv + g) * kCounterStride;
+__device__ __forceinline__ int32_t* slot_counter(const StepArgs& a, int s, int g) {
+  return a.counters + (int64_t)(s * a.Hkv + g) * kCounterStride;
 }
 // Counters wrap: `reached` compares by the sign of the difference.
 __device__ __forceinline__ bool reached(const int32_t* ctr, int32_t target) {
@@ -907,20 +909,19 @@ __device__ __forceinline__ bool reached(const int32_t* ctr, int32_t target) {
 }
 
 // Merge block of (slot s, KV head g): wait until the prefix chunks of its
-// prompt and its own response chunks have all arrived (bounded), then merge.
+// prompt and its own response chunks have all arrived on its counter
+// (bounded), then merge.
 template <class SH, bool L2>
 __device__ void merge_block(const StepArgs& a, int s, int g, unsigned long long* flag, float* smem) {
   if (threadIdx.x == 0) {
-    const int p = s / a.m;
-    const int32_t* pc = prefix_counter(a, p, g);
-    const int32_t* sc = suffix_counter(a, s, g);
-    const int32_t pt = a.prompt[p].target, stg = a.slot[s].target;
+    const int32_t* sc = slot_counter(a, s, g);
+    const int32_t target = a.slot[s].target;
     bool ok = false;
     if (a.merge_polls >= 0) {
-      ok = reached(sc, stg) && reached(pc, pt);
+      ok = reached(sc, target);
       for (int spins = 0; !ok && spins < a.merge_polls; ++spins) {
         __builtin_amdgcn_s_sleep(2);
-        ok = reached(sc, stg) && reached(pc, pt);
+        ok = reached(sc, target);
       }
     }
     *flag = ok;
@@ -951,7 +952,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
       prefix_mfma<SH, L2>(a, p, c, g, smem);
     else
       prefix_wave<SH, L2>(a, p, c, g, smem);
-    arrive(prefix_counter(a, p, g));
+    arrive(a, p * a.m, a.m, g);
     return;
   }
   int it = item - a.n_prefix_items;
@@ -966,7 +967,7 @@ __device__ __forceinline__ void decode_block(const StepArgs& a, float* smem, uns
     if (s < 0) return;  // unreachable with a consistent plan
     const int c = it - a.slot[s].item_begin;
     suffix_chunk<SH, L2>(a, s, c, g, smem);
-    arrive(suffix_counter(a, s, g));
+    arrive(a, s, 1, g);
     return;
   }
   it -= a.n_suffix_items;

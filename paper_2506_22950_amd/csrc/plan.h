@@ -35,7 +35,8 @@ struct SlotPlan {
   int32_t item_begin;  // first response-chunk item of this slot
   int32_t cur_page;    // page holding position len-1 (where this step's K/V go)
   int32_t sample;      // sample id (token counters)
-  int32_t target;      // response-arrival counter value once this launch's chunks of the slot arrived
+  int32_t target;      // slot counter value once this launch's producers for the slot (its response
+                       // chunks and its prompt's prefix chunks) have all arrived
   int32_t seq;         // page-table row of the sample's response (a sequence handle)
   int32_t pad_[2];
 };
@@ -44,7 +45,7 @@ struct PromptPlan {
   int32_t plen;        // prefix length
   int32_t nchunks;     // prefix chunks this step (0 when the prompt has no live slot)
   int32_t item_begin;  // first prefix item
-  int32_t target;      // prefix-arrival counter value once this launch's prefix chunks arrived
+  int32_t pad_;
 };
 
 struct StepArgs {
@@ -59,9 +60,10 @@ struct StepArgs {
   int32_t* page_table; // [sequence handles][pages_per_slot]
   float* ws_o;         // partial outputs   [..., d]
   float* ws_ml;        // partial (max, sum) [..., 2]
-  int32_t* counters;   // arrival counters, kCounterStride apart: [num_prompts][Hkv] prefix chunks,
-                       // then [S][Hkv] response chunks.  They only grow (wrapping); each launch
-                       // carries the values they reach once its producers have all arrived.
+  int32_t* counters;   // arrival counters [S][Hkv], kCounterStride apart: a prefix chunk counts on every
+                       // live slot of its prompt, a response chunk on its own slot.  They only grow
+                       // (wrapping); each launch carries the values they reach once its producers
+                       // have all arrived.
   int32_t* tokens;     // [num_prompts, G] per-sample token counters
   int32_t* status;     // device status word: 1 after a merge wait hit its bound, 2 after a work-group
                        // of an XCD-local exchange ran on another XCD than planned

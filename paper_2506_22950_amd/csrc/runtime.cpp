@@ -78,9 +78,9 @@ struct infs_ctx {
   std::vector<std::vector<int32_t>> seq_pages;     // host copy of each handle's page list
   std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_pages;
   std::vector<std::vector<uint8_t>> dispatched;    // [prompt][G]
-  // Arrivals each device counter has been sent so far (the same for every KV
-  // head): prefix counters per prompt, response counters per slot.
-  std::vector<uint32_t> prefix_arrivals, suffix_arrivals;
+  // Arrivals each slot's device counter has been sent so far (the same for
+  // every KV head): its response chunks and its prompt's prefix chunks.
+  std::vector<uint32_t> slot_arrivals;
   bool step_open = false;
   // Probe phase of prefix reuse.
   int probe_k = 0;                                 // probe tokens per sample (0: no prefix reuse)
@@ -95,8 +95,7 @@ struct infs_ctx {
   StepArgs pplan{};
   int pgrid = 0;
   double pstep_bytes = 0, pstep_flops = 0;
-  uint32_t probe_prefix_arrivals = 0;
-  std::vector<uint32_t> probe_suffix_arrivals;
+  std::vector<uint32_t> probe_slot_arrivals;
   std::vector<uint8_t> layer_done;
   int layers_done = 0;
   StepArgs plan{};
@@ -160,10 +159,10 @@ void free_device(infs_ctx* c) {
   (void)hipFree(c->status);
 }
 
-// Counters: decode prefix [NP][Hkv], decode response [S][Hkv], then the probe
-// launches' own prefix [1][Hkv] and response [kMaxSlots][Hkv] counters.
+// Counters: one per (slot, KV head) for decode launches [S][Hkv], then the
+// probe launches' own [kMaxSlots][Hkv].
 size_t counter_bytes(const infs_ctx* c) {
-  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->NP + c->S + 1 + infs::kMaxSlots) * c->Hkv;
+  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->S + infs::kMaxSlots) * c->Hkv;
 }
 
 void reset_host(infs_ctx* c) {
@@ -176,15 +175,13 @@ void reset_host(infs_ctx* c) {
   c->free_pages = {};
   for (int i = 0; i < c->num_pages; ++i) c->free_pages.push(i);
   c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
-  c->prefix_arrivals.assign(c->NP, 0);
-  c->suffix_arrivals.assign(c->S, 0);
+  c->slot_arrivals.assign(c->S, 0);
   c->step_open = false;
   c->probe_len.assign(c->probe_k > 0 ? c->NP : 0, std::vector<int32_t>(c->G, 0));
   c->probe_open = false;
   c->probe_layer_done.assign(c->L, 0);
   c->probe_layers_done = 0;
-  c->probe_prefix_arrivals = 0;
-  c->probe_suffix_arrivals.assign(infs::kMaxSlots, 0);
+  c->probe_slot_arrivals.assign(infs::kMaxSlots, 0);
   c->layer_done.assign(c->L, 0);
   c->layers_done = 0;
   c->stats = infs_stats{};
@@ -395,13 +392,10 @@ infs_status check_status(infs_ctx* c) {
 // Advance the arrival targets by this launch's producers.
 void set_targets(infs_ctx* c) {
   StepArgs& a = c->plan;
-  for (int p = 0; p < c->NP; ++p) {
-    c->prefix_arrivals[p] += (uint32_t)a.prompt[p].nchunks;
-    a.prompt[p].target = (int32_t)c->prefix_arrivals[p];
-  }
   for (int s = 0; s < c->S; ++s) {
-    if (a.slot[s].len > 0) c->suffix_arrivals[s] += (uint32_t)ceil_div(a.slot[s].len, c->split);
-    a.slot[s].target = (int32_t)c->suffix_arrivals[s];
+    if (a.slot[s].len > 0)
+      c->slot_arrivals[s] += (uint32_t)(ceil_div(a.slot[s].len, c->split) + a.prompt[s / c->m].nchunks);
+    a.slot[s].target = (int32_t)c->slot_arrivals[s];
   }
 }
 
@@ -828,13 +822,12 @@ infs_status infs_probe_step(infs_ctx* c, int32_t layer, int32_t prompt, int32_t 
                (size_t)prompt * c->Hkv * infs::prefix_elems_per_head(c->key, c->pmax_pad) * c->kv_es;
     a.pool = c->pool + c->pool_layer_bytes * layer;
     a.tokens = c->tokens + (size_t)prompt * c->G;
-    a.counters = c->counters + (size_t)(c->NP + c->S) * c->Hkv * infs::kCounterStride;
+    a.counters = c->counters + (size_t)c->S * c->Hkv * infs::kCounterStride;
     a.count_tokens = layer == 0;
-    c->probe_prefix_arrivals += (uint32_t)a.prompt[0].nchunks;
-    a.prompt[0].target = (int32_t)c->probe_prefix_arrivals;
     for (int j = 0; j < n; ++j) {
-      if (a.slot[j].len > 0) c->probe_suffix_arrivals[j] += (uint32_t)ceil_div(a.slot[j].len, c->split);
-      a.slot[j].target = (int32_t)c->probe_suffix_arrivals[j];
+      if (a.slot[j].len > 0)
+        c->probe_slot_arrivals[j] += (uint32_t)(ceil_div(a.slot[j].len, c->split) + a.prompt[0].nchunks);
+      a.slot[j].target = (int32_t)c->probe_slot_arrivals[j];
     }
     infs_status st = timed_launch(c, c->pkey, a, c->pgrid);
     if (st != INFS_OK) return st;
