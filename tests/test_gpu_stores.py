@@ -163,26 +163,38 @@ def test_merge_timeout_is_reported():
     ctx.destroy()
 
 
-def test_exchange_modes_agree_bitwise():
+@pytest.mark.parametrize("case", ["bf16", "reuse", "fp8"])
+def test_exchange_modes_agree_bitwise(case):
     # The XCD-local exchange of partials (the default for 8 KV heads on this
     # device) and the exchange through the coherence point move the same
-    # values: every output agrees bit for bit, and both match the oracle.
+    # values: every output agrees bit for bit (decode, probe launches, E4M3
+    # cache), and the outputs match the oracle.
     cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(700,), samples_per_prompt=24,
                                              length_dist=("lognormal", 4.0, 1.0, 1, 300), max_suffix_len=300,
                                              pool_rows=None)
+    reuse = 8 if case == "reuse" else 0
+    kv8 = case == "fp8"
     wl = Workload(cfg)
     modes = {}
 
     def seen(ctx, step, log):
         modes.setdefault("default", ctx.exchange_mode())
 
-    _, log, _, cap_default, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, inspect=seen)
+    runs = []
+    for exchange in (None, 0):
+        probe = {} if reuse else None
+        _, log, _, cap, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, inspect=seen, exchange=exchange,
+                                             reuse=reuse, probe=probe, kv_fp8=kv8)
+        runs.append((log, cap, probe))
     assert modes["default"] == 1, "8 KV heads on this device should exchange partials through the XCD's L2"
-    _, log0, _, cap0, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, exchange=0)
-    assert log == log0 and cap_default.keys() == cap0.keys()
+    (log1, cap1, pr1), (log0, cap0, pr0) = runs
+    assert log1 == log0 and cap1.keys() == cap0.keys()
     for k in cap0:
-        assert np.array_equal(cap_default[k], cap0[k]), k
-    check_against_oracle(cfg, wl, log0, {k: cap0[k] for k in list(cap0)[::5]})
+        assert np.array_equal(cap1[k], cap0[k]), k
+    if reuse:
+        for j in pr0["captured"]:
+            assert np.array_equal(pr1["captured"][j], pr0["captured"][j]), j
+    check_against_oracle(cfg, wl, log0, {k: cap0[k] for k in list(cap0)[::5]}, kv_fp8=kv8)
 
 
 def test_exchange_mode_guard():
