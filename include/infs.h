@@ -146,8 +146,10 @@ int32_t infs_abi_version(void);
 
 /* Create a context: validates cfg, allocates the prefix store, the response page pool, the slot
    table and the split-K workspace on the current HIP device (all zero-initialised), and records
-   `hip_stream` (a hipStream_t; NULL = default stream) for all later work.  On failure *out is NULL
-   and infs_last_error(NULL) describes why. */
+   `hip_stream` (a hipStream_t; NULL = default stream) for all later work.  E_ARG also when a derived
+   size leaves its index range: the page table or the split-K output workspace at 2 GiB or more (the
+   workspace is addressed with 32-bit offsets), or a page pool beyond INT32_MAX pages.  On failure *out
+   is NULL and infs_last_error(NULL) describes why. */
 infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out);
 
 /* Free everything infs_create allocated.  Waits for the context's stream first.  NULL is a no-op. */

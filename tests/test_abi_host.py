@@ -188,7 +188,11 @@ def test_create_validation():
     bad = [dict(num_q_heads=3), dict(head_dim=96), dict(num_prompts=0), dict(num_prompts=17),
            dict(slots_per_prompt=65), dict(samples_per_prompt=0), dict(max_suffix_len=0), dict(page_tokens=32),
            dict(split_tokens=100), dict(dtype=7), dict(scale=-1.0), dict(flags=2), dict(num_layers=0),
-           dict(slots_per_prompt=16)]   # fp32 with 32 prefix rows: no kernel
+           dict(slots_per_prompt=16),   # fp32 with 32 prefix rows: no kernel
+           # page table of 2^20 probe sequences x 512 pages = 2 GiB
+           dict(samples_per_prompt=1 << 20, probe_tokens=1, max_suffix_len=1 << 13),
+           # split-K workspace: 4 slots x 16 chunks x 2^16 KV heads x 2 rows x 64 floats, plus the prefix: > 2 GiB
+           dict(num_q_heads=1 << 17, num_kv_heads=1 << 16, max_suffix_len=4096)]
     for b in bad:
         with pytest.raises(infs.InfsError) as ei:
             infs.Context(infs.make_config(**{**base, **b}))
