@@ -234,12 +234,18 @@ __device__ __forceinline__ uint2 narrow_e4m3(const u32x4& v) {  // 8 bf16 -> 8 E
   return uint2{narrow4_e4m3(v.x, v.y), narrow4_e4m3(v.z, v.w)};
 }
 // One lane's EPL stored elements as a 16-byte register of the compute type.
+// Load one lane's EPL stored elements, widened to the compute type.  Each K/V
+// byte is read once per launch: the loads are non-temporal, so the stream of
+// K/V lines through the XCD's L2 does not push out the split-K partials that
+// the merges read back from there.
 template <class SH>
 __device__ __forceinline__ u32x4 ld_kv(const char* p) {
-  if constexpr (SH::KV8)
-    return widen_e4m3(*(const uint2*)p);
-  else
-    return *(const u32x4*)p;
+  if constexpr (SH::KV8) {
+    const u32x2 w = __builtin_nontemporal_load((const u32x2*)p);
+    return widen_e4m3(uint2{w.x, w.y});
+  } else {
+    return __builtin_nontemporal_load((const u32x4*)p);
+  }
 }
 // Store one lane's EPL elements (given in the compute type) into a stored row.
 template <class SH>
