@@ -234,17 +234,25 @@ __device__ __forceinline__ uint2 narrow_e4m3(const u32x4& v) {  // 8 bf16 -> 8 E
   return uint2{narrow4_e4m3(v.x, v.y), narrow4_e4m3(v.z, v.w)};
 }
 // One lane's EPL stored elements as a 16-byte register of the compute type.
-// Load one lane's EPL stored elements, widened to the compute type.  Each K/V
-// byte is read once per launch: the loads are non-temporal, so the stream of
-// K/V lines through the XCD's L2 does not push out the split-K partials that
-// the merges read back from there.
-template <class SH>
+// Load one lane's EPL stored elements, widened to the compute type.  Every
+// K/V byte is read once per launch.  Response K/V (NT) is loaded
+// non-temporal, so its stream through the XCD's L2 does not push out the
+// split-K partials that the merges read back from there; the shared prefix,
+// a fifth of the bytes and read again by every step, keeps the default policy
+// (measured slightly faster than non-temporal).
+template <class SH, bool NT>
 __device__ __forceinline__ u32x4 ld_kv(const char* p) {
   if constexpr (SH::KV8) {
-    const u32x2 w = __builtin_nontemporal_load((const u32x2*)p);
+    u32x2 w;
+    if constexpr (NT)
+      w = __builtin_nontemporal_load((const u32x2*)p);
+    else
+      w = *(const u32x2*)p;
     return widen_e4m3(uint2{w.x, w.y});
-  } else {
+  } else if constexpr (NT) {
     return __builtin_nontemporal_load((const u32x4*)p);
+  } else {
+    return *(const u32x4*)p;
   }
 }
 // Store one lane's EPL elements (given in the compute type) into a stored row.
@@ -318,7 +326,7 @@ __device__ __forceinline__ void wave_partial(const Addr& ad, int t0, int t1, con
 #pragma unroll
         for (int u = b * SB; u < b * SB + SB; ++u) {
           u32x4& dst = kind ? vv[u] : kk[u];
-          dst = ld_kv<SH>(ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1));
+          dst = ld_kv<SH, Addr::kNonTemporal>(ad.row(kind, base + u * TPI, base - t0 + u * TPI, pg[(u * TPI) >> 4], t1));
         }
     }
 #pragma unroll
@@ -462,6 +470,7 @@ __device__ __forceinline__ void block_store_partial(float* smem, const float (&m
 // tokens still read inside this head's region.
 template <class SH>
 struct PrefixAddr {
+  static constexpr bool kNonTemporal = false;
   const char* base[2];
   __device__ int page(int) const { return 0; }
   __device__ const char* row(int kind, int tokbase, int, int, int end) const {
@@ -477,6 +486,7 @@ struct PrefixAddr {
 // (page base) + (token in page) * KROWB + lane * LANEB -- uniform plus lane offset.
 template <class SH>
 struct SuffixAddr {
+  static constexpr bool kNonTemporal = true;
   const char* pool;
   int pages;
   int hkv, g;
@@ -631,13 +641,13 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
-        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
+        ka[mb][kb] = __builtin_bit_cast(bf16x8, ld_kv<SH, false>(kblk + ((mb * KB + kb) * 64 + lane) * 8 * SH::KES));
   };
   auto fetch_v = [&](int b, bf16x8 (&va)[DB]) {
     const char* vblk = head + (int64_t)((t0 + b * kMfmaBlock) / kMfmaBlock) * (2 * kMfmaBlock * D * SH::KES) +
                        kMfmaBlock * D * SH::KES;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH>(vblk + (db * 64 + lane) * 8 * SH::KES));
+    for (int db = 0; db < DB; ++db) va[db] = __builtin_bit_cast(bf16x8, ld_kv<SH, false>(vblk + (db * 64 + lane) * 8 * SH::KES));
   };
   // With two tiles per wavefront the accumulators leave room to prefetch only
   // the next block's K; its V is fetched once the current block is done.
