@@ -527,7 +527,7 @@ __device__ void prefix_wave(const StepArgs& a, int p, int c, int g, float* smem)
   float m[PR], l[PR], o[PR][SH::EPL];
   wave_partial<SH, PR>(ad, wt0, wt1, q, a.scale_log2, m, l, o);
   wave_combine_groups<SH, PR>(m, l, o);
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * PR;
+  const int64_t rec0 = (((int64_t)p * a.Hkv + g) * a.prefix_chunks_max + c) * PR;
   block_store_partial<SH, PR, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
 }
 
@@ -683,7 +683,7 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
     lrow[nb] += __shfl_xor(lrow[nb], 16);
     lrow[nb] += __shfl_xor(lrow[nb], 32);
   }
-  const int64_t rec0 = (((int64_t)p * a.prefix_chunks_max + c) * a.Hkv + g) * SH::PR;
+  const int64_t rec0 = (((int64_t)p * a.Hkv + g) * a.prefix_chunks_max + c) * SH::PR;
   const Exchange<L2> ex(a);
   if constexpr (TG == 1) {
 #pragma unroll
@@ -785,7 +785,7 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
     }
   }
   wave_combine_groups<SH, HPK>(m, l, o);
-  const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.suffix_chunks_max + c) * a.Hkv + g) * HPK;
+  const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.Hkv + g) * a.suffix_chunks_max + c) * HPK;
   block_store_partial<SH, HPK, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
 
   if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
@@ -824,10 +824,10 @@ __device__ void merge_outputs(const StepArgs& a, int s, int g, float* smem) {
   const int p = s / a.m, si = s - p * a.m;
   const int nP = a.prompt[p].nchunks;
   const int n = nP + (a.slot[s].len + a.split - 1) / a.split;
-  const int64_t pbase = ((int64_t)p * a.prefix_chunks_max * a.Hkv + g) * SH::PR + si * HPK;
-  const int64_t pstride = (int64_t)a.Hkv * SH::PR;
-  const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.suffix_chunks_max * a.Hkv + g) * HPK;
-  const int64_t sstride = (int64_t)a.Hkv * HPK;
+  const int64_t pbase = ((int64_t)p * a.Hkv + g) * a.prefix_chunks_max * SH::PR + si * HPK;
+  const int64_t pstride = SH::PR;
+  const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.Hkv + g) * a.suffix_chunks_max * HPK;
+  const int64_t sstride = HPK;
   auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + c * pstride : sbase + (c - nP) * sstride) + j; };
   const Exchange<L2> ex(a);
 

@@ -20,6 +20,7 @@ constexpr int kMaxSplit = 4096;    // split-K chunk length limit (a wavefront co
 
 constexpr int kMergeSpins = 1 << 20;   // bound on a merge block's wait for its producers
 constexpr int kCounterStride = 32;     // int32 per arrival counter: each counter has a 128-byte line of its own
+constexpr int kRecordsPerLine = 16;   // (max, sum) records of 8 bytes per 128-byte line
 constexpr int kClockSlots = 16;        // timing slots per launch (see StepArgs::clock_start)
 constexpr int kClockStride = 16;       // uint64 per timing slot: one 128-byte line each
 

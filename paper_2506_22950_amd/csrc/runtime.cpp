@@ -165,6 +165,21 @@ size_t counter_bytes(const infs_ctx* c) {
   return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->S + infs::kMaxSlots) * c->Hkv;
 }
 
+// Split-K record capacities.  Records are numbered (prompt, KV head)-major for
+// prefix chunks and (slot, KV head)-major for response chunks, so padding the
+// chunks per (prompt | slot, KV head) to fill whole 128-byte lines of (max,
+// sum) records gives every line to one KV head: in the XCD-local exchange no
+// two XCDs then write the same line.
+int lines_of_records(int chunks, int rows) {
+  const int per_line = std::max(1, infs::kRecordsPerLine / rows);
+  return (chunks + per_line - 1) / per_line * per_line;
+}
+int prefix_chunk_capacity(const infs::KernelKey& key, const infs::KernelKey* probe_key, int chunks) {
+  const int rows = probe_key ? std::min(key.prefix_rows, probe_key->prefix_rows) : key.prefix_rows;
+  return lines_of_records(chunks, rows);
+}
+int response_chunk_capacity(const infs::KernelKey& key, int chunks) { return lines_of_records(chunks, key.hpk); }
+
 void reset_host(infs_ctx* c) {
   c->plen.assign(c->NP, -1);
   c->prefilled.assign(c->NP, std::vector<uint8_t>(c->L, 0));
@@ -507,7 +522,9 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       return fail(nullptr, INFS_E_ARG,
                   "max_prompt_len and max_suffix_len need %d split-K chunks per slot (limit %d): raise split_tokens",
                   parts, infs::kMaxPartials);
-    const int pcm = std::max(1, (k.max_prompt_len + psplit - 1) / psplit), scm = (k.max_suffix_len + split - 1) / split;
+    const int pcm = prefix_chunk_capacity(key, k.probe_tokens > 0 ? &pkey : nullptr,
+                                          std::max(1, (k.max_prompt_len + psplit - 1) / psplit));
+    const int scm = response_chunk_capacity(key, (k.max_suffix_len + split - 1) / split);
     int64_t recs = infs::workspace_records(key, k.num_prompts, k.num_kv_heads, pcm, k.num_prompts * k.slots_per_prompt, scm);
     if (k.probe_tokens > 0)
       recs = std::max(recs, infs::workspace_records(pkey, 1, k.num_kv_heads, pcm, probe_batch, scm));
@@ -556,8 +573,9 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     c->num_pages = (int)pages;
   }
   c->prefix_split = key.mfma ? infs::kMfmaPrefixSplit : c->split;
-  c->pcmax = std::max(1, ceil_div(k.max_prompt_len, c->prefix_split));
-  c->scmax = ceil_div(k.max_suffix_len, c->split);
+  c->pcmax = prefix_chunk_capacity(key, c->probe_k > 0 ? &pkey : nullptr,
+                                   std::max(1, ceil_div(k.max_prompt_len, c->prefix_split)));
+  c->scmax = response_chunk_capacity(key, ceil_div(k.max_suffix_len, c->split));
   c->prefix_layer_bytes = (size_t)c->NP * c->Hkv * infs::prefix_elems_per_head(key, c->pmax_pad) * c->kv_es;
   c->pool_layer_bytes = (size_t)c->num_pages * c->Hkv * 2 * infs::kPageTokens * c->D * c->kv_es;
   c->ws_records = infs::workspace_records(key, c->NP, c->Hkv, c->pcmax, c->S, c->scmax);
