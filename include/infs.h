@@ -227,6 +227,23 @@ infs_status infs_release_sample(infs_ctx* ctx, int32_t prompt, int64_t sample_id
 infs_status infs_decode_step(infs_ctx* ctx, int32_t layer, const void* q_dev, const void* k_new_dev,
                              const void* v_new_dev, float* o_dev);
 
+/* For callers that cannot allocate device memory during the decode loop (code under HIP graph capture,
+   tight serving loops, harnesses that forbid hipMalloc): infs_decode_step with the same arguments,
+   validation, state rules and results, except that the launch's split-K workspace (partial outputs and
+   (max, sum) records) and its arrival counters live in a static device array of the library
+   (INFS_STATIC_SCRATCH_BYTES per GPU, 256-byte aligned, held until the process ends; its device address
+   is looked up once per device in infs_create) instead of the context's own workspace.  The call itself
+   allocates nothing: it enqueues a small kernel that zeroes the counters it uses, then the decode launch.
+   E_CAPACITY (before anything is enqueued) if the context's workspace and counters, laid out as
+   counters [S][Hkv] x 128 bytes, then (max, sum) records, then partial outputs (each part 256-byte
+   aligned), exceed INFS_STATIC_SCRATCH_BYTES.  Every call on one GPU shares that GPU's array and it keeps
+   the last call's contents: calls whose stream work overlaps on one GPU (two streams, two threads, two
+   contexts) race and give invalid outputs; order them on one stream.  Mixing it with infs_decode_step
+   layer by layer within a step is allowed. */
+#define INFS_STATIC_SCRATCH_BYTES (16u << 20)
+infs_status infs_decode_step_static(infs_ctx* ctx, int32_t layer, const void* q_dev, const void* k_new_dev,
+                                    const void* v_new_dev, float* o_dev);
+
 /* Close the step: every live slot's length grows by one.  E_STATE unless every layer was decoded
    exactly once since the previous end_step (a step with no live slot needs no decode). */
 infs_status infs_end_step(infs_ctx* ctx);

@@ -23,7 +23,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 # Decode kernel instantiations are spread over several translation units
 # (inst_*.hip) that compile in parallel; the device code is in decode.h.
 SOURCES = ["kernels.hip", "inst_wave.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip", "inst_mfma_d128b.hip",
-           "inst_kv8a.hip", "inst_kv8b.hip", "runtime.cpp", "sched.cpp"]
+           "inst_kv8a.hip", "inst_kv8b.hip", "scratch.hip", "runtime.cpp", "sched.cpp"]
 CALIB_SOURCES = ["calib.hip"]
 
 

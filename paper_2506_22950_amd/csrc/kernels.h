@@ -55,6 +55,14 @@ KernelTable kernels_kv8b();        // E4M3 K/V, head_dim 128, hpk 4 and 8
 // Record the XCD each of `blocks` work-groups runs on: out[b] = XCC id of work-group b.
 hipError_t launch_xcd_probe(int32_t* out, int blocks, hipStream_t stream);
 
+// Device address of this GPU's static scratch array (kStaticScratchBytes,
+// 256-byte aligned), looked up with hipGetSymbolAddress on the first call for
+// the current device and kept per device.
+hipError_t static_scratch_ptr(void** out);
+
+// Zero n 32-bit words at p on `stream` (a small fill kernel).
+hipError_t launch_zero_words(uint32_t* p, int64_t n, hipStream_t stream);
+
 // Copy one prompt's K/V [plen, Hkv, D] into the shared-prefix store (layout chosen by key).
 hipError_t launch_prefill(const KernelKey& key, void* prefix_layer, const void* k, const void* v,
                           int prompt, int plen, int hkv, int max_prompt_len_padded, hipStream_t stream);

@@ -4,6 +4,7 @@
 // on the CPU and hands it over in the kernel argument block: no per-step
 // host-to-device copy is needed.  The same plan serves every layer of a step.
 #pragma once
+#include <stddef.h>
 #include <stdint.h>
 
 namespace infs {
@@ -23,6 +24,10 @@ constexpr int kCounterStride = 32;     // int32 per arrival counter: each counte
 constexpr int kRecordsPerLine = 16;   // (max, sum) records of 8 bytes per 128-byte line
 constexpr int kClockSlots = 16;        // timing slots per launch (see StepArgs::clock_start)
 constexpr int kClockStride = 16;       // uint64 per timing slot: one 128-byte line each
+// Size of the file-scope device array that holds the split-K workspace and the
+// arrival counters of infs_decode_step_static (one copy per GPU, kept until the
+// process ends).
+constexpr size_t kStaticScratchBytes = size_t(16) << 20;
 
 // Work item kinds, in grid order: prefix chunks, response chunks, idle slots,
 // then one merge item per live slot.  Grid x = item * Hkv + kv_head, so with 8

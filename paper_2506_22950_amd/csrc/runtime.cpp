@@ -22,6 +22,7 @@ using infs::KernelKey;
 using infs::StepArgs;
 
 static_assert(sizeof(StepArgs) <= 4096, "kernel argument block must fit 4 KiB");
+static_assert(INFS_STATIC_SCRATCH_BYTES == infs::kStaticScratchBytes, "static scratch size: header and library agree");
 
 namespace {
 thread_local std::string g_thread_error = "no error";
@@ -64,6 +65,7 @@ struct infs_ctx {
   int32_t* counters = nullptr;
   int32_t* tokens = nullptr;
   int32_t* status = nullptr;
+  void* scratch = nullptr;  // this device's static scratch array (infs_decode_step_static)
   // host state
   std::vector<int32_t> plen;                       // per prompt, -1 before its first prefill
   std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
@@ -431,6 +433,26 @@ infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int gri
   return INFS_OK;
 }
 
+// Layout of a decode launch's split-K exchange in the static scratch array:
+// the arrival counters [S][Hkv] (one 128-byte line each), then the (max, sum)
+// records, then the partial outputs, each part 256-byte aligned.  Returns the
+// bytes needed.
+struct StaticLayout {
+  size_t counters = 0, ml = 0, o = 0, ml_bytes = 0, o_bytes = 0, total = 0;
+};
+StaticLayout static_layout(const infs_ctx* c) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  StaticLayout s;
+  const int64_t recs = infs::workspace_records(c->key, c->NP, c->Hkv, c->pcmax, c->S, c->scmax);
+  s.counters = 0;
+  s.ml = up(sizeof(int32_t) * infs::kCounterStride * (size_t)c->S * c->Hkv);
+  s.ml_bytes = sizeof(float) * 2 * (size_t)recs;
+  s.o = s.ml + up(s.ml_bytes);
+  s.o_bytes = sizeof(float) * (size_t)c->D * recs;
+  s.total = s.o + up(s.o_bytes);
+  return s;
+}
+
 // Where work-groups run: a probe launch of kProbeBlocks work-groups records
 // each one's XCD.  If work-group b ran on XCD b % n for n distinct XCDs and Hkv
 // is a multiple of n, every KV head's work-groups share one XCD (item * Hkv + g
@@ -635,6 +657,12 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       delete c;
       return st;
     }
+    const hipError_t se = infs::static_scratch_ptr(&c->scratch);
+    if (se != hipSuccess) {
+      free_device(c);
+      delete c;
+      return device_fail(nullptr, se, "hipGetSymbolAddress(static scratch)");
+    }
     a.l2_xcds = c->l2_xcds;
     a.page_table = c->page_table;
     a.ws_o = c->ws_o;
@@ -745,13 +773,27 @@ infs_status infs_release_sample(infs_ctx* c, int32_t prompt, int64_t sample_id) 
   return INFS_OK;
 }
 
-infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev,
-                             const void* v_new_dev, float* o_dev) {
+}  // extern "C"
+
+namespace {
+
+// One layer of the open (or opening) step; with `static_ws` the split-K
+// workspace and arrival counters are taken from the static scratch array.
+infs_status decode_layer(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev, const void* v_new_dev,
+                         float* o_dev, bool static_ws) {
   CHECK_CTX(c);
   if (layer < 0 || layer >= c->L) return fail(c, INFS_E_ARG, "layer %d out of range [0, %d)", layer, c->L);
   if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
   if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
     return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
+  if (static_ws) {
+    const StaticLayout sl = static_layout(c);
+    if (sl.total > infs::kStaticScratchBytes)
+      return fail(c, INFS_E_CAPACITY,
+                  "decode_step_static needs %zu bytes of static scratch for this context's split-K workspace "
+                  "(limit %zu): use infs_decode_step, or fewer slots, KV heads or split-K chunks",
+                  sl.total, infs::kStaticScratchBytes);
+  }
   if (c->probe_open) return fail(c, INFS_E_STATE, "decode_step while a probe step is open");
   if (c->step_open && c->layer_done[layer])
     return fail(c, INFS_E_STATE, "layer %d already decoded in this step", layer);
@@ -774,9 +816,29 @@ infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, cons
     a.prefix = c->prefix + c->prefix_layer_bytes * layer;
     a.pool = c->pool + c->pool_layer_bytes * layer;
     a.count_tokens = layer == 0;
-    set_targets(c);
-    infs_status st = timed_launch(c, c->key, a, c->grid);
-    if (st != INFS_OK) return st;
+    if (!static_ws) {
+      set_targets(c);
+      infs_status st = timed_launch(c, c->key, a, c->grid);
+      if (st != INFS_OK) return st;
+    } else {
+      // The counters start from zero in every call (the array keeps whatever
+      // the last call on this GPU left), so each merge waits for exactly this
+      // launch's arrivals; the context's own counters and targets are untouched.
+      const StaticLayout sl = static_layout(c);
+      char* base = (char*)c->scratch;
+      StepArgs sa = a;
+      sa.counters = (int32_t*)(base + sl.counters);
+      sa.ws_ml = (float*)(base + sl.ml);
+      sa.ws_o = (float*)(base + sl.o);
+      sa.ws_ml_bytes = (uint32_t)sl.ml_bytes;
+      sa.ws_o_bytes = (uint32_t)sl.o_bytes;
+      for (int s = 0; s < c->S; ++s)
+        sa.slot[s].target = sa.slot[s].len > 0 ? ceil_div(sa.slot[s].len, c->split) + sa.prompt[s / c->m].nchunks : 0;
+      HIP_TRY(c, infs::launch_zero_words((uint32_t*)sa.counters, (int64_t)infs::kCounterStride * c->S * c->Hkv,
+                                         c->stream));
+      infs_status st = timed_launch(c, c->key, sa, c->grid);
+      if (st != INFS_OK) return st;
+    }
   }
   c->layer_done[layer] = 1;
   ++c->layers_done;
@@ -784,6 +846,20 @@ infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, cons
   c->stats.alg_bytes += c->step_bytes;
   c->stats.alg_flops += c->step_flops;
   return INFS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+infs_status infs_decode_step(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev,
+                             const void* v_new_dev, float* o_dev) {
+  return decode_layer(c, layer, q_dev, k_new_dev, v_new_dev, o_dev, false);
+}
+
+infs_status infs_decode_step_static(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev,
+                                    const void* v_new_dev, float* o_dev) {
+  return decode_layer(c, layer, q_dev, k_new_dev, v_new_dev, o_dev, true);
 }
 
 infs_status infs_end_step(infs_ctx* c) {

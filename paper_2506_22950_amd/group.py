@@ -77,7 +77,7 @@ def probe_group(ctx: infs.Context, lengths, k: int, num_layers: int, provide: Ca
 def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_layers: int,
                  provide: Callable, after_step: Optional[Callable] = None,
                  log: Optional[list] = None, stop_after: Optional[int] = None,
-                 accepted: Optional[list] = None, reuse: int = 0) -> int:
+                 accepted: Optional[list] = None, reuse: int = 0, entry: str = "decode_step") -> int:
     """Decode every sample of every prompt; returns the number of running steps.
 
     lengths[p][i]: true length of sample i of prompt p.
@@ -93,7 +93,10 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     reuse = k: the samples went through a probe phase of k tokens (probe_group);
     a dispatched sample resumes at token k+1, and one that finished within its
     probe tokens is skipped (the scheduler is told it is done at once).
+    entry: the C call that decodes a layer -- "decode_step", or
+    "decode_step_static" (split-K workspace in the library's static scratch).
     """
+    decode = {"decode_step": ctx.decode_step, "decode_step_static": ctx.decode_step_static}[entry]
     NP = len(scheds)
     m = ctx.config.slots_per_prompt
     S = NP * m
@@ -128,7 +131,7 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
             log.append(tuple((s // m, slot_sample[s], slot_len[s] + 1) if slot_sample[s] >= 0 else None
                              for s in range(S)))
         for layer in range(num_layers):
-            ctx.decode_step(layer, *provide(step, layer))
+            decode(layer, *provide(step, layer))
         ctx.end_step()
         if after_step is not None:
             after_step(step)

@@ -25,6 +25,7 @@ POLICY = {"naive": NAIVE, "fixed_row": FIXED_ROW, "fifo": FIFO, "sjf": SJF, "fpt
 FPTAS_EPSILON = 0.1
 FLAG_DRY_RUN = 1
 FLAG_KV_FP8 = 2
+STATIC_SCRATCH_BYTES = 16 << 20
 
 # Every symbol include/infs.h declares.
 EXPORTS = (
@@ -34,7 +35,7 @@ EXPORTS = (
     "infs_last_error", "infs_sched_create", "infs_sched_next", "infs_sched_done", "infs_sched_pending",
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
-    "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode",
+    "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode", "infs_decode_step_static",
 )
 
 
@@ -86,6 +87,7 @@ def load():
         "infs_refill_slot": (I32, [P, I32, I32, I64]),
         "infs_retire_slot": (I32, [P, I32]),
         "infs_decode_step": (I32, [P, I32, P, P, P, P]),
+        "infs_decode_step_static": (I32, [P, I32, P, P, P, P]),
         "infs_end_step": (I32, [P]),
         "infs_slot_state": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I32)]),
         "infs_sample_tokens": (I32, [P, I32, ctypes.POINTER(I32), I32]),
@@ -189,6 +191,9 @@ class Context:
 
     def decode_step(self, layer, q, k_new, v_new, o):
         self._call(load().infs_decode_step, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o))
+
+    def decode_step_static(self, layer, q, k_new, v_new, o):
+        self._call(load().infs_decode_step_static, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o))
 
     def end_step(self):
         self._call(load().infs_end_step)

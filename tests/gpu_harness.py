@@ -22,13 +22,13 @@ def say(*a):
 
 
 def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
-                  probe=None, inspect=None, kv_fp8=False, exchange=None):
+                  probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step"):
     """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
     reuse first; if `probe` is a dict it receives 'log' (probe step log) and
     'captured' (the O buffer [L, batch, Hq, d] after every probe step).
     inspect(ctx, step, log) is called after every decode step; kv_fp8 stores the
     KV cache as E4M3; exchange sets the partial exchange mode (default: the
-    library's)."""
+    library's); entry names the C call that decodes each layer."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
@@ -91,7 +91,7 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
         if probe is not None:
             probe["log"], probe["captured"] = plog, pcap
     steps = decode_group(ctx, schedulers_for(cfg, policy, wl.L_hat), wl.L, L, provide, after_step=after,
-                         stop_after=stop_after, reuse=reuse)
+                         stop_after=stop_after, reuse=reuse, entry=entry)
     torch.cuda.synchronize()
     tokens = np.stack([ctx.sample_tokens(p) for p in range(cfg.num_prompts)])
     stats = ctx.get_stats()

@@ -387,3 +387,31 @@ def test_exchange_mode_on_dry_run():
     ctx.set_exchange(0)
     assert ctx.exchange_mode() == 0
     ctx.destroy()
+
+
+def test_static_entry_point_workspace_limit():
+    # infs_decode_step_static keeps the split-K workspace and counters in a
+    # static array of INFS_STATIC_SCRATCH_BYTES: the benchmark and long-tail
+    # groups fit; the four-prompt 8B-shaped group (about 68 MB of workspace) is
+    # rejected with E_CAPACITY before anything changes, and the regular entry
+    # point still decodes it.
+    for name, fits in (("qwen3_1p7b_g64", True), ("longtail_g128", True), ("qwen3_8b_4prompts", False)):
+        cfg = get_config(name)
+        ctx = context_for(cfg, dry_run=True)
+        for p in range(cfg.num_prompts):
+            for layer in range(cfg.layers):
+                ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
+        for s in range(cfg.num_slots):
+            ctx.refill_slot(s, s // cfg.slots_per_prompt, s % cfg.slots_per_prompt)
+        none4 = (None, None, None, None)
+        if fits:
+            ctx.decode_step_static(0, *none4)
+        else:
+            assert _code(ctx.decode_step_static, 0, *none4) == infs.E_CAPACITY
+            assert "static scratch" in ctx.last_error
+            assert ctx.get_stats().launches == 0
+            ctx.decode_step(0, *none4)
+        for layer in range(1, cfg.layers):
+            ctx.decode_step(layer, *none4)
+        ctx.end_step()
+        assert ctx.get_stats().launches == cfg.layers
