@@ -14,15 +14,16 @@ from . import infs
 
 
 def context_for(cfg, stream=None, dry_run=False, split_tokens=0, num_pages=0, probe_tokens=0,
-                kv_fp8=False) -> infs.Context:
-    """Create a context for a workload preset (workload.GroupConfig or alike)."""
+                kv_fp8=False, scale=0.0) -> infs.Context:
+    """Create a context for a workload preset (workload.GroupConfig or alike);
+    scale 0 is the default softmax scale 1/sqrt(head_dim)."""
     c = infs.make_config(
         num_layers=cfg.layers, num_q_heads=cfg.num_q_heads, num_kv_heads=cfg.num_kv_heads,
         head_dim=cfg.head_dim, num_prompts=cfg.num_prompts, slots_per_prompt=cfg.slots_per_prompt,
         samples_per_prompt=cfg.samples_per_prompt, max_prompt_len=max(cfg.prompt_lens),
         max_suffix_len=cfg.max_suffix_len, page_tokens=0, num_pages=num_pages,
         split_tokens=split_tokens, dtype=infs.BF16 if cfg.dtype == "bf16" else infs.F32,
-        scale=0.0, flags=(infs.FLAG_DRY_RUN if dry_run else 0) | (infs.FLAG_KV_FP8 if kv_fp8 else 0),
+        scale=scale, flags=(infs.FLAG_DRY_RUN if dry_run else 0) | (infs.FLAG_KV_FP8 if kv_fp8 else 0),
         probe_tokens=probe_tokens)
     return infs.Context(c, stream=None if dry_run else stream)
 

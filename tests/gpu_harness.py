@@ -22,13 +22,14 @@ def say(*a):
 
 
 def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
-                  probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step"):
+                  probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step", scale=0.0):
     """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
     reuse first; if `probe` is a dict it receives 'log' (probe step log) and
     'captured' (the O buffer [L, batch, Hq, d] after every probe step).
     inspect(ctx, step, log) is called after every decode step; kv_fp8 stores the
     KV cache as E4M3; exchange sets the partial exchange mode (default: the
-    library's); entry names the C call that decodes each layer."""
+    library's); entry names the C call that decodes each layer; scale is the
+    context's softmax scale (0: 1/sqrt(head_dim))."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
@@ -37,7 +38,7 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
     log = plan_steps(cfg, wl.L, policy, wl.L_hat, stop_after=stop_after, reuse=reuse, probe_log=plog)
     dev = DeviceInputs(wl)
     stream = torch.cuda.current_stream()
-    ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse, kv_fp8=kv_fp8)
+    ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse, kv_fp8=kv_fp8, scale=scale)
     if exchange is not None:
         ctx.set_exchange(exchange)
     keep = []
@@ -118,9 +119,10 @@ class _PrefixCache:
         return self._wl.query(layer, p, i, t)
 
 
-def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None, kv_fp8=False):
+def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None, kv_fp8=False, scale=None):
     """Max abs error over every captured live (step, slot, layer) output; idle rows must be 0.
-    kv_fp8: the oracle rounds keys and values to E4M3 as the FP8 cache stores them."""
+    kv_fp8: the oracle rounds keys and values to E4M3 as the FP8 cache stores them; scale: the
+    softmax scale (None: 1/sqrt(head_dim))."""
     tol = tol if tol is not None else (1e-2 if cfg.dtype == "bf16" else 1e-5)
     layers = range(cfg.layers) if layers is None else layers
     wl = _PrefixCache(wl)
@@ -133,7 +135,7 @@ def check_against_oracle(cfg, wl, log, captured, layers=None, tol=None, kv_fp8=F
                 continue
             p, i, t = e
             for layer in layers:
-                ref = attend_slot(wl, layer, p, i, t, kv_fp8=kv_fp8)
+                ref = attend_slot(wl, layer, p, i, t, scale=scale, kv_fp8=kv_fp8)
                 err = float(np.abs(o[layer, s].astype(np.float64) - ref).max())
                 assert np.isfinite(o[layer, s]).all()
                 if err > worst:

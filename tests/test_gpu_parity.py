@@ -15,16 +15,17 @@ from workload import Workload, get_config
 pytestmark = pytest.mark.gpu
 
 
-def _run_and_check(cfg, policy, capture=None, layers=None, split=0, window=1024, kv_fp8=False):
+def _run_and_check(cfg, policy, capture=None, layers=None, split=0, window=1024, kv_fp8=False, scale=0.0):
     wl = Workload(cfg)
     want_log = oracle_log(cfg, wl, policy)
     cap = capture(want_log).__contains__ if capture else (lambda k: True)
     wl, log, steps, captured, tokens, stats = run_gpu_group(cfg, policy, capture=cap, split=split,
-                                                          window=window, wl=wl, kv_fp8=kv_fp8)
+                                                          window=window, wl=wl, kv_fp8=kv_fp8, scale=scale)
     assert log == want_log, "step log differs from the oracle simulator"
     assert steps == len(want_log)
     assert np.array_equal(tokens, wl.L), "device token counters differ from the drawn lengths"
-    worst, n = check_against_oracle(cfg, wl, log, captured, layers=layers, kv_fp8=kv_fp8)
+    worst, n = check_against_oracle(cfg, wl, log, captured, layers=layers, kv_fp8=kv_fp8,
+                                    scale=scale if scale > 0 else None)
     say(f"  [{cfg.name} {policy}] checked {n} (slot, layer) outputs over {len(captured)} steps, "
         f"max abs err {worst:.3g}")
     return wl, log, captured
@@ -202,11 +203,64 @@ def test_schedule_invariance_and_determinism():
 ])
 def test_full_size_sampled(name, every, window):
     # Whole workload in the launch configuration the benchmark uses; outputs of
-    # sampled steps (and the first and last ones) on the first and last layer
-    # against the oracle.
+    # sampled steps (and the first and last ones) on the first, middle and last
+    # layer against the oracle.
     cfg = get_config(name)
     _run_and_check(cfg, cfg.policy, capture=lambda log: sample_steps(log, every=every, edge=2, refills=8),
-                   layers=(0, cfg.layers - 1), window=window)
+                   layers=(0, cfg.layers // 2, cfg.layers - 1), window=window)
+
+
+# --- softmax scale and wide score ranges ------------------------------------------------------------
+# A non-default scale reaches the kernels only through infs_config.scale; inputs
+# with Q scaled up and K rows ramped (qk_scale) make scores span two orders of
+# magnitude, with the first prefix chunk's maximum far below later chunks' and
+# the responses' (bf16 cases: about 2 against 100+, so the weight of an early
+# partial underflows to exactly 0 in the online rescale and in the merge).
+_BF16_SMALL = dict(layers=2, prompt_lens=(700,), samples_per_prompt=24,
+                   length_dist=("lognormal", 4.0, 1.0, 1, 300), max_suffix_len=300, pool_rows=None)
+
+
+@pytest.mark.parametrize("case", ["mfma32_scale1", "mfma32_wide", "mfma16_wide", "mfma64_hpk4_wide",
+                                  "wave_bf16_wide", "wave_bf16_scale1"])
+def test_bf16_scale_and_wide_scores(case):
+    wide = (8.0, 0.1, 8.0)
+    if case == "mfma32_scale1":        # 32 prefix rows on MFMA tiles, scale 1.0 at d=128
+        cfg, scale = get_config("qwen3_1p7b_g64").with_(**_BF16_SMALL), 1.0
+    elif case == "mfma32_wide":
+        cfg, scale = get_config("qwen3_1p7b_g64").with_(**_BF16_SMALL, qk_scale=wide), 0.0
+    elif case == "mfma16_wide":        # 16 rows (m=8)
+        cfg, scale = get_config("qwen3_1p7b_l1_g32").with_(prompt_lens=(600,), qk_scale=wide), 0.0
+    elif case == "mfma64_hpk4_wide":   # 4 query heads per KV head, 64 rows, two prompts
+        cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(130, 511), samples_per_prompt=20,
+                                                    length_dist=("lognormal", 4.0, 1.0, 1, 260),
+                                                    max_suffix_len=260, pool_rows=None, qk_scale=wide)
+        scale = 0.0
+    else:                              # m=1: 2 prefix rows, the bf16 wavefront path
+        cfg = get_config("qwen3_1p7b_l1_g32").with_(slots_per_prompt=1, samples_per_prompt=4, prompt_lens=(600,),
+                                                    length_dist=("lognormal", 4.0, 0.8, 1, 300), max_suffix_len=300,
+                                                    qk_scale=wide if case == "wave_bf16_wide" else None)
+        scale = 1.0 if case == "wave_bf16_scale1" else 0.0
+    _run_and_check(cfg, "fifo" if cfg.pred_sigma is None else "sjf", split=128,
+                   capture=lambda log: sample_steps(log, every=2), scale=scale)
+
+
+@pytest.mark.parametrize("case", ["scale_half", "wide"])
+def test_f32_scale_and_wide_scores(case):
+    # fp32 wavefront path at 1e-5, d=64, three prefix chunks of 128 tokens:
+    # scale 0.5 (four times the default), or Q x 4 with K rows ramped 0.1 -> 2.
+    cfg = get_config("tiny_f32").with_(prompt_lens=(300,), length_dist=("uniform", 1, 400), max_suffix_len=400)
+    if case == "wide":
+        cfg = cfg.with_(qk_scale=(4.0, 0.1, 2.0))
+    _run_and_check(cfg, "fifo", split=128, capture=lambda log: sample_steps(log, every=3),
+                   scale=0.5 if case == "scale_half" else 0.0)
+
+
+def test_bf16_fixed_row_end_to_end():
+    # Fixed-slot continuous sampling (Section 3.2, mode 1): slot s runs samples
+    # s, s+m, s+2m, ...; step log equal to the simulator's, token counters equal
+    # to the lengths, outputs against the oracle.
+    cfg = get_config("qwen3_1p7b_g64").with_(**_BF16_SMALL)
+    _run_and_check(cfg, "fixed_row", split=128, capture=lambda log: sample_steps(log, every=3))
 
 
 def test_fp8_kv_small_every_other_step():

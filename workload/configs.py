@@ -33,6 +33,12 @@ class GroupConfig:
     seed: int
     pool_rows: Optional[int] = None  # None: every (layer, prompt, sample, t) row is unique
     description: str = ""
+    # Wide score ranges: (q_scale, k_first, k_last) multiplies every Q draw by
+    # q_scale and K pool row r by a factor rising linearly from k_first (row 0)
+    # to k_last (last row), before rounding to the storage type.  Rows are laid
+    # out prefix first (token order), then responses, so later prefix chunks and
+    # the responses reach much larger scores than the first prefix chunk.
+    qk_scale: Optional[Tuple[float, float, float]] = None
 
     @property
     def num_prompts(self) -> int:

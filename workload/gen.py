@@ -132,6 +132,12 @@ class Workload:
             stream = {"q": 0, "k": 1, "v": 2}[kind]
             rng = np.random.Generator(np.random.PCG64([3000 + self.cfg.seed, stream]))
             x = rng.standard_normal(self._shape(kind), dtype=np.float32)
+            if self.cfg.qk_scale is not None:
+                q_scale, k_first, k_last = self.cfg.qk_scale
+                if kind == "q":
+                    x *= np.float32(q_scale)
+                elif kind == "k":
+                    x *= np.linspace(k_first, k_last, x.shape[0], dtype=np.float32)[:, None, None]
             self._pools[kind] = f32_to_bf16_bits(x) if self.cfg.dtype == "bf16" else x
         return self._pools[kind]
 
