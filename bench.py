@@ -273,13 +273,18 @@ def schedule_table(n_groups=64, G=32, m=4, cap=1024):
     """Running steps of the refill policies (Table 2 style) and the length bias
     of dynamic-slot sampling (Table 1 style), from the library's host scheduler
     in dry-run mode (no GPU): n_groups groups of G samples on m slots per
-    length setting; steps summed over the groups."""
+    length setting; steps summed over the groups.  The post-hoc optimum
+    (Infinite*) comes from the library's exact branch and bound
+    (infs_sched_optimum); longest-first list scheduling on the true lengths is
+    only an upper bound on it."""
     import math
 
     from paper_2506_22950_amd.group import plan_steps
     from workload import SCHEDULER_STUDY, get_config, scheduler_study_lengths, scheduler_study_stream
 
     cfg = get_config("tiny_f32").with_(layers=1, samples_per_prompt=G, slots_per_prompt=m, max_suffix_len=cap)
+    from paper_2506_22950_amd import infs
+
     rows = [("naive micro groups", "naive", "pred"), ("fixed-slot", "fixed_row", "pred"),
             ("FPTAS only", "fptas", "pred"), ("SJF only", "sjf", "pred"), ("FPTAS + SJF", "fptas_sjf", "pred"),
             ("post-hoc LPT (true lengths)", "lpt", "true")]
@@ -300,12 +305,21 @@ def schedule_table(n_groups=64, G=32, m=4, cap=1024):
             dyn_steps += len(plan_steps(dcfg, stream[n:n + 1], "fifo", None, stop_after=G, accepted=acc))
             dyn_len.extend(int(stream[n, i]) for i in acc[0])
         lb = sum(max(math.ceil(int(L[n].sum()) / m), int(L[n].max())) for n in range(n_groups))
+        opt = [infs.sched_optimum(L[n], m) for n in range(n_groups)]
+        opt_best, opt_low = sum(o[0] for o in opt), sum(o[1] for o in opt)
+        unsolved = sum(o[0] != o[1] for o in opt)
         out.append(f"\n{label}: mean length {L.mean():.0f}")
         base = tot["fixed_row"]
         for name, policy, _ in rows:
             out.append(f"  {name:30s} {tot[policy]:8d}  (x{tot[policy] / base:.2f})  mean length {L.mean():6.1f}")
         out.append(f"  {'dynamic-slot (stream, first G)':30s} {dyn_steps:8d}  (x{dyn_steps / base:.2f})  "
                    f"mean length {sum(dyn_len) / len(dyn_len):6.1f}")
+        if unsolved == 0:
+            out.append(f"  {'post-hoc optimum (Infinite*)':30s} {opt_best:8d}  (x{opt_best / base:.2f})  "
+                       f"mean length {L.mean():6.1f}  (proven for all {n_groups} groups)")
+        else:
+            out.append(f"  {'post-hoc optimum (Infinite*)':30s} {opt_low:8d}..{opt_best}  "
+                       f"({n_groups - unsolved} of {n_groups} groups proven; the rest bounded)")
         out.append(f"  {'lower bound max(sum/m, max)':30s} {lb:8d}  (x{lb / base:.2f})")
     return "\n".join(out)
 
@@ -353,6 +367,9 @@ class Bench:
         self.plog = []
         self.log = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat, reuse=reuse, probe_log=self.plog)
         self.naive_steps = len(plan_steps(cfg, wl.L, "naive", wl.L_hat, reuse=reuse))
+        # Infinite*: the post-hoc optimum of the true lengths; prompts run side by side on their own slots
+        opt = [infs.sched_optimum(wl.L[p], cfg.slots_per_prompt) for p in range(cfg.num_prompts)]
+        self.optimum_steps = max(o[0] for o in opt) if all(o[0] == o[1] for o in opt) else None
         dev = DeviceInputs(wl)
         self.prefix = [[dev.prefix(l, p) for l in range(cfg.layers)] for p in range(cfg.num_prompts)]
         per_step = cfg.layers * cfg.num_slots * (cfg.num_q_heads + 2 * cfg.num_kv_heads) * cfg.head_dim * cfg.elem_bytes
@@ -643,7 +660,8 @@ def main():
             "layers": cfg.layers, "q_heads": cfg.num_q_heads, "kv_heads": cfg.num_kv_heads,
             "head_dim": cfg.head_dim, "prompt_len": list(cfg.prompt_lens), "G": cfg.samples_per_prompt,
             "m": cfg.slots_per_prompt, "policy": cfg.policy, "decode_steps": len(b.log),
-            "naive_decode_steps": b.naive_steps, "generated_tokens": b.tokens,
+            "naive_decode_steps": b.naive_steps, "optimum_decode_steps": b.optimum_steps,
+            "generated_tokens": b.tokens,
             "alg_bytes_per_group": round(b.alg_bytes),
             "end_to_end_alg_GBps": round((b.alg_bytes + b.probe_alg_bytes) / (ms_per_step / 1e3) / 1e9, 1),
             "probe_tokens": args.reuse, "probe_steps": len(b.plog),

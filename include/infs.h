@@ -87,8 +87,9 @@ typedef enum infs_policy {
     INFS_FPTAS_SJF = 5,  /* Algorithm 1: each slot starts with position 0 of its bin, every later
                             refill is SJF (Table 2, "Infinite") */
     INFS_LPT = 6         /* continuous refill with the largest predicted length, ties to the lowest
-                            id; given the true lengths, the post-hoc list schedule that serves as
-                            the reference of Tables 1 and 2 */
+                            id; given the true lengths, a post-hoc list schedule whose step count is
+                            an upper bound on the post-hoc optimum of Tables 1 and 2 ("Infinite*",
+                            infs_sched_optimum), at most 4/3 - 1/(3m) times it (Graham 1969) */
 } infs_policy;
 
 #define INFS_FPTAS_EPSILON 0.1
@@ -352,6 +353,18 @@ void infs_sched_destroy(infs_sched* s);
    pred_len: G finite values >= 0 with a positive sum; epsilon > 0.  E_ARG otherwise. */
 infs_status infs_fptas_assign(int32_t G, int32_t N, const double* pred_len, double epsilon, int32_t* group_out,
                               int32_t* pos_out);
+
+/* The post-hoc optimum that Tables 1 and 2 compare against ("Infinite*": every response placed after
+   generation, with the fewest running steps possible; Table 1 caption, Section 5.4).  A slot runs the
+   samples it is given back to back, so a schedule's running steps are its largest per-slot sum of true
+   lengths, and the optimum is the minimum of that over all assignments of the G samples to the m slots
+   (the makespan problem P||Cmax).  Exact branch and bound, host only.
+   lengths: G true lengths >= 1.  max_nodes: search budget (>= 0; about 10^7 nodes take a second).
+   Writes *best_out (running steps of the best schedule found) and *lower_out (a proven lower bound);
+   they are equal when the optimum is proven, else the budget ran out and lower <= optimum <= best.
+   slot_out (G entries, or NULL): the slot of every sample in that best schedule.  E_ARG otherwise. */
+infs_status infs_sched_optimum(int32_t G, int32_t m, const int32_t* lengths, int64_t max_nodes, int64_t* best_out,
+                               int64_t* lower_out, int32_t* slot_out);
 
 #ifdef __cplusplus
 }

@@ -6,7 +6,7 @@ anything in this package.  The GPU library never calls it, and it shares no
 code with the GPU library: the two meet only at the seeded input generator in
 ``workload/``.
 
-Three parts, all plain and slow on purpose:
+Four parts, all plain and slow on purpose:
 
 * ``attention`` -- float64 softmax attention of a decode query over the
   concatenation of the shared prompt KV and the sample's own response KV
@@ -20,6 +20,8 @@ Three parts, all plain and slow on purpose:
   and 3), FPTAS micro-group assignment (Algorithm 2) alone or followed by
   shortest-job-first refill, longest-first list scheduling, and
   dynamic-slot sampling from an unbounded stream (Section 3.2, mode 2).
+* ``optimum`` -- the post-hoc optimum of Tables 1 and 2 ("Infinite*"): the
+  fewest running steps of any assignment of the samples to the slots.
 
 Every function is pinned by the ``-m "not gpu"`` tests against closed forms,
 a library routine, brute force and a hand-derived worked example.
@@ -27,6 +29,9 @@ a library routine, brute force and a hand-derived worked example.
 
 from .attention import attend, attend_slot, attention_weights, default_scale
 from .fp8 import E4M3_MAX, decode_e4m3, encode_e4m3, round_e4m3
+from .optimum import brute_force as optimum_brute_force
+from .optimum import lower_bound as optimum_lower_bound
+from .optimum import makespan, optimum
 from .simulator import (FPTAS_EPSILON, POLICIES, DynamicResult, SimResult, fptas_assign, simulate,
                         simulate_dynamic, simulate_group)
 
@@ -47,4 +52,8 @@ __all__ = [
     "simulate_dynamic",
     "simulate",
     "simulate_group",
+    "optimum",
+    "optimum_lower_bound",
+    "optimum_brute_force",
+    "makespan",
 ]

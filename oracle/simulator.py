@@ -26,8 +26,10 @@ Refill policies:
                    "Infinite"): every slot starts with position 0 of its bin,
                    and every later refill is shortest-job-first.
 * ``lpt``       -- continuous refill, longest predicted length first, ties to
-                   the lowest id.  Given the true lengths this is the post-hoc
-                   list schedule used as the reference of Tables 1 and 2.
+                   the lowest id.  Given the true lengths this is a post-hoc
+                   list schedule: an upper bound on the post-hoc optimum of
+                   Tables 1 and 2 ("Infinite*", ``optimum.optimum``), within
+                   4/3 - 1/(3m) of it (Graham 1969).
 
 Readings where the paper is silent: a sample of length L holds its slot for
 exactly L steps; when several slots free up in one step they are refilled in

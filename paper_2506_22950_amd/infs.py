@@ -36,6 +36,7 @@ EXPORTS = (
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
     "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode", "infs_decode_step_static",
+    "infs_sched_optimum",
 )
 
 
@@ -107,6 +108,8 @@ def load():
         "infs_sched_destroy": (None, [P]),
         "infs_fptas_assign": (I32, [I32, I32, ctypes.POINTER(ctypes.c_double), ctypes.c_double,
                                     ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+        "infs_sched_optimum": (I32, [I32, I32, ctypes.POINTER(I32), I64, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                     ctypes.POINTER(I32)]),
         "infs_probe_step": (I32, [P, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_uint8), P, P, P, P]),
         "infs_end_probe_step": (I32, [P]),
         "infs_probe_batch": (I32, [P]),
@@ -349,3 +352,16 @@ def fptas_assign(pred_len, N, epsilon=FPTAS_EPSILON):
     if st != OK:
         raise InfsError(st, "infs_fptas_assign")
     return group, pos
+
+
+def sched_optimum(lengths, m, max_nodes=20_000_000):
+    """infs_sched_optimum: (best, lower, slot array); best == lower when the optimum is proven."""
+    L = np.ascontiguousarray(lengths, dtype=np.int32)
+    slot = np.zeros(len(L), dtype=np.int32)
+    best, lower = ctypes.c_int64(), ctypes.c_int64()
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    st = load().infs_sched_optimum(len(L), m, L.ctypes.data_as(I32P), max_nodes, ctypes.byref(best),
+                                   ctypes.byref(lower), slot.ctypes.data_as(I32P))
+    if st != OK:
+        raise InfsError(st, "infs_sched_optimum")
+    return best.value, lower.value, slot

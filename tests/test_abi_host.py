@@ -415,3 +415,39 @@ def test_static_entry_point_workspace_limit():
             ctx.decode_step(layer, *none4)
         ctx.end_step()
         assert ctx.get_stats().launches == cfg.layers
+
+
+def test_sched_optimum_matches_oracle():
+    # infs_sched_optimum (branch and bound) against the oracle's capacity
+    # search on random small groups and on the scheduler study's groups the
+    # oracle finishes; every schedule it returns must have its reported steps.
+    from oracle import makespan, optimum
+    from workload import SCHEDULER_STUDY, scheduler_study_lengths
+
+    rng = np.random.default_rng(21)
+    cases = []
+    for _ in range(300):
+        G = int(rng.integers(1, 13))
+        cases.append((rng.integers(1, 60, size=G), int(rng.integers(1, 6))))
+    for k, (_, mu, sigma) in enumerate(SCHEDULER_STUDY):
+        L, _ = scheduler_study_lengths(mu, sigma, 8, 32, cap=1024, seed=k)
+        cases.extend((row, 4) for row in L)
+    checked = 0
+    for L, m in cases:
+        best, lower, slot = infs.sched_optimum(L, m)
+        assert best == lower, (L, m)
+        assert makespan(L, slot, m) == best
+        want, _ = optimum(L, m, max_nodes=300_000)
+        if want is not None:
+            assert best == want, (L, m)
+            checked += 1
+    assert checked >= len(cases) - 4
+
+
+def test_sched_optimum_budget_and_errors():
+    best, lower, slot = infs.sched_optimum([7, 6, 5, 4, 3, 3, 2, 2, 1], 3, max_nodes=0)
+    assert lower <= 11 <= best   # 33 / 3 = 11 is reached by 7+4 | 6+3+2 | 5+3+2+1
+    assert infs.sched_optimum([7, 6, 5, 4, 3, 3, 2, 2, 1], 3)[:2] == (11, 11)
+    for bad in (([0, 3], 2), ([3, 4], 0)):
+        with pytest.raises(infs.InfsError):
+            infs.sched_optimum(*bad)
