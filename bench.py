@@ -33,7 +33,8 @@ SIMDS = 1024  # 256 compute units x 4 SIMDs
 XCDS = 8
 MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE")
 KERNEL_SOURCES = tuple("paper_2506_22950_amd/csrc/" + f for f in (
-    "decode.h", "kernels.h", "plan.h", "kernels.hip", "inst_wave.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip",
+    "decode.h", "layers.h", "kernels.h", "plan.h", "kernels.hip", "inst_wave_f32_d64.hip", "inst_wave_f32_d128.hip",
+    "inst_wave_bf16_d64.hip", "inst_wave_bf16_d128.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip",
     "inst_mfma_d128b.hip", "inst_kv8a.hip", "inst_kv8b.hip"))
 METRIC = "generated tokens/sec per group decode + achieved HBM TB/s vs peak, 1 MI355X"
 
@@ -347,8 +348,11 @@ def algorithmic_bytes(cfg, steplog, kv_bytes=None):
 STAGE_BUDGET_BYTES = 160 << 30  # staged per-step inputs beyond this are cycled through a window
 
 
+ENTRIES = {"step": "decode_step_layers", "layer": "decode_step"}
+
+
 class Bench:
-    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False):
+    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False, entry="step"):
         import numpy as np
         import torch
 
@@ -358,6 +362,7 @@ class Bench:
         from workload.staging import DeviceInputs
 
         self.np, self.torch = np, torch
+        self.entry = ENTRIES[entry]
         infs.load()
         cfg = get_config(cfg_name)
         self.cfg = cfg
@@ -429,7 +434,7 @@ class Bench:
 
         cfg = self.cfg
         return decode_group(self.ctx, schedulers_for(cfg, cfg.policy, self.wl.L_hat), self.wl.L, cfg.layers,
-                            self.provide, reuse=self.reuse)
+                            self.provide, reuse=self.reuse, entry=self.entry)
 
     def group_decode(self):
         """One benchmark step: prefill every layer, the probe phase (with prefix
@@ -481,44 +486,92 @@ class Bench:
         return (ms, region_ms, n, st.alg_bytes - before.alg_bytes, st.launches - before.launches), probe
 
 
-def cpu_baseline(bench, budget_s=15.0):
-    """The float64 oracle on the host, single-threaded, on whole decode steps
-    (every layer, every live slot) sampled evenly over the run."""
-    import numpy as np
+CPU_POOL_MAX = 16  # worker processes at most (the host share of one GPU machine)
+
+
+def _oracle_worker_init(cfg_name, overrides):
+    global _ORACLE_WL
     from threadpoolctl import threadpool_limits
 
+    from workload import Workload, get_config
+
+    threadpool_limits(limits=1)
+    _ORACLE_WL = Workload(get_config(cfg_name, **overrides))
+
+
+def _oracle_worker(unit):
+    """One (step, layer) unit of the CPU baseline: the float64 oracle for every
+    live slot of that step at that layer.  Returns its wall seconds."""
     from oracle import attend_slot
 
-    cfg, wl, steplog = bench.cfg, bench.wl, bench.log
+    layer, entries = unit
+    t0 = time.perf_counter()
+    for p, i, t in entries:
+        attend_slot(_ORACLE_WL, layer, p, i, t)
+    return time.perf_counter() - t0
+
+
+def cpu_sample_steps(steplog):
+    """Steps of the CPU baseline's sample: every step = 0 mod 97, the first and
+    last 8, and every step in which some slot decodes its first token (a refill)."""
     n = len(steplog)
-    order = [int(x) for x in np.linspace(0, n - 1, 64)]
-    # visit the evenly spaced steps in a bit-reversed-like order so any prefix is spread out
-    order = order[::8] + [x for i, x in enumerate(order) if i % 8]
-    done, spent, toks = [], 0.0, 0
-    with threadpool_limits(limits=1):
-        for k in order:
-            t0 = time.perf_counter()
-            for e in steplog[k]:
-                if e is None:
-                    continue
-                p, i, t = e
-                for layer in range(cfg.layers):
-                    attend_slot(wl, layer, p, i, t)
-            spent += time.perf_counter() - t0
-            done.append(k)
-            if spent >= budget_s and len(done) >= 2:
-                break
-    per_step = spent / len(done)
-    est_total = per_step * n
+    keep = {k for k in range(n) if k % 97 == 0} | set(range(min(8, n))) | set(range(max(0, n - 8), n))
+    keep |= {k for k, row in enumerate(steplog) if any(e is not None and e[2] == 1 for e in row)}
+    return sorted(keep)
+
+
+def step_flops(cfg, row):
+    """Attention flops of one step at one layer: 4 * Hq * d * (P + t) per live slot."""
+    return sum(4.0 * cfg.num_q_heads * cfg.head_dim * (cfg.prompt_lens[e[0]] + e[2]) for e in row if e is not None)
+
+
+def cpu_baseline(bench):
+    """The float64 oracle on the host's cores (a pool of spawned worker processes,
+    one BLAS thread each) over a sample of the workload -- steps = 0 mod 97,
+    the first and last 8, every refill step, on layers 0, L/2 and L-1 -- with the
+    full run's time extrapolated by the ratio of attention flops."""
+    import multiprocessing as mp
+    from dataclasses import asdict
+
+    from threadpoolctl import threadpool_info
+
+    cfg, steplog = bench.cfg, bench.log
+    steps = cpu_sample_steps(steplog)
+    layers = sorted({0, cfg.layers // 2, cfg.layers - 1})
+    units = [(layer, [e for e in steplog[k] if e is not None]) for k in steps for layer in layers]
+    sample_flops = sum(step_flops(cfg, steplog[k]) for k in steps) * len(layers)
+    total_flops = sum(step_flops(cfg, row) for row in steplog) * cfg.layers
+    cores = len(os.sched_getaffinity(0))
+    workers = max(1, min(cores, CPU_POOL_MAX))
+    base = asdict(get_config_default(cfg.name))
+    overrides = {k: v for k, v in asdict(cfg).items() if base.get(k) != v}
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers, initializer=_oracle_worker_init, initargs=(cfg.name, overrides)) as pool:
+        pool.map(_oracle_worker, units[:workers])  # warm the workers up (pools drawn, imports done)
+        t0 = time.perf_counter()
+        busy = sum(pool.map(_oracle_worker, units, chunksize=1))
+        wall = time.perf_counter() - t0
+    blas = sorted({str(i.get("internal_api")) for i in threadpool_info()})
+    est = wall * total_flops / sample_flops
     return {
-        "value": round(bench.tokens / est_total, 4),
+        "value": round(bench.tokens / est, 4),
         "unit": "tokens/s",
-        "cores": 1,
+        "cores": workers,
         "kind": "oracle",
-        "sample": (f"{len(done)} whole decode steps (all {cfg.layers} layers x live slots) of {n}, evenly spaced; "
-                   f"{spent:.1f}s measured, {per_step:.2f}s/step extrapolated to {n} steps and "
-                   f"{bench.tokens} tokens; float64 numpy, 1 BLAS thread"),
+        "sample": (f"{len(steps)} of {len(steplog)} steps (= 0 mod 97, first and last 8, every refill step) x layers "
+                   f"{layers}: {len(units)} (step, layer) units, {sample_flops / 1e12:.3f} of {total_flops / 1e12:.2f} "
+                   f"TFLOP; {wall:.1f} s wall on {workers} worker processes ({busy:.1f} s busy), extrapolated to the "
+                   f"whole group by the flop ratio; float64 numpy, 1 BLAS thread per worker"),
+        "host_cpus": cores,
+        "blas": blas,
+        "blas_threads_per_worker": 1,
     }
+
+
+def get_config_default(name):
+    from workload import get_config
+
+    return get_config(name)
 
 
 def main():
@@ -537,6 +590,9 @@ def main():
     ap.add_argument("--exchange", type=int, choices=(0, 1), default=None,
                     help="partial exchange: 0 through the coherence point, 1 through the XCD's L2 "
                          "(default: the library's choice)")
+    ap.add_argument("--entry", choices=tuple(ENTRIES), default="step",
+                    help="step: one launch per running step through every layer (infs_decode_step_layers); "
+                         "layer: one launch per layer (infs_decode_step)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -565,7 +621,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         copy_calibration(torch)
-    b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8)
+    b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8, entry=args.entry)
     if args.exchange is not None:
         b.ctx.set_exchange(args.exchange)
 
@@ -602,10 +658,13 @@ def main():
         traffic = read_traffic(args.workload) if not (args.reuse or args.kv_fp8 or args.exchange is not None) else None
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "decode_kernel", "launches": n, "avg_launch_us": round(avg_us, 3),
+                "kernel": "layers_kernel" if b.entry == "decode_step_layers" else "decode_kernel",
+                "launches": n, "avg_launch_us": round(avg_us, 3),
                 "alg_bytes_per_launch": round(per_launch),
                 "timing": "HIP events on the kernels' stream around all decode launches of one group decode, "
                           "divided by their number",
+                "launch_covers": ("every layer of one running step" if b.entry == "decode_step_layers"
+                                  else "one layer of one running step"),
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}

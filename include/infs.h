@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define INFS_ABI_VERSION 2
+#define INFS_ABI_VERSION 3
 
 typedef enum infs_status {
     INFS_OK = 0,
@@ -244,6 +244,33 @@ infs_status infs_decode_step(infs_ctx* ctx, int32_t layer, const void* q_dev, co
 #define INFS_STATIC_SCRATCH_BYTES (16u << 20)
 infs_status infs_decode_step_static(infs_ctx* ctx, int32_t layer, const void* q_dev, const void* k_new_dev,
                                     const void* v_new_dev, float* o_dev);
+
+/* Every layer of one running step in a single launch (Section 2.1: a decode step passes through all
+   layers; Section 5.1: one running step decodes one token for every live slot): the same results as
+   infs_decode_step for layers 0 .. num_layers-1 in order.  Layer l reads q_dev + l * q_layer_stride
+   ([S, Hq, d]), k_new_dev / v_new_dev + l * kv_layer_stride ([S, Hkv, d]) and writes o_dev + l *
+   o_layer_stride ([S, Hq, d] fp32); strides are in bytes, multiples of 16, and 0 means one layer's rows
+   (dense [L, S, H, d] buffers).  All four buffers stay with the caller until the stream work is done.
+   The launch keeps as many work-groups as the GPU holds resident at once (infs_step_launch_workgroups)
+   and walks the layers in order: the queries and new K/V rows of layer l are read only after every
+   merge of layer l-1 of the same prompt has written its O rows (as a model's layer l would need), while
+   the cached prefix and response K/V of layer l may be loaded earlier.  Split-K partials always go
+   through the device coherence point here (the exchange mode of infs_set_exchange applies to
+   infs_decode_step).  Every device wait is bounded (infs_set_merge_wait); a wait that gives up makes the
+   next synchronising call return E_DEVICE.  The launch needs all its work-groups on the GPU at once: other
+   work running on the same GPU at the same time can delay it until its waits give up.
+   E_STATE: a layer of this step was already decoded, a probe step is open, a live slot's prompt lacks
+   a prefilled layer, or the device cannot hold the launch (infs_step_launch_workgroups() == 0).
+   E_CAPACITY as infs_decode_step.  E_ARG: null or misaligned buffers, strides below one layer's rows.
+   Close the step with infs_end_step; infs_get_stats counts the call as one launch. */
+infs_status infs_decode_step_layers(infs_ctx* ctx, const void* q_dev, const void* k_new_dev, const void* v_new_dev,
+                                    float* o_dev, int64_t q_layer_stride, int64_t kv_layer_stride,
+                                    int64_t o_layer_stride);
+
+/* Work-groups of an infs_decode_step_layers launch (the occupancy of its kernel times the compute
+   units; 0 on a dry-run context or when the device cannot hold one producer and one merge work-group per
+   KV head); -1 for a NULL context. */
+int32_t infs_step_launch_workgroups(const infs_ctx* ctx);
 
 /* Close the step: every live slot's length grows by one.  E_STATE unless every layer was decoded
    exactly once since the previous end_step (a step with no live slot needs no decode). */

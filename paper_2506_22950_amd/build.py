@@ -22,7 +22,8 @@ BUILD_DIR = os.path.join(HERE, "_build")
 
 # Decode kernel instantiations are spread over several translation units
 # (inst_*.hip) that compile in parallel; the device code is in decode.h.
-SOURCES = ["kernels.hip", "inst_wave.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip", "inst_mfma_d128b.hip",
+SOURCES = ["kernels.hip", "inst_wave_f32_d64.hip", "inst_wave_f32_d128.hip", "inst_wave_bf16_d64.hip",
+           "inst_wave_bf16_d128.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip", "inst_mfma_d128b.hip",
            "inst_kv8a.hip", "inst_kv8b.hip", "scratch.hip", "runtime.cpp", "sched.cpp"]
 CALIB_SOURCES = ["calib.hip"]
 
@@ -67,7 +68,7 @@ def build(verbose: bool = False) -> str:
             print("\n".join(msgs))
         return obj
 
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES) + len(CALIB_SOURCES))) as ex:
+    with ThreadPoolExecutor(max_workers=min(os.cpu_count() or 8, 16, len(SOURCES) + len(CALIB_SOURCES))) as ex:
         objs = list(ex.map(compile_one, SOURCES + CALIB_SOURCES))
     for lib, part in ((LIB, objs[:len(SOURCES)]), (CALIB_LIB, objs[len(SOURCES):])):
         tmp = lib + ".tmp"

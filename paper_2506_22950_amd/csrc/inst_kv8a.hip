@@ -1,10 +1,10 @@
 // Decode kernel instantiations: E4M3 K/V cache, bf16 compute, head_dim 128, MFMA prefix tiles, 1 or 2 query heads per KV head.
-#include "decode.h"
+#include "layers.h"
 
 namespace infs {
 namespace {
 
-#define INFS_ENTRY(d, hpk, pr) {{1, d, hpk, 1, pr, 1}, {decode_kernel<Shape<true, d, hpk, true, pr, true>, false>, decode_kernel<Shape<true, d, hpk, true, pr, true>, true>}},
+#define INFS_ENTRY(d, hpk, pr) {{1, d, hpk, 1, pr, 1}, {decode_kernel<Shape<true, d, hpk, true, pr, true>, false>, decode_kernel<Shape<true, d, hpk, true, pr, true>, true>}, layers_kernel<Shape<true, d, hpk, true, pr, true>>},
 
 const KernelEntry kEntries[] = {
     INFS_ENTRY(128, 1, 16)

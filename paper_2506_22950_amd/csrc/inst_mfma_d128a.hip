@@ -1,10 +1,10 @@
 // Decode kernel instantiations: bf16, head_dim 128, prefix on MFMA tiles of 16/32/64/128 padded rows, 1 or 2 query heads per KV head.
-#include "decode.h"
+#include "layers.h"
 
 namespace infs {
 namespace {
 
-#define INFS_ENTRY(bf, d, hpk, mf, pr) {{bf, d, hpk, mf, pr, 0}, {decode_kernel<Shape<bf, d, hpk, mf, pr>, false>, decode_kernel<Shape<bf, d, hpk, mf, pr>, true>}},
+#define INFS_ENTRY(bf, d, hpk, mf, pr) {{bf, d, hpk, mf, pr, 0}, {decode_kernel<Shape<bf, d, hpk, mf, pr>, false>, decode_kernel<Shape<bf, d, hpk, mf, pr>, true>}, layers_kernel<Shape<bf, d, hpk, mf, pr>>},
 
 const KernelEntry kEntries[] = {
     INFS_ENTRY(true, 128, 1, true, 16)

@@ -35,17 +35,28 @@ int64_t prefix_elems_per_head(const KernelKey& key, int max_prompt_len_padded);
 
 hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream);
 
+// The step launch through every layer (args.num_layers layers).
+hipError_t launch_layers(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream);
+
+// Work-groups of the step-launch kernel of `key` that the current device keeps
+// resident at once (occupancy per compute unit times compute units).
+hipError_t layers_resident(const KernelKey& key, int* resident);
+
 // The decode kernel instantiations, spread over several translation units
 // (inst_*.hip) so that they compile in parallel.
 struct KernelEntry {
   KernelKey key;
   void (*decode[2])(const StepArgs);  // [0]: partials through the coherence point, [1]: through the XCD's L2
+  void (*layers)(const StepArgs);     // step launch through every layer (partials through the coherence point)
 };
 struct KernelTable {
   const KernelEntry* entries;
   int count;
 };
-KernelTable kernels_wave();        // fp32, and bf16 below 16 prefix rows (wavefront reductions)
+KernelTable kernels_wave_f32_d64();    // fp32, head_dim 64 (wavefront reductions)
+KernelTable kernels_wave_f32_d128();   // fp32, head_dim 128
+KernelTable kernels_wave_bf16_d64();   // bf16 below 16 prefix rows, head_dim 64
+KernelTable kernels_wave_bf16_d128();  // bf16 below 16 prefix rows, head_dim 128
 KernelTable kernels_mfma_d64();    // bf16, head_dim 64, MFMA prefix tiles
 KernelTable kernels_mfma_d128a();  // bf16, head_dim 128, hpk 1 and 2
 KernelTable kernels_mfma_d128b();  // bf16, head_dim 128, hpk 4 and 8

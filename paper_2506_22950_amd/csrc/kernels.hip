@@ -2,13 +2,14 @@
 // selection, the launches, and the prefill kernels.  The device code (and what
 // the kernels compute) is in decode.h; the decode kernel instantiations are in
 // inst_*.hip.
-#include "decode.h"
+#include "layers.h"
 
 namespace infs {
 namespace {
 
 const KernelEntry* find_entry(const KernelKey& k) {
-  static const KernelTable tables[] = {kernels_wave(),      kernels_mfma_d64(), kernels_mfma_d128a(),
+  static const KernelTable tables[] = {kernels_wave_f32_d64(),  kernels_wave_f32_d128(), kernels_wave_bf16_d64(),
+                                       kernels_wave_bf16_d128(), kernels_mfma_d64(),      kernels_mfma_d128a(),
                                        kernels_mfma_d128b(), kernels_kv8a(),     kernels_kv8b()};
   for (const KernelTable& t : tables)
     for (int i = 0; i < t.count; ++i) {
@@ -53,6 +54,25 @@ hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, h
   if (!e) return hipErrorInvalidValue;
   hipLaunchKernelGGL(e->decode[args.l2_xcds > 0 ? 1 : 0], dim3(grid), dim3(kBlockThreads), 0, stream, args);
   return hipGetLastError();
+}
+
+hipError_t launch_layers(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream) {
+  const KernelEntry* e = find_entry(key);
+  if (!e) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(e->layers, dim3(grid), dim3(kBlockThreads), 0, stream, args);
+  return hipGetLastError();
+}
+
+hipError_t layers_resident(const KernelKey& key, int* resident) {
+  const KernelEntry* e = find_entry(key);
+  if (!e) return hipErrorInvalidValue;
+  int per_cu = 0, dev = 0, cus = 0;
+  hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, e->layers, kBlockThreads, 0);
+  if (err == hipSuccess) err = hipGetDevice(&dev);
+  if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (err != hipSuccess) return err;
+  *resident = per_cu * cus;
+  return hipSuccess;
 }
 
 #define INFS_PREFILL_CASE(bf, d, mf, k8)                                                               \

@@ -42,7 +42,9 @@ struct SlotPlan {
   int32_t cur_page;    // page holding position len-1 (where this step's K/V go)
   int32_t sample;      // sample id (token counters)
   int32_t target;      // slot counter value once this launch's producers for the slot (its response
-                       // chunks and its prompt's prefix chunks) have all arrived
+                       // chunks and its prompt's prefix chunks) have all arrived; in a step launch
+                       // through every layer, the value before the launch (each layer adds the
+                       // slot's producer count)
   int32_t seq;         // page-table row of the sample's response (a sequence handle)
   int32_t pad_[2];
 };
@@ -95,6 +97,21 @@ struct StepArgs {
                               // b % l2_xcds (0: written through to the device coherence point)
   int32_t l2_check_shift;     // 0; 1 makes every work-group's XCD check fail (error-path tests)
   int32_t merge_polls;        // bound on a merge block's polls of its counters (kMergeSpins; < 0: none)
+  // Step launch through every layer (infs_decode_step_layers); unused by per-layer launches.
+  // Layer l reads q + l * q_layer_stride (knew, vnew alike) and writes o + l * o_layer_stride; the
+  // prefix store and page pool of layer l are prefix + l * prefix_layer_bytes and pool + l *
+  // pool_layer_bytes.  Per KV head, the first n_pre_wg work-groups take the prefix items round
+  // robin, the next n_suf_wg the response items, and the next n_merge_wg work-groups do one slot's
+  // merge (or zeroing) per wavefront.
+  int32_t num_layers;
+  int32_t n_pre_wg, n_suf_wg, n_merge_wg;
+  int64_t q_layer_stride, kv_layer_stride, o_layer_stride;
+  int64_t prefix_layer_bytes, pool_layer_bytes;
+  int32_t* merged;                     // per prompt, kCounterStride apart: merges completed (they only grow);
+                                       // then per (prompt, KV head) the layer-done flags
+  int32_t merged_base[kMaxPrompts];    // value of each prompt's merged counter before this launch
+  int32_t merged_per_layer[kMaxPrompts];  // merges of each prompt per layer: its live slots * Hkv
+  uint64_t live_mask;                  // bit s set: slot s is live this step
   // this step
   int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;
   int32_t num_prompts;

@@ -66,6 +66,7 @@ struct infs_ctx {
   int32_t* tokens = nullptr;
   int32_t* status = nullptr;
   void* scratch = nullptr;  // this device's static scratch array (infs_decode_step_static)
+  int layers_resident = 0;  // work-groups of the step-launch kernel resident at once (0: no step launch)
   // host state
   std::vector<int32_t> plen;                       // per prompt, -1 before its first prefill
   std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
@@ -83,6 +84,8 @@ struct infs_ctx {
   // Arrivals each slot's device counter has been sent so far (the same for
   // every KV head): its response chunks and its prompt's prefix chunks.
   std::vector<uint32_t> slot_arrivals;
+  // Merges each prompt's "merged" counter has counted so far (step launches only).
+  std::vector<uint32_t> merged_arrivals;
   bool step_open = false;
   // Probe phase of prefix reuse.
   int probe_k = 0;                                 // probe tokens per sample (0: no prefix reuse)
@@ -162,9 +165,15 @@ void free_device(infs_ctx* c) {
 }
 
 // Counters: one per (slot, KV head) for decode launches [S][Hkv], then the
-// probe launches' own [kMaxSlots][Hkv].
-size_t counter_bytes(const infs_ctx* c) {
-  return sizeof(int32_t) * infs::kCounterStride * (size_t)(c->S + infs::kMaxSlots) * c->Hkv;
+// probe launches' own [kMaxSlots][Hkv], then for step launches one "merged"
+// counter per prompt and one layer-done flag per (prompt, KV head); each on a
+// 128-byte line of its own.
+size_t counter_lines(const infs_ctx* c) {
+  return (size_t)(c->S + infs::kMaxSlots) * c->Hkv + c->NP + (size_t)c->NP * c->Hkv;
+}
+size_t counter_bytes(const infs_ctx* c) { return sizeof(int32_t) * infs::kCounterStride * counter_lines(c); }
+int32_t* merged_counters(const infs_ctx* c) {
+  return c->counters + (size_t)(c->S + infs::kMaxSlots) * c->Hkv * infs::kCounterStride;
 }
 
 // Split-K record capacities.  Records are numbered (prompt, KV head)-major for
@@ -193,6 +202,7 @@ void reset_host(infs_ctx* c) {
   for (int i = 0; i < c->num_pages; ++i) c->free_pages.push(i);
   c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
   c->slot_arrivals.assign(c->S, 0);
+  c->merged_arrivals.assign(c->NP, 0);
   c->step_open = false;
   c->probe_len.assign(c->probe_k > 0 ? c->NP : 0, std::vector<int32_t>(c->G, 0));
   c->probe_open = false;
@@ -270,6 +280,9 @@ infs_status open_step(infs_ctx* c) {
   a.n_suffix_items = items;
   a.n_zero_items = zeros;
   a.n_merge_items = lives;
+  a.live_mask = 0;
+  for (int s = 0; s < c->S; ++s)
+    if (a.slot[s].len > 0) a.live_mask |= uint64_t(1) << s;
   c->grid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items + a.n_merge_items) * c->Hkv;
   c->step_bytes = bytes;
   c->step_flops = flops;
@@ -345,6 +358,9 @@ infs_status open_probe(infs_ctx* c, int p, int first, int n, const uint8_t* live
   a.n_suffix_items = items;
   a.n_zero_items = zeros;
   a.n_merge_items = lives;
+  a.live_mask = 0;
+  for (int j = 0; j < n; ++j)
+    if (a.slot[j].len > 0) a.live_mask |= uint64_t(1) << j;
   c->pgrid = (a.n_prefix_items + a.n_suffix_items + a.n_zero_items + a.n_merge_items) * c->Hkv;
   c->pstep_bytes = bytes;
   c->pstep_flops = flops;
@@ -398,7 +414,8 @@ infs_status check_status(infs_ctx* c) {
   if (st != 0) {
     fail(c, INFS_E_DEVICE, st == 2 ? "a work-group ran on another XCD than the XCD-local exchange of partials "
                                      "assumes; outputs are invalid (infs_set_exchange(ctx, 0) avoids it)"
-                                   : "a merge work-group gave up waiting for its producers; outputs are invalid");
+                                   : "a decode launch gave up waiting (a merge for its producers, or a layer of a "
+                                     "step launch for the previous layer); outputs are invalid");
     c->dead = true;
     c->dead_msg = c->err;
     return INFS_E_DEVICE;
@@ -416,8 +433,9 @@ void set_targets(infs_ctx* c) {
   }
 }
 
-// Launch one decode or probe kernel; in timing mode it records its start and end.
-infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int grid) {
+// Launch one decode or probe kernel (or, with `layers`, the step launch through
+// every layer); in timing mode it records its start and end.
+infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int grid, bool layers = false) {
   Timing& t = c->timing;
   a.clock_start = a.clock_end = nullptr;
   if (t.on) {
@@ -429,7 +447,7 @@ infs_status timed_launch(infs_ctx* c, const KernelKey& key, StepArgs& a, int gri
     a.clock_end = t.clocks + ((size_t)t.capacity + t.used) * kClockWords;
     ++t.used;
   }
-  HIP_TRY(c, infs::launch_decode(key, a, grid, c->stream));
+  HIP_TRY(c, layers ? infs::launch_layers(key, a, grid, c->stream) : infs::launch_decode(key, a, grid, c->stream));
   return INFS_OK;
 }
 
@@ -663,6 +681,14 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       delete c;
       return device_fail(nullptr, se, "hipGetSymbolAddress(static scratch)");
     }
+    const hipError_t oe = infs::layers_resident(key, &c->layers_resident);
+    if (oe != hipSuccess) {
+      free_device(c);
+      delete c;
+      return device_fail(nullptr, oe, "occupancy query of the step launch");
+    }
+    // a step launch needs at least one producer and one merge work-group per KV head
+    if (c->layers_resident / c->Hkv < 2) c->layers_resident = 0;
     a.l2_xcds = c->l2_xcds;
     a.page_table = c->page_table;
     a.ws_o = c->ws_o;
@@ -861,6 +887,101 @@ infs_status infs_decode_step_static(infs_ctx* c, int32_t layer, const void* q_de
                                     const void* v_new_dev, float* o_dev) {
   return decode_layer(c, layer, q_dev, k_new_dev, v_new_dev, o_dev, true);
 }
+
+infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* k_new_dev, const void* v_new_dev,
+                                    float* o_dev, int64_t q_layer_stride, int64_t kv_layer_stride,
+                                    int64_t o_layer_stride) {
+  CHECK_CTX(c);
+  const int64_t q_bytes = (int64_t)c->S * c->Hq * c->D * (int64_t)c->es;
+  const int64_t kv_bytes = (int64_t)c->S * c->Hkv * c->D * (int64_t)c->es;
+  const int64_t o_bytes = (int64_t)c->S * c->Hq * c->D * (int64_t)sizeof(float);
+  if (q_layer_stride == 0) q_layer_stride = q_bytes;
+  if (kv_layer_stride == 0) kv_layer_stride = kv_bytes;
+  if (o_layer_stride == 0) o_layer_stride = o_bytes;
+  if (q_layer_stride < q_bytes || kv_layer_stride < kv_bytes || o_layer_stride < o_bytes)
+    return fail(c, INFS_E_ARG, "layer strides must be 0 or at least one layer's rows (%lld, %lld, %lld bytes)",
+                (long long)q_bytes, (long long)kv_bytes, (long long)o_bytes);
+  if ((q_layer_stride | kv_layer_stride | o_layer_stride) & 15)
+    return fail(c, INFS_E_ARG, "layer strides must be multiples of 16 bytes");
+  if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
+  if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
+    return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
+  if (c->probe_open) return fail(c, INFS_E_STATE, "decode_step_layers while a probe step is open");
+  if (c->step_open && c->layers_done > 0)
+    return fail(c, INFS_E_STATE, "decode_step_layers needs a step with no layer decoded yet (%d decoded)",
+                c->layers_done);
+  if (!c->dry && c->layers_resident == 0)
+    return fail(c, INFS_E_STATE, "no step launch on this device: too few work-groups resident per KV head");
+  for (int p = 0; p < c->NP; ++p) {
+    bool live = false;
+    for (int s = p * c->m; s < (p + 1) * c->m; ++s) live |= c->slot_sample[s] >= 0;
+    for (int layer = 0; live && layer < c->L; ++layer)
+      if (!c->prefilled[p][layer])
+        return fail(c, INFS_E_STATE, "prompt %d has live slots but layer %d is not prefilled", p, layer);
+  }
+  if (!c->step_open) {
+    infs_status st = open_step(c);
+    if (st != INFS_OK) return st;
+  }
+  if (!c->dry) {
+    StepArgs& a = c->plan;
+    a.q = q_dev;
+    a.knew = k_new_dev;
+    a.vnew = v_new_dev;
+    a.o = o_dev;
+    a.prefix = c->prefix;
+    a.pool = c->pool;
+    a.count_tokens = 1;
+    a.num_layers = c->L;
+    a.q_layer_stride = q_layer_stride;
+    a.kv_layer_stride = kv_layer_stride;
+    a.o_layer_stride = o_layer_stride;
+    a.prefix_layer_bytes = (int64_t)c->prefix_layer_bytes;
+    a.pool_layer_bytes = (int64_t)c->pool_layer_bytes;
+    a.merged = merged_counters(c);
+    // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix and
+    // response chunks in proportion to their counts (at least one each when there are any).
+    const int nj = c->layers_resident / c->Hkv;
+    a.n_merge_wg = std::min(ceil_div(c->S, infs::kWaves), nj - 1);
+    const int prod = nj - a.n_merge_wg;
+    const int npi = a.n_prefix_items, nsi = a.n_suffix_items;
+    int pre = 0;
+    if (npi > 0) {
+      pre = (int)((int64_t)prod * npi / std::max(1, npi + nsi));
+      pre = std::max(1, std::min(pre, npi));
+      if (nsi > 0) pre = std::min(pre, prod - 1);
+    }
+    a.n_pre_wg = std::max(pre, 0);
+    a.n_suf_wg = prod - a.n_pre_wg;
+    if ((npi > 0 && a.n_pre_wg < 1) || (nsi > 0 && a.n_suf_wg < 1))
+      return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
+                  "chunks, response chunks and merges", nj);
+    // counter targets: each slot counts its producers once per layer, each prompt its merges
+    for (int s = 0; s < c->S; ++s) {
+      a.slot[s].target = (int32_t)c->slot_arrivals[s];
+      if (a.slot[s].len > 0)
+        c->slot_arrivals[s] +=
+            (uint32_t)c->L * (uint32_t)(ceil_div(a.slot[s].len, c->split) + a.prompt[s / c->m].nchunks);
+    }
+    for (int p = 0; p < c->NP; ++p) {
+      int live = 0;
+      for (int s = p * c->m; s < (p + 1) * c->m; ++s) live += a.slot[s].len > 0;
+      a.merged_base[p] = (int32_t)c->merged_arrivals[p];
+      a.merged_per_layer[p] = live * c->Hkv;
+      c->merged_arrivals[p] += (uint32_t)c->L * (uint32_t)(live * c->Hkv);
+    }
+    infs_status st = timed_launch(c, c->key, a, c->Hkv * (a.n_pre_wg + a.n_suf_wg + a.n_merge_wg), true);
+    if (st != INFS_OK) return st;
+  }
+  std::fill(c->layer_done.begin(), c->layer_done.end(), 1);
+  c->layers_done = c->L;
+  ++c->stats.launches;
+  c->stats.alg_bytes += c->step_bytes * c->L;
+  c->stats.alg_flops += c->step_flops * c->L;
+  return INFS_OK;
+}
+
+int32_t infs_step_launch_workgroups(const infs_ctx* c) { return c ? c->layers_resident : -1; }
 
 infs_status infs_end_step(infs_ctx* c) {
   CHECK_CTX(c);

@@ -95,9 +95,15 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
     a dispatched sample resumes at token k+1, and one that finished within its
     probe tokens is skipped (the scheduler is told it is done at once).
     entry: the C call that decodes a layer -- "decode_step", or
-    "decode_step_static" (split-K workspace in the library's static scratch).
+    "decode_step_static" (split-K workspace in the library's static scratch) --
+    or "decode_step_layers": every layer of a step in one launch, fed with the
+    pointers provide(step, 0) returns, whose layers must be laid out densely
+    ([L, S, H, d] for Q, the new K/V rows and O).  A function of the step
+    number picks the entry step by step.
     """
-    decode = {"decode_step": ctx.decode_step, "decode_step_static": ctx.decode_step_static}[entry]
+    entries = {"decode_step": ctx.decode_step, "decode_step_static": ctx.decode_step_static,
+               "decode_step_layers": None}
+    entry_of = entry if callable(entry) else (lambda step: entry)
     NP = len(scheds)
     m = ctx.config.slots_per_prompt
     S = NP * m
@@ -131,8 +137,12 @@ def decode_group(ctx: infs.Context, scheds: Sequence[infs.Sched], lengths, num_l
         if log is not None:
             log.append(tuple((s // m, slot_sample[s], slot_len[s] + 1) if slot_sample[s] >= 0 else None
                              for s in range(S)))
-        for layer in range(num_layers):
-            decode(layer, *provide(step, layer))
+        decode = entries[entry_of(step)]
+        if decode is None:
+            ctx.decode_step_layers(*provide(step, 0))
+        else:
+            for layer in range(num_layers):
+                decode(layer, *provide(step, layer))
         ctx.end_step()
         if after_step is not None:
             after_step(step)

@@ -36,7 +36,7 @@ EXPORTS = (
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
     "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode", "infs_decode_step_static",
-    "infs_sched_optimum",
+    "infs_sched_optimum", "infs_decode_step_layers", "infs_step_launch_workgroups",
 )
 
 
@@ -89,6 +89,8 @@ def load():
         "infs_retire_slot": (I32, [P, I32]),
         "infs_decode_step": (I32, [P, I32, P, P, P, P]),
         "infs_decode_step_static": (I32, [P, I32, P, P, P, P]),
+        "infs_decode_step_layers": (I32, [P, P, P, P, P, I64, I64, I64]),
+        "infs_step_launch_workgroups": (I32, [P]),
         "infs_end_step": (I32, [P]),
         "infs_slot_state": (I32, [P, I32, ctypes.POINTER(I64), ctypes.POINTER(I32)]),
         "infs_sample_tokens": (I32, [P, I32, ctypes.POINTER(I32), I32]),
@@ -197,6 +199,14 @@ class Context:
 
     def decode_step_static(self, layer, q, k_new, v_new, o):
         self._call(load().infs_decode_step_static, layer, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o))
+
+    def decode_step_layers(self, q, k_new, v_new, o, q_layer_stride=0, kv_layer_stride=0, o_layer_stride=0):
+        self._call(load().infs_decode_step_layers, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(o), q_layer_stride,
+                   kv_layer_stride, o_layer_stride)
+
+    @property
+    def step_launch_workgroups(self):
+        return load().infs_step_launch_workgroups(self._h)
 
     def end_step(self):
         self._call(load().infs_end_step)

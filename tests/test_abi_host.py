@@ -29,7 +29,7 @@ def test_exports_every_declared_symbol():
     assert declared == set(infs.EXPORTS)
     for name in declared:
         assert hasattr(lib, name), name
-    assert lib.infs_abi_version() == 2
+    assert lib.infs_abi_version() == 3
 
 
 def _oracle_log(cfg, L, policy, pred):
@@ -451,3 +451,58 @@ def test_sched_optimum_budget_and_errors():
     for bad in (([0, 3], 2), ([3, 4], 0)):
         with pytest.raises(infs.InfsError):
             infs.sched_optimum(*bad)
+
+
+def test_step_launch_state_machine():
+    # infs_decode_step_layers on a dry-run context: one call decodes every
+    # layer of a step (one launch, L layers of bytes), needs a step with no
+    # layer decoded yet, checks its strides, and leaves the step for end_step.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, prompt_lens=(200,), samples_per_prompt=8,
+                                             length_dist=("uniform", 1, 40), max_suffix_len=40, pool_rows=None)
+    ctx = context_for(cfg, dry_run=True)
+    assert ctx.step_launch_workgroups == 0
+    none4 = (None, None, None, None)
+    ctx.refill_slot(0, 0, 0)
+    for layer in range(2):
+        ctx.prefill_shared(0, layer, 200, None, None)
+    assert _code(ctx.decode_step_layers, *none4) == infs.E_STATE     # layer 2 not prefilled
+    ctx.prefill_shared(0, 2, 200, None, None)
+    assert _code(ctx.decode_step_layers, *none4, 16, 0, 0) == infs.E_ARG    # stride below one layer
+    S, Hq, d = cfg.num_slots, cfg.num_q_heads, cfg.head_dim
+    assert _code(ctx.decode_step_layers, *none4, S * Hq * d * 2 + 8, 0, 0) == infs.E_ARG  # not a multiple of 16
+    ctx.decode_step_layers(*none4)
+    assert _code(ctx.decode_step, 0, *none4) == infs.E_STATE         # every layer already decoded
+    assert _code(ctx.decode_step_layers, *none4) == infs.E_STATE
+    ctx.end_step()
+    ctx.decode_step(0, *none4)
+    assert _code(ctx.decode_step_layers, *none4) == infs.E_STATE     # a layer of this step is decoded
+    ctx.decode_step(1, *none4)
+    ctx.decode_step(2, *none4)
+    ctx.end_step()
+    st = ctx.get_stats()
+    assert (st.steps, st.launches) == (2, 4)
+    assert ctx.slot_state(0) == (0, 2)
+
+
+def test_step_launch_dry_run_logs_match_layer_path():
+    # Whole groups through decode_group with the step launch and with per-layer
+    # launches: identical step logs and byte counts (the library counts the
+    # same algorithmic bytes for both).
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(0, 130, 511), samples_per_prompt=12,
+                                                length_dist=("lognormal", 3.5, 1.0, 1, 100), max_suffix_len=100,
+                                                pool_rows=None)
+    wl = Workload(cfg)
+    out = {}
+    for entry in ("decode_step", "decode_step_layers"):
+        ctx = context_for(cfg, dry_run=True)
+        for p in range(cfg.num_prompts):
+            for layer in range(cfg.layers):
+                ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
+        log = []
+        decode_group(ctx, schedulers_for(cfg, "sjf", wl.L_hat), wl.L, cfg.layers, lambda s, l: (None,) * 4,
+                     log=log, entry=entry)
+        out[entry] = (log, ctx.get_stats())
+    (la, sa), (lb, sb) = out["decode_step"], out["decode_step_layers"]
+    assert la == lb
+    assert sa.launches == cfg.layers * sb.launches == cfg.layers * len(la)
+    assert sa.alg_bytes == sb.alg_bytes and sa.tokens == sb.tokens

@@ -1,0 +1,144 @@
+"""GPU parity of the step launch through every layer (infs_decode_step_layers).
+
+Each case decodes a whole group with one launch per running step and checks,
+against the float64 oracle: the step log and the device token counters bit
+for bit, every captured output within the tolerance (1e-2 bf16, 1e-5 fp32),
+idle rows exactly 0.  Each case is also decoded with one launch per layer
+(infs_decode_step): the two differ only in the order in which a merge folds
+the split-K partials, so their outputs agree to float rounding.
+"""
+
+import numpy as np
+import pytest
+
+from paper_2506_22950_amd import infs
+from tests.gpu_harness import check_against_oracle, oracle_log, run_gpu_group, sample_steps, say
+from workload import Workload, get_config
+
+pytestmark = pytest.mark.gpu
+
+
+def _layers_case(cfg, policy, split=128, every=2, layers=None, kv_fp8=False, window=1024, against_layer_path=True,
+                 entry="decode_step_layers", scale=0.0):
+    wl = Workload(cfg)
+    want = oracle_log(cfg, wl, policy)
+    cap = sample_steps(want, every=every, edge=2, refills=8).__contains__
+    _, log, steps, captured, tokens, stats = run_gpu_group(cfg, policy, wl=wl, split=split, capture=cap,
+                                                           kv_fp8=kv_fp8, window=window, entry=entry, scale=scale)
+    assert log == want and steps == len(want), "step log differs from the oracle simulator"
+    assert np.array_equal(tokens, wl.L), "device token counters differ from the drawn lengths"
+    if entry == "decode_step_layers":
+        assert stats.launches == steps, "one launch per running step"
+    worst, n = check_against_oracle(cfg, wl, want, captured, layers=layers, kv_fp8=kv_fp8,
+                                    scale=scale if scale > 0 else None)
+    diff = 0.0
+    if against_layer_path:
+        _, _, _, per_layer, _, _ = run_gpu_group(cfg, policy, wl=wl, split=split, capture=cap, kv_fp8=kv_fp8,
+                                                 window=window, scale=scale)
+        for k in captured:
+            diff = max(diff, float(np.abs(captured[k].astype(np.float64) - per_layer[k]).max()))
+        assert diff <= 1e-5, f"step launch and per-layer launches differ by {diff:.3g}"
+    say(f"  [{cfg.name} {policy} step launch] {steps} steps, {n} outputs vs oracle max err {worst:.3g}; "
+        f"vs per-layer launches {diff:.3g}")
+
+
+_BF16_SMALL = dict(prompt_lens=(700,), samples_per_prompt=24, length_dist=("lognormal", 4.0, 1.0, 1, 300),
+                   max_suffix_len=300, pool_rows=None)
+
+
+def test_step_launch_bf16_mfma32_four_layers():
+    # The throughput workload's shape (16Q/8KV, d=128, m=16: 32 prefix rows on MFMA
+    # tiles) with four layers, so that layers wait on their predecessors.
+    _layers_case(get_config("qwen3_1p7b_g64").with_(layers=4, **_BF16_SMALL), "sjf")
+
+
+def test_step_launch_f32_wave_every_step():
+    # fp32 wavefront path, three layers, three prefix chunks, responses to 400.
+    cfg = get_config("tiny_f32").with_(layers=3, prompt_lens=(300,), length_dist=("uniform", 1, 400),
+                                       max_suffix_len=400)
+    _layers_case(cfg, "fifo", every=1)
+
+
+def test_step_launch_hpk4_three_prompts():
+    # 32Q/8KV (64 prefix rows per prompt), three prompts including an empty prefix:
+    # each prompt's layers wait only on that prompt's merges.
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=3, prompt_lens=(0, 130, 511), samples_per_prompt=20,
+                                                length_dist=("lognormal", 4.0, 1.0, 1, 260), max_suffix_len=260,
+                                                pool_rows=None)
+    _layers_case(cfg, "sjf", every=3)
+
+
+def test_step_launch_bf16_wave_single_slot():
+    # m=1: 2 prefix rows on the bf16 wavefront path.
+    cfg = get_config("qwen3_1p7b_l1_g32").with_(layers=3, slots_per_prompt=1, samples_per_prompt=4,
+                                                prompt_lens=(257,), length_dist=("lognormal", 4.0, 0.8, 1, 300),
+                                                max_suffix_len=300)
+    _layers_case(cfg, "fifo", every=5)
+
+
+def test_step_launch_wide_scores_and_scale():
+    # Wide score ranges (see test_gpu_parity) and a non-default scale through the step launch.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, **_BF16_SMALL, qk_scale=(8.0, 0.1, 8.0))
+    _layers_case(cfg, "sjf", every=3)
+    _layers_case(get_config("qwen3_1p7b_g64").with_(layers=2, **_BF16_SMALL), "sjf", every=3, scale=1.0)
+
+
+def test_step_launch_fp8_cache():
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, **_BF16_SMALL)
+    _layers_case(cfg, "sjf", every=3, kv_fp8=True)
+
+
+def test_step_launch_alternating_with_layer_launches():
+    # Step launches and per-layer launches mixed step by step in one context:
+    # the arrival counters and page tables they share stay consistent.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, **_BF16_SMALL)
+    _layers_case(cfg, "sjf", every=2, entry=lambda step: "decode_step_layers" if step % 2 else "decode_step")
+
+
+@pytest.mark.parametrize("name,every,window", [
+    ("qwen3_1p7b_g64", 397, 512),
+    ("longtail_g128", 997, 256),
+    ("qwen3_8b_4prompts", 1201, 128),
+])
+def test_step_launch_full_size_sampled(name, every, window):
+    # Whole workload, one step launch per running step (the benchmark's
+    # configuration); sampled steps on the first, middle and last layer.
+    cfg = get_config(name)
+    _layers_case(cfg, cfg.policy, split=0, every=every, layers=(0, cfg.layers // 2, cfg.layers - 1),
+                 window=window, against_layer_path=False)
+
+
+def test_step_launch_wait_give_up_is_reported():
+    # Every wait of the step launch bounded: forced to give up at once from the
+    # host, merges write NaN, the launch runs to its end, and the next
+    # synchronising call reports E_DEVICE.
+    import torch
+
+    from paper_2506_22950_amd.group import context_for
+    from workload.staging import DeviceInputs
+
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, **_BF16_SMALL)
+    wl = Workload(cfg)
+    dev = DeviceInputs(wl)
+    ctx = context_for(cfg, stream=torch.cuda.current_stream())
+    assert ctx.step_launch_workgroups > 0
+    keep = []
+    for layer in range(cfg.layers):
+        k, v = dev.prefix(layer, 0)
+        keep.append((k, v))
+        ctx.prefill_shared(0, layer, cfg.prompt_lens[0], k, v)
+    ctx.refill_slot(0, 0, 0)
+    ctx.refill_slot(3, 0, 1)
+    L, S, Hq, Hkv, d = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    q = torch.zeros((L, S, Hq, d), dtype=torch.int16, device="cuda")
+    kn = torch.zeros((L, S, Hkv, d), dtype=torch.int16, device="cuda")
+    o = torch.zeros((L, S, Hq, d), dtype=torch.float32, device="cuda")
+    ctx.set_merge_wait(-1)
+    ctx.decode_step_layers(q, kn, kn, o)
+    ctx.end_step()
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.sync()
+    assert ei.value.status == infs.E_DEVICE
+    assert torch.isnan(o[:, 0]).all() and torch.isnan(o[:, 3]).all()
+    assert not o[:, 1].any() and not o[:, 2].any()
+    ctx.destroy()
