@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace infs {
@@ -423,6 +425,9 @@ __device__ __forceinline__ void wave_combine_groups(float (&m)[NR], float (&l)[N
   }
 }
 
+template <class SH, int NR, bool L2>
+__device__ __forceinline__ void combine_store_partial(float* smem, const Exchange<L2>& ex, int64_t rec0);
+
 // Combine the four wavefronts' partials through LDS and store the block's
 // partial rows [0, NR) at records rec0 + r.
 template <class SH, int NR, bool L2>
@@ -446,6 +451,18 @@ __device__ __forceinline__ void block_store_partial(float* smem, const float (&m
       sml[(w * NR + r) * 2 + 1] = l[r];
     }
   }
+  combine_store_partial<SH, NR, L2>(smem, ex, rec0);
+}
+
+// Second half of block_store_partial: after every wavefront has published its
+// partial rows to LDS (so = [4][NR][D] unnormalised outputs, then
+// sml = [4][NR][2] (m, l)), combine them and store rows [0, NR) at records
+// rec0 + r.
+template <class SH, int NR, bool L2>
+__device__ __forceinline__ void combine_store_partial(float* smem, const Exchange<L2>& ex, int64_t rec0) {
+  constexpr int D = SH::D;
+  const float* so = smem;
+  const float* sml = smem + 4 * NR * D;
   __syncthreads();
   for (int idx = threadIdx.x; idx < NR * D; idx += kBlockThreads) {
     const int r = idx / D, d = idx - r * D;
@@ -494,6 +511,256 @@ struct SuffixAddr {
   __device__ const char* row(int kind, int tokbase, int, int pg, int) const {
     const int lane = threadIdx.x & 63;
     return pool + ((int64_t)(pg * hkv + g) * 2 + kind) * SH::PAGEB + (tokbase & 15) * SH::KROWB + lane * SH::LANEB;
+  }
+};
+
+// ----------------------------------------------------------------------------
+// Response chunk on MFMA tiles (bf16 and E4M3 pages).  A page holds 16 tokens
+// of one KV head, K then V, each in MFMA operand order:
+//   K unit (kb, lane), 8 elements: token lane%16, dims 32kb + 8(lane/16) + e;
+//   V unit (db, lane), 4 elements: dim 16db + lane%16, tokens 4(lane/16) + e;
+// so a wavefront reads one operand tile with one coalesced load per lane
+// (16 / 8 bytes for bf16).  Per page, S^T[tok][col] = K[tok] . Q[col] is one
+// 16x16 tile (A = K units, B = Q^T, col = query row of the KV head: HPK of
+// the 16 columns carry rows, the rest are zero).  Two consecutive pages form
+// one 32-token k-block of O^T[d][col] += V^T[d][tok] P^T[tok][col]: the P^T
+// operand is the eight probabilities a lane holds after the pages' two S^T
+// tiles (the first page's four, then the second's) and the V^T operand is the
+// two pages' V units side by side, so the contraction index is the same
+// token permutation on both operands.  The running (m, l) and O^T are indexed
+// by col = lane % 16 as on the prefix tiles; l is a per-lane sum until
+// publish() adds the four lane groups.
+// ----------------------------------------------------------------------------
+template <class SH>
+struct RespMfma {
+  static constexpr int D = SH::D, KB = SH::KB, DB = SH::DB, HPK = SH::HPK, KES = SH::KES;
+  static constexpr int NPG = D >= 128 ? 4 : 8;        // pages per load round
+  static constexpr int TOK = 16 * NPG;                // tokens per load round
+  static constexpr int KUB = 8 * KES, VUB = 4 * KES;  // bytes of one K / V unit
+  using KUnit = std::conditional_t<SH::KV8, u32x2, u32x4>;
+  using VUnit = std::conditional_t<SH::KV8, uint32_t, u32x2>;
+  using VPair = std::conditional_t<SH::KV8, u32x2, u32x4>;  // two pages' V units, side by side
+  struct Regs {
+    KUnit k[NPG][KB];
+    VPair v[NPG / 2][DB];
+  };
+  static constexpr int kLoads = NPG * (KB + DB);  // load instructions of one round
+  // Running partial: O^T tiles, m per column and, in lt, the column's sum of
+  // probabilities (every element; an all-ones V^T tile through the same MFMA).
+  struct Acc {
+    f32x4 o[DB];
+    f32x4 lt;
+    float m;
+  };
+  // The newest token's rows, loaded with the queries: kq[kb] = K dims
+  // 32kb + 8(lane/16) .. +7 and vq[db] = V dims 16db + 4(lane/16) .. +3.
+  struct NewRows {
+    u32x4 kq[KB];
+    u32x2 vq[DB];
+  };
+  static_assert(HPK <= 16 && KB * 32 == D && DB * 16 == D, "response tile shape");
+
+  __device__ __forceinline__ static int k_unit(int kb, int lane) { return (kb * 64 + lane) * KUB; }
+  __device__ __forceinline__ static int v_unit(int db, int lane) { return (db * 64 + lane) * VUB; }
+  // Page pg of KV head g: K at the returned address, V PAGEB bytes later.
+  __device__ __forceinline__ static const char* page(const char* pool, int pg, int hkv, int g) {
+    return pool + (int64_t)(pg * hkv + g) * 2 * SH::PAGEB;
+  }
+
+  // Loads of the round whose first page is entry ps of the wavefront's page
+  // list (lane i of `pages`: its i-th page; entries past the range name page
+  // 0, so every load stays inside the pool).  K of every page, then V, each
+  // pair's V units straight into one MFMA operand register.
+  __device__ __forceinline__ static void load_round(const char* pool, int pages, int hkv, int g, int ps, Regs& R) {
+    const int lane = threadIdx.x & 63;
+    const char* pp[NPG];
+#pragma unroll
+    for (int pr = 0; pr < NPG; ++pr) pp[pr] = page(pool, __builtin_amdgcn_readlane(pages, min(ps + pr, 63)), hkv, g);
+#pragma unroll
+    for (int pr = 0; pr < NPG; ++pr)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) R.k[pr][kb] = __builtin_nontemporal_load((const KUnit*)(pp[pr] + k_unit(kb, lane)));
+#pragma unroll
+    for (int j = 0; j < NPG / 2; ++j)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const VUnit a0 = __builtin_nontemporal_load((const VUnit*)(pp[2 * j] + SH::PAGEB + v_unit(db, lane)));
+        const VUnit a1 = __builtin_nontemporal_load((const VUnit*)(pp[2 * j + 1] + SH::PAGEB + v_unit(db, lane)));
+        if constexpr (SH::KV8)
+          R.v[j][db] = u32x2{a0, a1};
+        else
+          R.v[j][db] = __builtin_shufflevector(a0, a1, 0, 1, 2, 3);
+      }
+  }
+
+  __device__ __forceinline__ static bf16x8 k_op(const KUnit& u) {
+    if constexpr (SH::KV8)
+      return __builtin_bit_cast(bf16x8, widen_e4m3(uint2{u.x, u.y}));
+    else
+      return __builtin_bit_cast(bf16x8, u);
+  }
+  __device__ __forceinline__ static u32x4 v_op(const VPair& u) {  // eight elements as bf16
+    if constexpr (SH::KV8)
+      return widen_e4m3(uint2{u.x, u.y});
+    else
+      return u;
+  }
+  // Bits of elements 2k and 2k + 1 of a four-element V unit that belong to
+  // the first n tokens.
+  __device__ __forceinline__ static uint32_t keep(int n, int k) {
+    return (n > 2 * k ? 0x0000ffffu : 0u) | (n > 2 * k + 1 ? 0xffff0000u : 0u);
+  }
+
+  // Q^T operand: lane l holds query row row0 + l%16 (zero from HPK on), dims
+  // 32kb + 8(l/16) .. +7.
+  __device__ __forceinline__ static void load_q(const void* q, int64_t row0, bf16x8 (&bq)[KB]) {
+    const int lane = threadIdx.x & 63, col = lane & 15, h = lane >> 4;
+    const uint16_t* qr = (const uint16_t*)q + (row0 + col) * D + h * 8;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) bq[kb] = col < HPK ? *(const bf16x8*)(qr + kb * 32) : bf16x8{};
+  }
+  // The newest token's K / V rows (bf16, the caller's row layout), rounded to
+  // E4M3 and back for E4M3 pages: the token is attended as its page stores it.
+  __device__ __forceinline__ static void load_new(const char* krow, const char* vrow, NewRows& N) {
+    const int h = (threadIdx.x & 63) >> 4;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) N.kq[kb] = *(const u32x4*)(krow + (kb * 32 + h * 8) * 2);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) N.vq[db] = *(const u32x2*)(vrow + (db * 16 + h * 4) * 2);
+  }
+  __device__ __forceinline__ static void round_new(NewRows& N) {
+    if constexpr (SH::KV8) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) N.kq[kb] = widen_e4m3(narrow_e4m3(N.kq[kb]));
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int b = (int)narrow4_e4m3(N.vq[db].x, N.vq[db].y);
+        N.vq[db] = u32x2{__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(b, 1.0f, false)),
+                         __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(b, 1.0f, true))};
+      }
+    }
+  }
+
+  // A partial that holds only the newest token (A's first contribution).
+  __device__ __forceinline__ static void start_new(const NewRows& N, const bf16x8 (&bq)[KB], float sl2, Acc& A) {
+    float s = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) s += dot16B<true>(N.kq[kb], __builtin_bit_cast(u32x4, bq[kb]));
+    s += __shfl_xor(s, 16);
+    s += __shfl_xor(s, 32);
+    // the token's own weight is 2^(x - m) = 1 with m = x
+    A.m = s * sl2;
+    A.lt = f32x4{1.f, 1.f, 1.f, 1.f};
+#pragma unroll
+    for (int db = 0; db < DB; ++db) A.o[db] = f32x4{bf_lo(N.vq[db].x), bf_hi(N.vq[db].x), bf_lo(N.vq[db].y), bf_hi(N.vq[db].y)};
+  }
+
+  __device__ __forceinline__ static void init(Acc& A) {
+    A.m = NEG_INF;
+    A.lt = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int db = 0; db < DB; ++db) A.o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // Tokens base .. base + TOK - 1 (the round held in R), of which those below
+  // t1 count: one online-softmax step per page pair (32 tokens).
+  __device__ __forceinline__ static void round(const Regs& R, const bf16x8 (&bq)[KB], int base, int t1, float sl2,
+                                               Acc& A) {
+    const int lane = threadIdx.x & 63, h = lane >> 4;
+    const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+    for (int j = 0; j < NPG / 2; ++j) {
+      const int pb0 = base + 32 * j;
+      if (pb0 >= t1) break;
+      // a pair that reaches past t1 masks its tail (scores and V elements)
+      const bool edge = pb0 + 32 > t1;
+      f32x4 st[2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        f32x4 t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_op(R.k[2 * j + mb][kb]), bq[kb], t, 0, 0, 0);
+        t *= sl2;
+        if (edge) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) t[e] = (pb0 + 16 * mb + 4 * h + e < t1) ? t[e] : NEG_INF;
+        }
+        st[mb] = t;
+      }
+      float mx = fmaxf(fmaxf(fmaxf(st[0][0], st[0][1]), fmaxf(st[0][2], st[0][3])),
+                       fmaxf(fmaxf(st[1][0], st[1][1]), fmaxf(st[1][2], st[1][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(A.m, mx);
+      const float mu = (mn == NEG_INF) ? 0.f : mn;
+      const float corr = exp2_fast(A.m - mu);
+      A.m = mn;
+      A.lt *= corr;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) A.o[db] *= corr;
+      bf16x8 pb;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        pb[e] = (__bf16)exp2_fast(st[0][e] - mu);
+        pb[4 + e] = (__bf16)exp2_fast(st[1][e] - mu);
+      }
+      A.lt = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb, A.lt, 0, 0, 0);
+      // V elements of tokens at or past t1 (a page's unused tail holds whatever
+      // was there) are cleared so that their zero weights give exact zeros.
+      const int n0 = min(max(t1 - (pb0 + 4 * h), 0), 4), n1 = min(max(t1 - (pb0 + 16 + 4 * h), 0), 4);
+      const u32x4 vm = {keep(n0, 0), keep(n0, 1), keep(n1, 0), keep(n1, 1)};
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        u32x4 va = v_op(R.v[j][db]);
+        if (edge) va &= vm;
+        A.o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va), pb, A.o[db], 0, 0, 0);
+      }
+    }
+  }
+
+  // Store the newest token (position t, 0..15, of the page at pgk) in operand
+  // order from the rows in N: K unit (kb, 16h + t) from the lanes with
+  // lane % 16 == 0 (lane group h), V element (dim 16db + 4h + i, token t) from
+  // lane 16h + i, i < 4.
+  __device__ __forceinline__ static void store_new(char* pgk, int t, const NewRows& N) {
+    const int lane = threadIdx.x & 63, h = lane >> 4, i = lane & 15;
+    if (i == 0) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) st_kv<SH>(pgk + k_unit(kb, h * 16 + t), N.kq[kb]);
+    }
+    if (i < 4) {
+      char* vb = pgk + SH::PAGEB + (t & 3) * KES;
+      const int l0 = 16 * (t >> 2) + 4 * h + i;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint32_t w = (i & 2) ? N.vq[db].y : N.vq[db].x;
+        const uint32_t bits = (i & 1) ? (w >> 16) : (w & 0xffffu);
+        if constexpr (SH::KV8) {
+          // N.vq holds E4M3 values widened to bf16: narrowing again is exact
+          const uint32_t b = narrow4_e4m3(bits, 0u) & 0xffu;
+          *(uint8_t*)(vb + v_unit(db, l0)) = (uint8_t)b;
+        } else {
+          *(uint16_t*)(vb + v_unit(db, l0)) = (uint16_t)bits;
+        }
+      }
+    }
+  }
+
+  // Publish the wavefront's partial rows to LDS in block_store_partial's
+  // layout (finish with combine_store_partial<SH, HPK, L2>).
+  __device__ __forceinline__ static void publish(float* smem, const Acc& A) {
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, col = lane & 15, h = lane >> 4;
+    float* so = smem;
+    float* sml = smem + 4 * HPK * D;
+    if (col < HPK) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) *(f32x4*)(so + (w * HPK + col) * D + db * 16 + h * 4) = A.o[db];
+      if (h == 0) {
+        sml[(w * HPK + col) * 2 + 0] = A.m;
+        sml[(w * HPK + col) * 2 + 1] = A.lt[0];
+      }
+    }
   }
 };
 
@@ -740,7 +1007,14 @@ __device__ void prefix_mfma(const StepArgs& a, int p, int c, int g, float* smem)
 // K/V when the chunk holds the newest position.
 // ----------------------------------------------------------------------------
 template <class SH, bool L2>
+__device__ void suffix_chunk_mfma(const StepArgs& a, int s, int c, int g, float* smem);
+
+template <class SH, bool L2>
 __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem) {
+  if constexpr (SH::BF) {
+    suffix_chunk_mfma<SH, L2>(a, s, c, g, smem);
+    return;
+  }
   constexpr int HPK = SH::HPK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, ch = lane % SH::LPT;
   const SlotPlan& sp = a.slot[s];
@@ -787,6 +1061,62 @@ __device__ void suffix_chunk(const StepArgs& a, int s, int c, int g, float* smem
   wave_combine_groups<SH, HPK>(m, l, o);
   const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.Hkv + g) * a.suffix_chunks_max + c) * HPK;
   block_store_partial<SH, HPK, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
+
+  if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
+    const int pos = len - 1;
+    a.page_table[(int64_t)sp.seq * a.pages_per_slot + (pos >> 4)] = sp.cur_page;
+    if (a.count_tokens)
+      __hip_atomic_fetch_add(&a.tokens[(s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Response chunk of one live slot on MFMA tiles (bf16 and E4M3 pages; see
+// RespMfma): wavefront w takes tokens [wt0, wt1) of the chunk in rounds of
+// RespMfma::TOK; the wavefront whose range holds the newest position starts
+// from that token (read from the caller's rows together with the queries) and
+// stores it into its page; the four wavefronts' partials combine through LDS.
+template <class SH, bool L2>
+__device__ void suffix_chunk_mfma(const StepArgs& a, int s, int c, int g, float* smem) {
+  using RM = RespMfma<SH>;
+  constexpr int HPK = SH::HPK;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const SlotPlan& sp = a.slot[s];
+  const int len = sp.len;
+  const int t0 = c * a.split, t1 = min(t0 + a.split, len);
+  const int sub = a.split / 4;
+  const int wt0 = min(t0 + w * sub, t1), wt1 = min(wt0 + sub, t1);
+  const int npg = (wt1 - wt0 + kPageTokens - 1) / kPageTokens;
+  const int32_t* ptab = a.page_table + (int64_t)sp.seq * a.pages_per_slot + (wt0 >> 4);
+  const int pages = lane < npg ? ptab[lane] : 0;
+  const int last = len - 1;
+  const bool has_new = last >= wt0 && last < wt1;
+  const int te = has_new ? last : wt1;  // stored tokens of this wavefront: [wt0, te)
+  typename RM::Regs R;
+  RM::load_round((const char*)a.pool, pages, a.Hkv, g, 0, R);
+  // queries and the newest token's rows in one batch of loads; that token is
+  // folded in first and stored into its page
+  bf16x8 bq[SH::KB];
+  RM::load_q(a.q, (int64_t)s * a.Hq + g * HPK, bq);
+  typename RM::NewRows N;
+  if (has_new) {
+    const int64_t newrow = ((int64_t)s * a.Hkv + g) * SH::ROWB;
+    RM::load_new((const char*)a.knew + newrow, (const char*)a.vnew + newrow, N);
+  }
+  typename RM::Acc A;
+  if (has_new) {
+    RM::round_new(N);
+    RM::start_new(N, bq, a.scale_log2, A);
+    RM::store_new((char*)RM::page((const char*)a.pool, sp.cur_page, a.Hkv, g), last & 15, N);
+  } else {
+    RM::init(A);
+  }
+  for (int base = wt0; base < te; base += RM::TOK) {
+    if (base != wt0) RM::load_round((const char*)a.pool, pages, a.Hkv, g, (base - wt0) >> 4, R);
+    RM::round(R, bq, base, te, a.scale_log2, A);
+  }
+  RM::publish(smem, A);
+  const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)s * a.Hkv + g) * a.suffix_chunks_max + c) * HPK;
+  combine_store_partial<SH, HPK, L2>(smem, Exchange<L2>(a), rec0);
 
   if (t1 == len && g == 0 && threadIdx.x == 0) {  // bookkeeping of this step's token (K/V stored above)
     const int pos = len - 1;

@@ -487,7 +487,7 @@ struct PrefixMfma {
   }
 };
 
-// ---- Response chunk (see suffix_chunk) --------------------------------------
+// ---- Response chunk, fp32 pages on wavefront dot products (see suffix_chunk) -
 struct RespItem {
   int s, c, len, wt0, wt1, last;
   bool has_new;
@@ -572,6 +572,57 @@ struct Resp {
     }
     const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)r.s * a.Hkv + g) * a.suffix_chunks_max + r.c) * HPK;
     block_store_partial<SH, HPK, false>(smem, m, l, o, Exchange<false>(a), rec0);
+    after_stores();
+  }
+};
+
+// The same response item on MFMA tiles (bf16 and E4M3 pages; see RespMfma):
+// issue() loads the wavefront's first round, finish() runs the rest once the
+// item's queries may be read.
+template <class SH>
+struct RespTiles {
+  using RM = RespMfma<SH>;
+  using Regs = typename RM::Regs;
+  static constexpr int HPK = SH::HPK;
+  static constexpr int kLoads = RM::kLoads;
+  __device__ __forceinline__ static void issue(const StepArgs& a, const LayerView& V, const RespItem& r, int pages, int g, Regs& R) {
+    RM::load_round(V.pool, pages, a.Hkv, g, 0, R);
+  }
+  template <class Before, class After>
+  __device__ __forceinline__ static void finish(const StepArgs& a, const LayerView& V, const RespItem& r, int pages, int g,
+                                float* smem, Regs& R, Before&& before, After&& after_stores) {
+    const SlotPlan& sp = a.slot[r.s];
+    const int te = r.has_new ? r.last : r.wt1;
+    before();
+    // queries and the newest token's rows in one batch of loads, issued as soon
+    // as the layer may read them; that token is folded in first
+    bf16x8 bq[SH::KB];
+    RM::load_q(V.q, (int64_t)r.s * a.Hq + g * HPK, bq);
+    typename RM::NewRows N;
+    if (r.has_new) {
+      const int64_t newrow = ((int64_t)r.s * a.Hkv + g) * SH::ROWB;
+      RM::load_new(V.knew + newrow, V.vnew + newrow, N);
+    }
+    typename RM::Acc A;
+    if (r.has_new) {
+      RM::round_new(N);
+      RM::start_new(N, bq, a.scale_log2, A);
+      RM::store_new((char*)RM::page(V.pool, sp.cur_page, a.Hkv, g), r.last & 15, N);
+    } else {
+      RM::init(A);
+    }
+    for (int base = r.wt0; base < te; base += RM::TOK) {
+      if (base != r.wt0) RM::load_round(V.pool, pages, a.Hkv, g, (base - r.wt0) >> 4, R);
+      RM::round(R, bq, base, te, a.scale_log2, A);
+    }
+    if (V.layer == 0 && r.c * a.split + a.split >= r.len && g == 0 && threadIdx.x == 0) {
+      // bookkeeping of this step's token, once per step (its K/V are stored above)
+      a.page_table[(int64_t)sp.seq * a.pages_per_slot + (r.last >> 4)] = sp.cur_page;
+      __hip_atomic_fetch_add(&a.tokens[(r.s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    RM::publish(smem, A);
+    const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)r.s * a.Hkv + g) * a.suffix_chunks_max + r.c) * HPK;
+    combine_store_partial<SH, HPK, false>(smem, Exchange<false>(a), rec0);
     after_stores();
   }
 };
@@ -708,7 +759,7 @@ template <class SH>
 __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, float* smem) {
   if (jr >= a.n_suffix_items) return;
   const int nk = (a.n_suffix_items - jr + a.n_suf_wg - 1) / a.n_suf_wg;
-  using P = Resp<SH>;
+  using P = std::conditional_t<SH::BF, RespTiles<SH>, Resp<SH>>;
   typename P::Regs R;
   RespItem it = resp_item(a, jr);
   int pages = resp_pages(a, it);

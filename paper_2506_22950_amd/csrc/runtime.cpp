@@ -1172,10 +1172,26 @@ infs_status infs_read_response(infs_ctx* c, int32_t slot, int32_t layer, void* k
                          hipMemcpyDeviceToHost));
     for (int r = 0; r < infs::kPageTokens && lp * infs::kPageTokens + r < len; ++r) {
       const int tok = lp * infs::kPageTokens + r;
-      for (int g = 0; g < Hkv; ++g)
-        for (int kind = 0; kind < 2; ++kind)
-          std::memcpy(out[kind] + ((size_t)tok * Hkv + g) * rowb,
-                      buf.data() + ((size_t)g * 2 + kind) * pageb + (size_t)r * rowb, rowb);
+      for (int g = 0; g < Hkv; ++g) {
+        const uint8_t* kp = buf.data() + (size_t)g * 2 * pageb;
+        const uint8_t* vp = kp + pageb;
+        uint8_t* kd = out[0] + ((size_t)tok * Hkv + g) * rowb;
+        uint8_t* vd = out[1] + ((size_t)tok * Hkv + g) * rowb;
+        if (!c->key.bf16) {  // fp32 pages: token rows
+          std::memcpy(kd, kp + (size_t)r * rowb, rowb);
+          std::memcpy(vd, vp + (size_t)r * rowb, rowb);
+          continue;
+        }
+        // bf16 / E4M3 pages in MFMA operand order: K unit (kb, lane) holds token
+        // lane % 16, dims 32 kb + 8 (lane / 16) + e; V unit (db, lane) holds dim
+        // 16 db + lane % 16, tokens 4 (lane / 16) + e.
+        for (int d = 0; d < D; ++d) {
+          const size_t ku = (size_t)((d / 32) * 64 + ((d % 32) / 8) * 16 + r) * 8 + d % 8;
+          const size_t vu = (size_t)((d / 16) * 64 + (r / 4) * 16 + d % 16) * 4 + r % 4;
+          std::memcpy(kd + d * es, kp + ku * es, es);
+          std::memcpy(vd + d * es, vp + vu * es, es);
+        }
+      }
     }
   }
   return INFS_OK;
