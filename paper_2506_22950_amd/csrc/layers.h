@@ -29,6 +29,18 @@
 // Every wait is bounded by merge_polls (and gives up at once once any wait of
 // the launch has given up, or when merge_polls < 0); a wait that gives up sets
 // the status word and the launch runs to its end with invalid outputs.
+//
+// Memory-queue sharing.  The GPU keeps two of these work-groups on every CU,
+// and the vector memory instructions of a CU pass through one queue to the
+// memory system, which a CU drains at a bounded rate.  A work-group that
+// issues its next layer's K/V loads while the other work-group of its CU
+// still has this layer's partial stores or merges to do puts those behind
+// the whole stream.  So a response work-group issues its next layer's loads
+// only once its CU mate is past its part of the layer (or after a short
+// bound), and a prefix work-group -- whose chunk is small and whose partial
+// is needed early -- loads its next layer's chunk only when that layer may
+// start.  Which work-groups share a CU is read from the hardware (see
+// mate_gate); none of this affects results.
 #pragma once
 #include <type_traits>
 
@@ -712,6 +724,48 @@ __device__ void merge_wave(const StepArgs& a, const LayerView& V, int s, int g, 
   }
 }
 
+// Hardware id of the CU running this work-group (XCD, shader engine, array, CU).
+__device__ __forceinline__ int32_t cu_id() {
+  const int32_t hw = __builtin_amdgcn_s_getreg(4 | (31 << 11));  // HW_REG_HW_ID: CU id in bits 8..15
+  return ((hw >> 8) & 0xff) | ((__builtin_amdgcn_s_getreg(kXccIdReg) & 15) << 8);
+}
+__device__ __forceinline__ int32_t* peer_line(const StepArgs& a, int b) { return a.peer + (int64_t)b * kCounterStride; }
+// Wavefront w of this work-group (a producer: the work-group, w = 0) is done with layer l.
+__device__ __forceinline__ void peer_mark(const StepArgs& a, int l, int w) {
+  __hip_atomic_store(peer_line(a, blockIdx.x) + w, (int32_t)((uint32_t)a.peer_base + (uint32_t)l + 1u),
+                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// All threads of a producer work-group that is done with layer l: wait until
+// the other work-group of its CU is too, at most kMateWaitTicks.  The grid
+// holds two work-groups per CU and the dispatcher gives every CU one before
+// any gets a second, so work-group b shares its CU with b +- gridDim.x / 2,
+// which for KV head g is index j +- nj / 2; the pair waits only when the CU
+// ids they recorded at their start agree.
+__device__ void mate_gate(const StepArgs& a, int l) {
+  const int nj = gridDim.x / a.Hkv;
+  if (threadIdx.x < kWaves && (nj & 1) == 0 && a.merge_polls >= 0) {
+    const int g = blockIdx.x % a.Hkv, j = blockIdx.x / a.Hkv;
+    const int jm = j < nj / 2 ? j + nj / 2 : j - nj / 2;
+    const int w = threadIdx.x;
+    bool need;
+    if (jm < a.n_pre_wg)
+      need = w == 0 && jm < a.n_prefix_items;
+    else if (jm < a.n_pre_wg + a.n_suf_wg)
+      need = w == 0 && jm - a.n_pre_wg < a.n_suffix_items;
+    else
+      need = (jm - a.n_pre_wg - a.n_suf_wg) * kWaves + w < a.n_merge_items + a.n_zero_items;
+    const int32_t* line = peer_line(a, jm * a.Hkv + g);
+    if (need && __hip_atomic_load(line + 4, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == cu_id() + 1) {
+      const int32_t target = (int32_t)((uint32_t)a.peer_base + (uint32_t)l + 1u);
+      const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+      while (__hip_atomic_load(line + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target < 0 &&
+             __builtin_amdgcn_s_memrealtime() - t0 < (uint64_t)kMateWaitTicks)
+        __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  __syncthreads();
+}
+
 // Layer l > 0 of prompt p may start once the prompt's layer l-1 is merged;
 // `ready` remembers the prompts a work-group has already seen done in l.
 __device__ __forceinline__ void layer_gate(const StepArgs& a, int p, int l, uint32_t& ready) {
@@ -722,39 +776,40 @@ __device__ __forceinline__ void layer_gate(const StepArgs& a, int p, int l, uint
 }
 
 // Prefix-chunk work-group jp of KV head g: prefix items jp, jp + n_pre_wg, ...
-// of every layer.  After storing an item's partial it issues the next item's
-// loads (the same chunk of the next layer, when it has one chunk per layer),
-// then waits only for its stores before counting the arrival.
+// of every layer.  The layer's first item is loaded once the layer may start;
+// a later item of the same layer is loaded right behind the previous item's
+// stores.
 template <class SH>
 __device__ __forceinline__ void prefix_loop(const StepArgs& a, int g, int jp, float* smem) {
   if (jp >= a.n_prefix_items) return;
   const int nk = (a.n_prefix_items - jp + a.n_pre_wg - 1) / a.n_pre_wg;
   using P = std::conditional_t<SH::MFMA, PrefixMfma<SH>, PrefixWave<SH>>;
   typename P::Regs R;
-  P::issue(a, layer_view(a, 0), prefix_item(a, jp), g, R);
   for (int l = 0; l < a.num_layers; ++l) {
     const LayerView V = layer_view(a, l);
     uint32_t ready = 0;
     for (int k = 0; k < nk; ++k) {
       const PrefixItem it = prefix_item(a, jp + k * a.n_pre_wg);
-      const bool has_next = k + 1 < nk || l + 1 < a.num_layers;
-      const int ln = k + 1 < nk ? l : l + 1;
+      if (k == 0) {
+        layer_gate(a, it.p, l, ready);
+        P::issue(a, V, it, g, R);
+      }
       P::finish(a, V, it, g, smem, R, [&]() { layer_gate(a, it.p, l, ready); },
                 [&]() {
-                  if (!has_next) {
-                    arrive_behind<0>(a, it.p * a.m, a.m, g);
-                    return;
-                  }
-                  const PrefixItem nx = prefix_item(a, jp + (k + 1 < nk ? k + 1 : 0) * a.n_pre_wg);
                   arrive_behind<0>(a, it.p * a.m, a.m, g);
-                  P::issue(a, layer_view(a, ln), nx, g, R);
+                  if (k + 1 < nk)
+                    P::issue(a, V, prefix_item(a, jp + (k + 1) * a.n_pre_wg), g, R);
+                  else if (threadIdx.x == 0)
+                    peer_mark(a, l, 0);
                 });
     }
   }
 }
 
 // Response-chunk work-group jr of KV head g: response items jr, jr + n_suf_wg,
-// ... of every layer, each with the next item's loads issued behind its stores.
+// ... of every layer, each with the next item's loads issued behind its stores
+// (behind the CU mate's part of the layer when the next item is in the next
+// layer).
 template <class SH>
 __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, float* smem) {
   if (jr >= a.n_suffix_items) return;
@@ -775,6 +830,7 @@ __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, fl
                 [&]() {
                   if (!has_next) {
                     arrive_behind<0>(a, it.s, 1, g);
+                    if (threadIdx.x == 0) peer_mark(a, l, 0);
                     return;
                   }
                   // With one item per layer the next item is this one in the next layer, on the same
@@ -783,6 +839,10 @@ __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, fl
                   const RespItem nx = resp_item(a, jr + (k + 1 < nk ? k + 1 : 0) * a.n_suf_wg);
                   if (nk != 1) pages = resp_pages(a, nx);
                   arrive_behind<0>(a, it.s, 1, g);
+                  if (ln != l) {  // the next item is in the next layer: let the CU mate finish this one first
+                    if (threadIdx.x == 0) peer_mark(a, l, 0);
+                    mate_gate(a, l);
+                  }
                   P::issue(a, layer_view(a, ln), nx, pages, g, R);
                 });
     }
@@ -822,6 +882,7 @@ __device__ void merge_loop(const StepArgs& a, int g, int mj) {
         for (int x = lane * 4; x < SH::HPK * SH::D; x += 256) *(f32x4*)(orow + x) = f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
+    if (lane == 0) peer_mark(a, l, w);
   }
 }
 
@@ -834,6 +895,7 @@ __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void layers_kernel(co
   if (a.clock_start && threadIdx.x == 0)
     __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) __hip_atomic_store(peer_line(a, blockIdx.x) + 4, cu_id() + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int g = blockIdx.x % a.Hkv, j = blockIdx.x / a.Hkv;
   if (j < a.n_pre_wg)
     prefix_loop<SH>(a, g, j, smem);

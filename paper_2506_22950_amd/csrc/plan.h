@@ -24,6 +24,7 @@ constexpr int kCounterStride = 32;     // int32 per arrival counter: each counte
 constexpr int kRecordsPerLine = 16;   // (max, sum) records of 8 bytes per 128-byte line
 constexpr int kClockSlots = 16;        // timing slots per launch (see StepArgs::clock_start)
 constexpr int kClockStride = 16;       // uint64 per timing slot: one 128-byte line each
+constexpr int kMateWaitTicks = 2000;   // bound on a step-launch work-group's wait for its CU mate (100 MHz ticks)
 // Size of the file-scope device array that holds the split-K workspace and the
 // arrival counters of infs_decode_step_static (one copy per GPU, kept until the
 // process ends).
@@ -112,6 +113,10 @@ struct StepArgs {
   int32_t merged_base[kMaxPrompts];    // value of each prompt's merged counter before this launch
   int32_t merged_per_layer[kMaxPrompts];  // merges of each prompt per layer: its live slots * Hkv
   uint64_t live_mask;                  // bit s set: slot s is live this step
+  int32_t* peer;                       // per work-group of the launch, kCounterStride apart: words 0..3 =
+                                       // peer_base + l + 1 once its wavefront w (a producer: the whole
+                                       // work-group, word 0) is done with layer l; word 4 = its CU id + 1
+  int32_t peer_base;                   // progress value before this launch (grows by num_layers a launch)
   // this step
   int32_t n_prefix_items, n_suffix_items, n_zero_items, n_merge_items;
   int32_t num_prompts;

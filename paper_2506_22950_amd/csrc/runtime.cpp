@@ -86,6 +86,7 @@ struct infs_ctx {
   std::vector<uint32_t> slot_arrivals;
   // Merges each prompt's "merged" counter has counted so far (step launches only).
   std::vector<uint32_t> merged_arrivals;
+  uint32_t peer_progress = 0;  // peer-line progress value reached by the step launches so far
   bool step_open = false;
   // Probe phase of prefix reuse.
   int probe_k = 0;                                 // probe tokens per sample (0: no prefix reuse)
@@ -166,14 +167,17 @@ void free_device(infs_ctx* c) {
 
 // Counters: one per (slot, KV head) for decode launches [S][Hkv], then the
 // probe launches' own [kMaxSlots][Hkv], then for step launches one "merged"
-// counter per prompt and one layer-done flag per (prompt, KV head); each on a
-// 128-byte line of its own.
+// counter per prompt, one layer-done flag per (prompt, KV head) and one peer
+// line per work-group; each on a 128-byte line of its own.
 size_t counter_lines(const infs_ctx* c) {
-  return (size_t)(c->S + infs::kMaxSlots) * c->Hkv + c->NP + (size_t)c->NP * c->Hkv;
+  return (size_t)(c->S + infs::kMaxSlots) * c->Hkv + c->NP + (size_t)c->NP * c->Hkv + (size_t)c->layers_resident;
 }
 size_t counter_bytes(const infs_ctx* c) { return sizeof(int32_t) * infs::kCounterStride * counter_lines(c); }
 int32_t* merged_counters(const infs_ctx* c) {
   return c->counters + (size_t)(c->S + infs::kMaxSlots) * c->Hkv * infs::kCounterStride;
+}
+int32_t* peer_lines(const infs_ctx* c) {
+  return merged_counters(c) + ((size_t)c->NP + (size_t)c->NP * c->Hkv) * infs::kCounterStride;
 }
 
 // Split-K record capacities.  Records are numbered (prompt, KV head)-major for
@@ -203,6 +207,7 @@ void reset_host(infs_ctx* c) {
   c->dispatched.assign(c->NP, std::vector<uint8_t>(c->G, 0));
   c->slot_arrivals.assign(c->S, 0);
   c->merged_arrivals.assign(c->NP, 0);
+  c->peer_progress = 0;
   c->step_open = false;
   c->probe_len.assign(c->probe_k > 0 ? c->NP : 0, std::vector<int32_t>(c->G, 0));
   c->probe_open = false;
@@ -655,6 +660,13 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       if (e != hipSuccess) return fail(nullptr, INFS_E_DEVICE, "hipMemset(%s): %s", what, hipGetErrorString(e));
       return INFS_OK;
     };
+    const hipError_t oe = infs::layers_resident(key, &c->layers_resident);
+    if (oe != hipSuccess) {
+      delete c;
+      return device_fail(nullptr, oe, "occupancy query of the step launch");
+    }
+    // a step launch needs at least one producer and one merge work-group per KV head
+    if (c->layers_resident / c->Hkv < 2) c->layers_resident = 0;
     infs_status st = INFS_OK;
     if (st == INFS_OK) st = alloc((void**)&c->prefix, c->prefix_layer_bytes * c->L, "prefix store");
     if (st == INFS_OK) st = alloc((void**)&c->pool, c->pool_layer_bytes * c->L, "page pool");
@@ -681,14 +693,6 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
       delete c;
       return device_fail(nullptr, se, "hipGetSymbolAddress(static scratch)");
     }
-    const hipError_t oe = infs::layers_resident(key, &c->layers_resident);
-    if (oe != hipSuccess) {
-      free_device(c);
-      delete c;
-      return device_fail(nullptr, oe, "occupancy query of the step launch");
-    }
-    // a step launch needs at least one producer and one merge work-group per KV head
-    if (c->layers_resident / c->Hkv < 2) c->layers_resident = 0;
     a.l2_xcds = c->l2_xcds;
     a.page_table = c->page_table;
     a.ws_o = c->ws_o;
@@ -939,6 +943,8 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     a.prefix_layer_bytes = (int64_t)c->prefix_layer_bytes;
     a.pool_layer_bytes = (int64_t)c->pool_layer_bytes;
     a.merged = merged_counters(c);
+    a.peer = peer_lines(c);
+    a.peer_base = (int32_t)c->peer_progress;
     // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix and
     // response chunks in proportion to their counts (at least one each when there are any).
     const int nj = c->layers_resident / c->Hkv;
@@ -972,6 +978,7 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     }
     infs_status st = timed_launch(c, c->key, a, c->Hkv * (a.n_pre_wg + a.n_suf_wg + a.n_merge_wg), true);
     if (st != INFS_OK) return st;
+    c->peer_progress += (uint32_t)c->L;
   }
   std::fill(c->layer_done.begin(), c->layer_done.end(), 1);
   c->layers_done = c->L;
