@@ -169,10 +169,14 @@ struct Shape {
 //    bypass the XCD's L2 (the policy of agent-scope atomic stores and loads),
 //    for producers and merges on any XCDs;
 //  * XCD-local (StepArgs::l2_xcds > 0): stores stop in the XCD's L2 and loads
-//    only miss the CU's L1.  Valid when every work-group of a KV head runs on
-//    one XCD: work-group b on XCD b % l2_xcds with Hkv a multiple of l2_xcds,
-//    which the host verified when it created the context and which every
-//    work-group checks again (a mismatch sets the status word).
+//    are served by the XCD's L2 or by the CU's L1.  The L1 is clean when a
+//    launch starts, and a merge first reads a record line only after every
+//    producer of that line has arrived, so the L1 never returns an older
+//    copy within one launch that writes each record once.  Valid when every
+//    work-group of a KV head runs on one XCD: work-group b on XCD
+//    b % l2_xcds with Hkv a multiple of l2_xcds, which the host verified
+//    when it created the context and which every work-group checks again (a
+//    mismatch sets the status word).
 // Neither needs an agent-scope fence (on this chip one writes back the whole
 // L2).  Raw buffer resources over the workspace let a lane's 16 bytes leave
 // as one write; offsets are in bytes and below ws_o_bytes / ws_ml_bytes.  The
@@ -183,13 +187,18 @@ constexpr int kRawBufferWord3 = 0x00020000;
 constexpr int kStoreThrough = 16;  // sc1
 constexpr int kLoadCoherent = 16;  // sc1
 constexpr int kStoreL2 = 0;
-constexpr int kLoadL2 = 1;         // sc0: miss the CU's L1, hit the XCD's L2
+constexpr int kLoadL2 = 1;         // sc0: coherent at work-group scope: may hit the CU's L1 (clean at a launch's start), else the XCD's L2
 constexpr int kXccIdReg = 20 | (3 << 11);  // s_getreg operand: HW_REG_XCC_ID bits 3:0
 
-template <bool L2>
+// MISS_L1: loads miss the CU's L1 also in the XCD-local exchange (sc0 loads
+// are coherent only at work-group scope and may hit a line the L1 kept from
+// an earlier read; a launch that rewrites and rereads the same records, as
+// the step launch through every layer does, needs this).  Stores are the same
+// either way.
+template <bool L2, bool MISS_L1 = false>
 struct Exchange {
   static constexpr int kStore = L2 ? kStoreL2 : kStoreThrough;
-  static constexpr int kLoad = L2 ? kLoadL2 : kLoadCoherent;
+  static constexpr int kLoad = (L2 && !MISS_L1) ? kLoadL2 : kLoadCoherent;
   __amdgpu_buffer_rsrc_t o, ml;
   __device__ explicit Exchange(const StepArgs& a)
       : o(__builtin_amdgcn_make_buffer_rsrc(a.ws_o, 0, (int)a.ws_o_bytes, kRawBufferWord3)),

@@ -4,7 +4,7 @@
 namespace infs {
 namespace {
 
-#define INFS_ENTRY(d, hpk, pr) {{1, d, hpk, 1, pr, 1}, {decode_kernel<Shape<true, d, hpk, true, pr, true>, false>, decode_kernel<Shape<true, d, hpk, true, pr, true>, true>}, layers_kernel<Shape<true, d, hpk, true, pr, true>>},
+#define INFS_ENTRY(d, hpk, pr) {{1, d, hpk, 1, pr, 1}, {decode_kernel<Shape<true, d, hpk, true, pr, true>, false>, decode_kernel<Shape<true, d, hpk, true, pr, true>, true>}, {layers_kernel<Shape<true, d, hpk, true, pr, true>, false>, layers_kernel<Shape<true, d, hpk, true, pr, true>, true>}},
 
 const KernelEntry kEntries[] = {
     INFS_ENTRY(128, 1, 16)

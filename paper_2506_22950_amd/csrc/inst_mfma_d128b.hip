@@ -4,7 +4,7 @@
 namespace infs {
 namespace {
 
-#define INFS_ENTRY(bf, d, hpk, mf, pr) {{bf, d, hpk, mf, pr, 0}, {decode_kernel<Shape<bf, d, hpk, mf, pr>, false>, decode_kernel<Shape<bf, d, hpk, mf, pr>, true>}, layers_kernel<Shape<bf, d, hpk, mf, pr>>},
+#define INFS_ENTRY(bf, d, hpk, mf, pr) {{bf, d, hpk, mf, pr, 0}, {decode_kernel<Shape<bf, d, hpk, mf, pr>, false>, decode_kernel<Shape<bf, d, hpk, mf, pr>, true>}, {layers_kernel<Shape<bf, d, hpk, mf, pr>, false>, layers_kernel<Shape<bf, d, hpk, mf, pr>, true>}},
 
 const KernelEntry kEntries[] = {
     INFS_ENTRY(true, 128, 4, true, 16)

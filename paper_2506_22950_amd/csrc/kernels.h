@@ -47,7 +47,8 @@ hipError_t layers_resident(const KernelKey& key, int* resident);
 struct KernelEntry {
   KernelKey key;
   void (*decode[2])(const StepArgs);  // [0]: partials through the coherence point, [1]: through the XCD's L2
-  void (*layers)(const StepArgs);     // step launch through every layer (partials through the coherence point)
+  void (*layers[2])(const StepArgs);  // step launch through every layer: [0] partials through the coherence
+                                      // point, [1] through the XCD's L2
 };
 struct KernelTable {
   const KernelEntry* entries;

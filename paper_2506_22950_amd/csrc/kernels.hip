@@ -59,7 +59,7 @@ hipError_t launch_decode(const KernelKey& key, const StepArgs& args, int grid, h
 hipError_t launch_layers(const KernelKey& key, const StepArgs& args, int grid, hipStream_t stream) {
   const KernelEntry* e = find_entry(key);
   if (!e) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(e->layers, dim3(grid), dim3(kBlockThreads), 0, stream, args);
+  hipLaunchKernelGGL(e->layers[args.l2_xcds > 0 ? 1 : 0], dim3(grid), dim3(kBlockThreads), 0, stream, args);
   return hipGetLastError();
 }
 
@@ -67,7 +67,7 @@ hipError_t layers_resident(const KernelKey& key, int* resident) {
   const KernelEntry* e = find_entry(key);
   if (!e) return hipErrorInvalidValue;
   int per_cu = 0, dev = 0, cus = 0;
-  hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, e->layers, kBlockThreads, 0);
+  hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, e->layers[0], kBlockThreads, 0);
   if (err == hipSuccess) err = hipGetDevice(&dev);
   if (err == hipSuccess) err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (err != hipSuccess) return err;

@@ -20,11 +20,14 @@
 // a per-KV-head flag that the producers of that head poll.
 //
 // Split-K partials go through the device coherence point (write-through
-// stores, loads that miss the caches): with several layers per launch the
-// same record addresses are rewritten and reread, and a cached copy from an
-// earlier layer must never be returned.  The workspace is safe to rewrite
-// because a producer of layer l writes only after every merge of layer l-1 of
-// its prompt has read its partials.
+// stores, loads that miss the caches) or, in the XCD-local exchange (every
+// work-group of a KV head on one XCD, as in the per-layer launch), through
+// that XCD's L2 (stores stop there).  With several layers per launch the same
+// record addresses are rewritten and reread, so a merge's loads miss the CU's
+// L1 in both modes (device-scope loads): an L1 line kept from an earlier
+// layer's read is never returned.  The workspace is safe to rewrite because a producer of
+// layer l writes only after every merge of layer l-1 of its prompt has read
+// its partials.
 //
 // Every wait is bounded by merge_polls (and gives up at once once any wait of
 // the launch has given up, or when merge_polls < 0); a wait that gives up sets
@@ -271,7 +274,7 @@ __device__ __forceinline__ PrefixItem prefix_item(const StepArgs& a, int k) {
 }
 
 // ---- Prefix chunk on the wavefront path (see prefix_wave) -------------------
-template <class SH>
+template <class SH, bool L2>
 struct PrefixWave {
   using Regs = WaveRegs<SH, SH::PR>;
   static constexpr int kLoads = 2 * Regs::U;  // load instructions of issue()
@@ -304,13 +307,13 @@ struct PrefixWave {
     wave_compute<SH, PR>(addr(a, V, it.p, g), wt0, wt1, q, a.scale_log2, R, m, l, o);
     wave_combine_groups<SH, PR>(m, l, o);
     const int64_t rec0 = (((int64_t)it.p * a.Hkv + g) * a.prefix_chunks_max + it.c) * PR;
-    block_store_partial<SH, PR, false>(smem, m, l, o, Exchange<false>(a), rec0);
+    block_store_partial<SH, PR, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
     after_stores();
   }
 };
 
 // ---- Prefix chunk on MFMA tiles (see prefix_mfma) ---------------------------
-template <class SH>
+template <class SH, bool L2>
 struct PrefixMfma {
   static constexpr int D = SH::D, KB = SH::KB, DB = SH::DB;
   static constexpr bool PREFETCH_V = SH::NBW == 1;
@@ -446,7 +449,7 @@ struct PrefixMfma {
       lrow[nb] += __shfl_xor(lrow[nb], 32);
     }
     const int64_t rec0 = (((int64_t)it.p * a.Hkv + g) * a.prefix_chunks_max + it.c) * SH::PR;
-    const Exchange<false> ex(a);
+    const Exchange<L2> ex(a);
     if constexpr (TG == 1) {
 #pragma unroll
       for (int nb = 0; nb < NBW; ++nb) {
@@ -537,7 +540,7 @@ __device__ __forceinline__ int resp_pages(const StepArgs& a, const RespItem& r) 
   return lane < npg ? ptab[lane] : 0;
 }
 
-template <class SH>
+template <class SH, bool L2>
 struct Resp {
   static constexpr int HPK = SH::HPK;
   using Regs = WaveRegs<SH, HPK>;
@@ -583,7 +586,7 @@ struct Resp {
       __hip_atomic_fetch_add(&a.tokens[(r.s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)r.s * a.Hkv + g) * a.suffix_chunks_max + r.c) * HPK;
-    block_store_partial<SH, HPK, false>(smem, m, l, o, Exchange<false>(a), rec0);
+    block_store_partial<SH, HPK, L2>(smem, m, l, o, Exchange<L2>(a), rec0);
     after_stores();
   }
 };
@@ -591,7 +594,7 @@ struct Resp {
 // The same response item on MFMA tiles (bf16 and E4M3 pages; see RespMfma):
 // issue() loads the wavefront's first round, finish() runs the rest once the
 // item's queries may be read.
-template <class SH>
+template <class SH, bool L2>
 struct RespTiles {
   using RM = RespMfma<SH>;
   using Regs = typename RM::Regs;
@@ -634,7 +637,7 @@ struct RespTiles {
     }
     RM::publish(smem, A);
     const int64_t rec0 = prefix_records(a, SH::PR) + (((int64_t)r.s * a.Hkv + g) * a.suffix_chunks_max + r.c) * HPK;
-    combine_store_partial<SH, HPK, false>(smem, Exchange<false>(a), rec0);
+    combine_store_partial<SH, HPK, L2>(smem, Exchange<L2>(a), rec0);
     after_stores();
   }
 };
@@ -650,7 +653,7 @@ struct MergeWaveShape {
   static constexpr int MCW = MV == 1 ? 24 : MV == 2 ? 8 : 4;
 };
 
-template <class SH>
+template <class SH, bool L2>
 __device__ void merge_wave(const StepArgs& a, const LayerView& V, int s, int g, int32_t target) {
   using MW = MergeWaveShape<SH>;
   constexpr int D = SH::D, HPK = SH::HPK, MV = MW::MV, MCW = MW::MCW;
@@ -676,7 +679,7 @@ __device__ void merge_wave(const StepArgs& a, const LayerView& V, int s, int g, 
   const int64_t pbase = ((int64_t)p * a.Hkv + g) * a.prefix_chunks_max * SH::PR + si * HPK;
   const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.Hkv + g) * a.suffix_chunks_max * HPK;
   auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + (int64_t)c * SH::PR : sbase + (int64_t)(c - nP) * HPK) + j; };
-  const Exchange<false> ex(a);
+  const Exchange<L2, true> ex(a);
   float M[MV], L[MV];
   f32x4 O[MV];
 #pragma unroll
@@ -779,11 +782,11 @@ __device__ __forceinline__ void layer_gate(const StepArgs& a, int p, int l, uint
 // of every layer.  The layer's first item is loaded once the layer may start;
 // a later item of the same layer is loaded right behind the previous item's
 // stores.
-template <class SH>
+template <class SH, bool L2>
 __device__ __forceinline__ void prefix_loop(const StepArgs& a, int g, int jp, float* smem) {
   if (jp >= a.n_prefix_items) return;
   const int nk = (a.n_prefix_items - jp + a.n_pre_wg - 1) / a.n_pre_wg;
-  using P = std::conditional_t<SH::MFMA, PrefixMfma<SH>, PrefixWave<SH>>;
+  using P = std::conditional_t<SH::MFMA, PrefixMfma<SH, L2>, PrefixWave<SH, L2>>;
   typename P::Regs R;
   for (int l = 0; l < a.num_layers; ++l) {
     const LayerView V = layer_view(a, l);
@@ -810,11 +813,11 @@ __device__ __forceinline__ void prefix_loop(const StepArgs& a, int g, int jp, fl
 // ... of every layer, each with the next item's loads issued behind its stores
 // (behind the CU mate's part of the layer when the next item is in the next
 // layer).
-template <class SH>
+template <class SH, bool L2>
 __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, float* smem) {
   if (jr >= a.n_suffix_items) return;
   const int nk = (a.n_suffix_items - jr + a.n_suf_wg - 1) / a.n_suf_wg;
-  using P = std::conditional_t<SH::BF, RespTiles<SH>, Resp<SH>>;
+  using P = std::conditional_t<SH::BF, RespTiles<SH, L2>, Resp<SH, L2>>;
   typename P::Regs R;
   RespItem it = resp_item(a, jr);
   int pages = resp_pages(a, it);
@@ -849,7 +852,7 @@ __device__ __forceinline__ void suffix_loop(const StepArgs& a, int g, int jr, fl
   }
 }
 
-template <class SH>
+template <class SH, bool L2>
 __device__ void merge_loop(const StepArgs& a, int g, int mj) {
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -862,7 +865,7 @@ __device__ void merge_loop(const StepArgs& a, int g, int mj) {
         const int p = s / a.m;
         const uint32_t per = (uint32_t)((a.slot[s].len + a.split - 1) / a.split + a.prompt[p].nchunks);
         const int32_t target = (int32_t)((uint32_t)a.slot[s].target + (uint32_t)(l + 1) * per);
-        merge_wave<SH>(a, V, s, g, target);
+        merge_wave<SH, L2>(a, V, s, g, target);
         // Counted once this wavefront's partial loads and O stores have completed;
         // the merge that completes the prompt's layer raises every head's flag.
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -888,7 +891,7 @@ __device__ void merge_loop(const StepArgs& a, int g, int mj) {
 
 // The step launch.  Timing mode as in decode_kernel (one start / end pair for
 // the whole launch).
-template <class SH>
+template <class SH, bool L2>
 __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void layers_kernel(const StepArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[SH::SMEM > 4 ? SH::SMEM : 4];
   const int cs = (blockIdx.x % kClockSlots) * kClockStride;
@@ -896,13 +899,16 @@ __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void layers_kernel(co
     __hip_atomic_fetch_min(a.clock_start + cs, (unsigned long long)__builtin_amdgcn_s_memrealtime(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
   if (threadIdx.x == 0) __hip_atomic_store(peer_line(a, blockIdx.x) + 4, cu_id() + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (L2 && threadIdx.x == 0 &&
+      (__builtin_amdgcn_s_getreg(kXccIdReg) & 15) != (int)((blockIdx.x + a.l2_check_shift) % a.l2_xcds))
+    __hip_atomic_store(a.status, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int g = blockIdx.x % a.Hkv, j = blockIdx.x / a.Hkv;
   if (j < a.n_pre_wg)
-    prefix_loop<SH>(a, g, j, smem);
+    prefix_loop<SH, L2>(a, g, j, smem);
   else if (j < a.n_pre_wg + a.n_suf_wg)
-    suffix_loop<SH>(a, g, j - a.n_pre_wg, smem);
+    suffix_loop<SH, L2>(a, g, j - a.n_pre_wg, smem);
   else if (j < a.n_pre_wg + a.n_suf_wg + a.n_merge_wg)
-    merge_loop<SH>(a, g, j - a.n_pre_wg - a.n_suf_wg);
+    merge_loop<SH, L2>(a, g, j - a.n_pre_wg - a.n_suf_wg);
   if (a.clock_start) {
     __syncthreads();
     if (threadIdx.x == 0)

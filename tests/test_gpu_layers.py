@@ -142,3 +142,64 @@ def test_step_launch_wait_give_up_is_reported():
     assert torch.isnan(o[:, 0]).all() and torch.isnan(o[:, 3]).all()
     assert not o[:, 1].any() and not o[:, 2].any()
     ctx.destroy()
+
+
+@pytest.mark.parametrize("kv_fp8", [False, True], ids=["bf16", "fp8"])
+def test_step_launch_exchange_modes_agree_bitwise(kv_fp8):
+    # The step launch exchanges split-K partials through the XCD's L2 when every
+    # work-group of a KV head runs on one XCD (the default for 8 KV heads on
+    # this device), else through the coherence point; both move the same
+    # values, so every output agrees bit for bit, and matches the oracle.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, **_BF16_SMALL)
+    wl = Workload(cfg)
+    modes = {}
+
+    def seen(ctx, step, log):
+        modes.setdefault("default", ctx.exchange_mode())
+
+    runs = []
+    for exchange in (None, 0):
+        _, log, _, cap, _, _ = run_gpu_group(cfg, "sjf", wl=wl, split=128, inspect=seen, exchange=exchange,
+                                             kv_fp8=kv_fp8, entry="decode_step_layers")
+        runs.append((log, cap))
+    assert modes["default"] == 1, "8 KV heads on this device should exchange partials through the XCD's L2"
+    (log1, cap1), (log0, cap0) = runs
+    assert log1 == log0 and cap1.keys() == cap0.keys()
+    for k in cap0:
+        assert np.array_equal(cap1[k], cap0[k]), k
+    worst, n = check_against_oracle(cfg, wl, log0, {k: cap0[k] for k in list(cap0)[::5]}, kv_fp8=kv_fp8)
+    say(f"  [step launch exchange modes {'fp8' if kv_fp8 else 'bf16'}] {len(cap0)} steps bitwise equal; "
+        f"{n} outputs vs oracle max err {worst:.3g}")
+
+
+def test_step_launch_exchange_placement_check():
+    # In the XCD-local exchange every work-group of the step launch checks that
+    # it runs on the XCD the plan assumes; mode 2 makes that check fail on every
+    # work-group: the launch runs to its end and the next synchronising call
+    # reports E_DEVICE.
+    import torch
+
+    from paper_2506_22950_amd.group import context_for
+    from workload.staging import DeviceInputs
+
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, **_BF16_SMALL)
+    wl = Workload(cfg)
+    dev = DeviceInputs(wl)
+    ctx = context_for(cfg, stream=torch.cuda.current_stream())
+    keep = []
+    for layer in range(cfg.layers):
+        k, v = dev.prefix(layer, 0)
+        keep.append((k, v))
+        ctx.prefill_shared(0, layer, cfg.prompt_lens[0], k, v)
+    ctx.refill_slot(0, 0, 0)
+    L, S, Hq, Hkv, d = cfg.layers, cfg.num_slots, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
+    q = torch.zeros((L, S, Hq, d), dtype=torch.int16, device="cuda")
+    kn = torch.zeros((L, S, Hkv, d), dtype=torch.int16, device="cuda")
+    o = torch.zeros((L, S, Hq, d), dtype=torch.float32, device="cuda")
+    ctx.set_exchange(2)
+    ctx.decode_step_layers(q, kn, kn, o)
+    ctx.end_step()
+    with pytest.raises(infs.InfsError) as ei:
+        ctx.sync()
+    assert ei.value.status == infs.E_DEVICE
+    ctx.destroy()
