@@ -25,8 +25,8 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 COPY_CAL_BYTES = 1 << 30
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_traffic_{workload}.txt")
-MFMA_FILE = os.path.join(ROOT, "profiles", "decode_kernel_mfma_{workload}.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "{kernel}_traffic_{workload}.txt")
+MFMA_FILE = os.path.join(ROOT, "profiles", "{kernel}_mfma_{workload}.txt")
 CALIB_LIB = os.path.join(ROOT, "paper_2506_22950_amd", "libinfs_calib.so")
 PEAK_MFMA_BF16_TFLOPS = 2500.0
 SIMDS = 1024  # 256 compute units x 4 SIMDs
@@ -80,37 +80,74 @@ def _read_summary(path):
     return kv
 
 
-def read_traffic(workload):
-    """HBM bytes per decode launch from the committed counter summary of this
+KERNELS = {"decode_step_layers": "layers_kernel", "decode_step": "decode_kernel"}
+
+
+def entry_launches(cfg, steplog, entry):
+    """Kernel launches of one group decode: one per running step for the step
+    launch through every layer, one per layer and step otherwise."""
+    return len(steplog) * (1 if entry == "decode_step_layers" else cfg.layers)
+
+
+def read_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary of this
     workload, or None when there is none or the kernel source has changed since."""
-    kv = _read_summary(TRAFFIC_FILE.format(workload=workload))
+    kv = _read_summary(TRAFFIC_FILE.format(kernel=kernel, workload=workload))
     return None if kv is None else float(kv["traffic_bytes_per_launch"])
 
 
-def read_mfma(workload):
-    """MFMA counter summary of this workload's decode launches (or None)."""
-    return _read_summary(MFMA_FILE.format(workload=workload))
+def read_mfma(workload, kernel):
+    """MFMA counter summary of this workload's launches of `kernel` (or None)."""
+    return _read_summary(MFMA_FILE.format(kernel=kernel, workload=workload))
 
 
-def mfma_flops(cfg, steplog):
-    """MFMA flops of all decode launches of a step log: per prompt with a live
-    slot, the prefix contractions S^T = K Q^T and O^T = V^T P^T over the padded
-    row tile (m * hpk rows padded to 16/32/64) and 32-token blocks, 2 flops per
-    multiply-add, every KV head, every layer."""
+def mfma_flops(cfg, steplog, split=256):
+    """MFMA flops issued by all launches of a group decode (2 flops per
+    multiply-add of every 16x16x32 tile issued), every KV head, every layer:
+    (prefix) per prompt with a live slot, S^T = K Q^T and O^T = V^T P^T over
+    the padded row tile (m * hpk rows padded to 16/32/64/128) and 32-token
+    blocks; (responses, bf16 and E4M3 pages) per live slot, per wavefront of
+    each split-K chunk, per 32-token page pair of its stored tokens (the newest
+    token is folded in apart): two S^T tiles of head_dim / 32 steps, then
+    head_dim / 16 O^T tiles and one row-sum tile, each 16 columns wide with hpk
+    of them carrying query rows.  fp32 contexts issue no MFMA."""
+    if cfg.dtype != "bf16":
+        return 0.0
     rows = cfg.slots_per_prompt * cfg.hpk
     pad = 16 if rows <= 16 else 32 if rows <= 32 else 64 if rows <= 64 else 128
-    per_prompt = [4 * pad * (-(-plen // 32) * 32) * cfg.head_dim * cfg.num_kv_heads for plen in cfg.prompt_lens]
+    d = cfg.head_dim
+    per_prompt = [4 * pad * (-(-plen // 32) * 32) * d * cfg.num_kv_heads for plen in cfg.prompt_lens]
+    tile = 2 * 16 * 16 * 32
+    per_pair = (2 * (d // 32) + d // 16 + 1) * tile
+    sub = split // 4
+    pairs_memo = {}
+
+    def pairs(length):  # page pairs the wavefronts of one slot multiply
+        if length not in pairs_memo:
+            n, last = 0, length - 1
+            for t0 in range(0, length, split):
+                t1 = min(t0 + split, length)
+                for w in range(4):
+                    w0 = min(t0 + w * sub, t1)
+                    w1 = min(w0 + sub, t1)
+                    te = last if w0 <= last < w1 else w1
+                    n += -(-(te - w0) // 32) if te > w0 else 0
+            pairs_memo[length] = n
+        return pairs_memo[length]
+
     total = 0
     for row in steplog:
         total += sum(per_prompt[p] for p in {e[0] for e in row if e is not None})
+        total += sum(pairs(e[2]) for e in row if e is not None) * per_pair * cfg.num_kv_heads
     return total * cfg.layers
 
 
-def read_ceiling(torch, stream, nbytes, launches=200, pool_bytes=2 << 30):
+def read_ceiling(torch, stream, nbytes, launches=200, pool_bytes=2 << 30, read_budget=40 << 30):
     """The one-launch read-bandwidth reference: a plain streaming-read kernel
     (libinfs_calib.so) over `nbytes` (rounded down to a multiple of 16 KiB),
-    launched back to back over distinct buffers of a 2 GiB pool (so no launch
-    finds its bytes in the 256 MB last-level cache), timed like the decode
+    launched back to back over distinct buffers of a pool of at least 2 GiB and
+    two launches (so no launch finds its bytes in the 256 MB last-level cache),
+    timed like the decode
     launches: HIP events on `stream` around all launches, divided by their
     number.  Best of 256, 512 and 1024 work-groups.
     Returns (bytes, us per launch, work-groups)."""
@@ -122,7 +159,8 @@ def read_ceiling(torch, stream, nbytes, launches=200, pool_bytes=2 << 30):
     fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     fn.restype = ctypes.c_int
     nb = nbytes // (16 << 10) * (16 << 10)
-    nbuf = pool_bytes // nb
+    nbuf = max(2, pool_bytes // nb)  # a step launch through every layer can read more than the pool
+    launches = max(5, min(launches, read_budget // nb))  # at most ~40 GiB read per grid size
     pool = torch.empty(nbuf * nb, dtype=torch.uint8, device="cuda")
     sink = torch.zeros(1024, dtype=torch.int32, device="cuda")
     with torch.cuda.stream(stream):
@@ -177,18 +215,19 @@ def _pmc_rows(path, counter):
     return rows
 
 
-def summarize_pmc(workload, fetch_dir, write_dir):
+def summarize_pmc(workload, fetch_dir, write_dir, entry="decode_step_layers"):
     """Text summary of two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of
     `bench.py --steps 1 --warmup 0 --no-kernel-timing --no-cpu-baseline --copy-calibration`:
-    per-launch HBM traffic of decode_kernel, each counter scaled by its reading for
-    the calibration copy of known size."""
+    per-launch HBM traffic of the entry's kernel, each counter scaled by its
+    reading for the calibration copy of known size."""
     from paper_2506_22950_amd.group import plan_steps
     from workload import Workload, get_config
 
+    kernel = KERNELS[entry]
     out = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _pmc_rows(d, counter)
-        dec = [float(r["Counter_Value"]) for r in rows if "decode_kernel" in r["Kernel_Name"]]
+        dec = [float(r["Counter_Value"]) for r in rows if kernel in r["Kernel_Name"]]
         cps = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
         gmax = max(int(r["Grid_Size"]) for r in cps)
         cal = [float(r["Counter_Value"]) for r in cps if int(r["Grid_Size"]) == gmax]
@@ -200,24 +239,25 @@ def summarize_pmc(workload, fetch_dir, write_dir):
     cfg = get_config(workload)
     wl = Workload(cfg)
     steplog = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
-    launches = len(steplog) * cfg.layers
+    launches = entry_launches(cfg, steplog, entry)
     alg = algorithmic_bytes(cfg, steplog) / launches
     nf, fk, cf, sf = out["FETCH_SIZE"]
     nw, wk, cw, sw = out["WRITE_SIZE"]
     if nf != launches or nw != launches:
-        raise SystemExit(f"expected {launches} decode launches, got {nf} / {nw}")
+        raise SystemExit(f"expected {launches} {kernel} launches, got {nf} / {nw}")
     fetch_b, write_b = fk * 1024.0 * sf, wk * 1024.0 * sw
     lines = [
         f"kernel_source_sha256 = {kernel_source_hash()}",
         f"workload = {workload}",
-        f"decode_launches = {launches}",
+        f"kernel = {kernel}",
+        f"launches = {launches}",
         f"copy_bytes = {COPY_CAL_BYTES}",
         f"copy_fetch_kib = {cf:.1f}",
         f"copy_write_kib = {cw:.1f}",
         f"fetch_scale = {sf:.4f}",
         f"write_scale = {sw:.4f}",
-        f"decode_fetch_kib_per_launch = {fk:.1f}",
-        f"decode_write_kib_per_launch = {wk:.1f}",
+        f"fetch_kib_per_launch = {fk:.1f}",
+        f"write_kib_per_launch = {wk:.1f}",
         f"fetch_bytes_per_launch = {fetch_b:.0f}",
         f"write_bytes_per_launch = {write_b:.0f}",
         f"traffic_bytes_per_launch = {fetch_b + write_b:.0f}",
@@ -227,24 +267,25 @@ def summarize_pmc(workload, fetch_dir, write_dir):
     return "\n".join(lines)
 
 
-def summarize_mfma(workload, pmc_dir):
+def summarize_mfma(workload, pmc_dir, entry="decode_step_layers"):
     """Text summary of one rocprofv3 --pmc run of MFMA_COUNTERS over
     `bench.py --steps 1 --warmup 1 --no-kernel-timing --no-cpu-baseline`:
-    MFMA work and MFMA busy cycles of decode_kernel per launch.  Counter values
-    are summed over their hardware instances (shader engines, XCDs)."""
+    MFMA work and MFMA busy cycles of the entry's kernel per launch.  Counter
+    values are summed over their hardware instances (shader engines, XCDs)."""
     from paper_2506_22950_amd.group import plan_steps
     from workload import Workload, get_config
 
+    kernel = KERNELS[entry]
     per = {}
     for counter in MFMA_COUNTERS:
-        vals = [float(r["Counter_Value"]) for r in _pmc_rows(pmc_dir, counter) if "decode_kernel" in r["Kernel_Name"]]
+        vals = [float(r["Counter_Value"]) for r in _pmc_rows(pmc_dir, counter) if kernel in r["Kernel_Name"]]
         if not vals:
-            raise SystemExit(f"{counter}: no decode_kernel rows under {pmc_dir}")
+            raise SystemExit(f"{counter}: no {kernel} rows under {pmc_dir}")
         per[counter] = (len(vals), sum(vals) / len(vals))
     cfg = get_config(workload)
     wl = Workload(cfg)
     steplog = plan_steps(cfg, wl.L, cfg.policy, wl.L_hat)
-    launches = len(steplog) * cfg.layers
+    launches = entry_launches(cfg, steplog, entry)
     counts = {n for n, _ in per.values()}
     if len(counts) != 1 or next(iter(counts)) % launches:
         raise SystemExit(f"expected whole group decodes of {launches} launches per counter, got {sorted(counts)}")
@@ -257,7 +298,8 @@ def summarize_mfma(workload, pmc_dir):
     lines = [
         f"kernel_source_sha256 = {kernel_source_hash()}",
         f"workload = {workload}",
-        f"decode_launches = {launches} per group decode, {decodes} group decodes profiled",
+        f"kernel = {kernel}",
+        f"launches = {launches} per group decode, {decodes} group decodes profiled",
         f"mfma_mops_bf16_per_launch = {mops:.1f}",
         f"mfma_flops_per_launch = {mops * 512:.0f}",
         f"expected_mfma_flops_per_launch = {expect:.0f}",
@@ -268,6 +310,49 @@ def summarize_mfma(workload, pmc_dir):
         f"mfma_busy_over_busy_cu_simd_cycles = {busy / (cu_busy_quads * 4 * 4):.5f}",
     ]
     return "\n".join(lines)
+
+
+def summarize_stats(workload, stats_dir, bench_out, entry="decode_step_layers", command=""):
+    """Kernel statistics table of a `rocprofv3 --kernel-trace --stats` run of
+    `bench.py --steps K --warmup W` (without --no-kernel-timing): the run decodes
+    the group W + K + 2 times (warmup, timed, then the HIP-event and the
+    device-clock timing passes); the header says so and quotes the command and
+    the JSON line that run printed."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(stats_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one kernel_stats.csv under {stats_dir}, found {len(files)}")
+    with open(files[0]) as fh:
+        rows = list(csv.DictReader(fh))
+    with open(bench_out) as fh:
+        line = [ln.strip() for ln in fh if ln.strip().startswith("{")][-1]
+    b = json.loads(line)
+    passes = b["warmup"] + b["steps"] + 2
+    kernel = KERNELS[entry]
+    main = [r for r in rows if kernel in r["Name"]]
+    if not main:
+        raise SystemExit(f"no {kernel} row in {files[0]}")
+    out = [f"# rocprofv3 kernel statistics, workload {workload}: {passes} whole group decodes",
+           f"# ({b['warmup']} warmup, {b['steps']} timed, then the HIP-event and the device-clock timing passes)",
+           "# of the command below, run on one MI355X from the repository root after: cd /tmp && export TMPDIR=/tmp",
+           f"#   {command}" if command else "#   (command not given)",
+           f"#   python3 bench.py --workload {workload} --entry {'step' if entry == 'decode_step_layers' else 'layer'}"
+           f" --summarize-stats <stats dir> <bench output>",
+           "# bench.py line printed by that same run (its launch times include the profiler's per-dispatch overhead):",
+           "#   " + line, "",
+           f"{'kernel':<62}{'calls':>8}{'avg_us':>10}{'min_us':>10}{'max_us':>10}{'total_ms':>11}{'pct':>7}"]
+    for r in rows:
+        n = r["Name"]
+        short = n if len(n) <= 60 else n[:57] + "..."
+        out.append(f"{short:<62}{int(r['Calls']):>8}{float(r['AverageNs']) / 1e3:>10.3f}{float(r['MinNs']) / 1e3:>10.3f}"
+                   f"{float(r['MaxNs']) / 1e3:>10.3f}{float(r['TotalDurationNs']) / 1e6:>11.2f}{float(r['Percentage']):>7.2f}")
+    out += ["", f"{kernel} full name: " + main[0]["Name"],
+            f"{kernel} launches per group decode: {b['roofline']['launches'] if b.get('roofline') else 'n/a'}; "
+            f"average by the profiler {float(main[0]['AverageNs']) / 1e3:.3f} us, by HIP events in that run "
+            f"{b['roofline']['avg_launch_us'] if b.get('roofline') else 'n/a'} us"]
+    return "\n".join(out)
 
 
 def schedule_table(n_groups=64, G=32, m=4, cap=1024):
@@ -597,16 +682,25 @@ def main():
                     help="run three 1 GiB device copies first (counter calibration for --summarize-pmc)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="print the traffic summary of two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_DIR", "BENCH_OUT"),
+                    help="print the kernel statistics of a rocprofv3 --kernel-trace --stats run of bench.py "
+                         "(BENCH_OUT: the JSON line that run printed)")
+    ap.add_argument("--profile-command", default="",
+                    help="the profiled command line, quoted in the --summarize-stats header")
     ap.add_argument("--summarize-mfma", metavar="PMC_DIR",
                     help="print the MFMA summary of a rocprofv3 --pmc output folder and exit")
     ap.add_argument("--schedules", action="store_true",
                     help="print the running steps of the refill policies (host only, no GPU) and exit")
     args = ap.parse_args()
+    if args.summarize_stats:
+        print(summarize_stats(args.workload, *args.summarize_stats, entry=ENTRIES[args.entry],
+                              command=args.profile_command))
+        return
     if args.summarize_pmc:
-        print(summarize_pmc(args.workload, *args.summarize_pmc))
+        print(summarize_pmc(args.workload, *args.summarize_pmc, entry=ENTRIES[args.entry]))
         return
     if args.summarize_mfma:
-        print(summarize_mfma(args.workload, args.summarize_mfma))
+        print(summarize_mfma(args.workload, args.summarize_mfma, entry=ENTRIES[args.entry]))
         return
     if args.schedules:
         print(schedule_table())
@@ -655,10 +749,12 @@ def main():
         body_us = ms * 1000.0 / n
         per_launch = alg / n
         achieved = per_launch / (avg_us * 1e-6) / 1e9
-        traffic = read_traffic(args.workload) if not (args.reuse or args.kv_fp8 or args.exchange is not None) else None
+        kernel = KERNELS[b.entry]
+        traffic = (read_traffic(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.exchange is not None
+                                                               or args.split) else None)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
-                "kernel": "layers_kernel" if b.entry == "decode_step_layers" else "decode_kernel",
+                "kernel": kernel,
                 "launches": n, "avg_launch_us": round(avg_us, 3),
                 "alg_bytes_per_launch": round(per_launch),
                 "timing": "HIP events on the kernels' stream around all decode launches of one group decode, "
@@ -668,14 +764,14 @@ def main():
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}
-        mf = read_mfma(args.workload) if not (args.reuse or args.kv_fp8 or args.split) else None
+        mf = read_mfma(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.split) else None
         if mf is not None:
             fl = float(mf["mfma_flops_per_launch"])
-            roof["mfma"] = {"kernel": "decode_kernel (prefix contractions)", "flops_per_launch": round(fl),
+            roof["mfma"] = {"kernel": f"{kernel} (prefix and response contractions)", "flops_per_launch": round(fl),
                             "tflops": round(fl / (avg_us * 1e-6) / 1e12, 2), "peak_tflops": PEAK_MFMA_BF16_TFLOPS,
                             "frac": round(fl / (avg_us * 1e-6) / 1e12 / PEAK_MFMA_BF16_TFLOPS, 5),
                             "busy_over_active": float(mf["mfma_busy_over_active_simd_cycles"]),
-                            "source": os.path.relpath(MFMA_FILE.format(workload=args.workload), ROOT)}
+                            "source": os.path.relpath(MFMA_FILE.format(kernel=kernel, workload=args.workload), ROOT)}
         cb, cus, cblocks = read_ceiling(torch, b.stream, int(per_launch))
         cgbs = cb / (cus * 1e-6) / 1e9
         roof["read_ceiling"] = {"kernel": "plain streaming read, one launch (libinfs_calib.so)", "bytes": cb,

@@ -34,29 +34,49 @@ def test_algorithmic_bytes_closed_form():
 
 
 def test_mfma_flops_closed_form():
-    cfg = _cfg()  # m * hpk = 4 rows -> one 16-row tile; prompts padded to 64 and 64 tokens
+    # bf16, 2 layers, 16 query / 8 KV heads, d=128, prompts of 40 and 64 tokens, m=2:
+    # m * hpk = 4 rows -> one 16-row tile; both prompts padded to 64 tokens.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(40, 64), samples_per_prompt=4,
+                                             slots_per_prompt=2)
     log = [[(0, 0, 1), None, None, (1, 2, 3)], [None, None, (1, 0, 2), None], [None] * 4]
-    per = [4 * 16 * 64 * 64 * 2, 4 * 16 * 64 * 64 * 2]
-    assert bench.mfma_flops(cfg, log) == 2 * (per[0] + per[1] + per[1])
+    per = [4 * 16 * 64 * 128 * 8, 4 * 16 * 64 * 128 * 8]
+    tile = 2 * 16 * 16 * 32
+    pair = (2 * 4 + 8 + 1) * tile * 8  # two S^T tiles of 4 k-steps, 8 O^T tiles, the row-sum tile; 8 KV heads
+    # responses: t=1 stores nothing (its only token is the newest, folded in apart); t=3 and t=2: one pair
+    assert bench.mfma_flops(cfg, log) == 2 * (per[0] + per[1] + pair + per[1] + pair)
     big = get_config("qwen3_1p7b_g64")
     one = [[(0, 0, 1)] + [None] * 15]
     assert bench.mfma_flops(big, one) == 28 * 4 * 32 * 2048 * 128 * 8
+    # t=300, chunks of 256: four wavefronts of 64 stored tokens (2 pairs each), then 43 stored tokens
+    # (299 minus 256, the newest apart) on the next chunk's first wavefront (2 pairs): 10 pairs
+    long = [[(0, 0, 300)] + [None] * 15]
+    assert bench.mfma_flops(big, long) - bench.mfma_flops(big, one) == 28 * 10 * pair
+    assert bench.mfma_flops(get_config("tiny_f32"), log) == 0  # fp32 contexts issue no MFMA
+
+
+def test_launches_per_entry():
+    cfg = get_config("qwen3_1p7b_g64")
+    log = [[None] * 16] * 5
+    assert bench.entry_launches(cfg, log, "decode_step_layers") == 5
+    assert bench.entry_launches(cfg, log, "decode_step") == 5 * cfg.layers
 
 
 def test_summaries_follow_kernel_source(tmp_path, monkeypatch):
-    pattern = tmp_path / "t_{workload}.txt"
-    (tmp_path / "t_w.txt").write_text(f"# header = ignored\nkernel_source_sha256 = {bench.kernel_source_hash()}\n"
-                                      "traffic_bytes_per_launch = 123\n")
+    pattern = tmp_path / "t_{kernel}_{workload}.txt"
+    (tmp_path / "t_k_w.txt").write_text(f"# header = ignored\nkernel_source_sha256 = {bench.kernel_source_hash()}\n"
+                                        "traffic_bytes_per_launch = 123\n")
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(pattern))
-    assert bench.read_traffic("w") == 123.0
-    (tmp_path / "t_w.txt").write_text("kernel_source_sha256 = 00\ntraffic_bytes_per_launch = 123\n")
-    assert bench.read_traffic("w") is None
-    assert bench.read_traffic("absent") is None
+    assert bench.read_traffic("w", "k") == 123.0
+    assert bench.read_traffic("w", "other") is None
+    (tmp_path / "t_k_w.txt").write_text("kernel_source_sha256 = 00\ntraffic_bytes_per_launch = 123\n")
+    assert bench.read_traffic("w", "k") is None
+    assert bench.read_traffic("absent", "k") is None
 
 
 @pytest.mark.parametrize("name", ["traffic", "mfma"])
 def test_committed_summaries_parse(name):
-    path = (bench.TRAFFIC_FILE if name == "traffic" else bench.MFMA_FILE).format(workload="qwen3_1p7b_g64")
+    path = (bench.TRAFFIC_FILE if name == "traffic" else bench.MFMA_FILE).format(kernel="layers_kernel",
+                                                                               workload="qwen3_1p7b_g64")
     assert os.path.exists(path)
     kv = {}
     for ln in open(path):
@@ -64,6 +84,7 @@ def test_committed_summaries_parse(name):
             k, v = ln.split("=", 1)
             kv[k.strip()] = v.strip()
     assert len(kv["kernel_source_sha256"]) == 64
+    assert kv["kernel"] == "layers_kernel"
     if name == "mfma":
         assert kv["mfma_flops_per_launch"] == kv["expected_mfma_flops_per_launch"]
 
