@@ -603,8 +603,9 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
   c->pages_per_slot = ceil_div(k.max_suffix_len, infs::kPageTokens);
   c->H = c->probe_k > 0 ? c->NP * c->G : c->S;
   if ((int64_t)c->H * c->pages_per_slot * (int64_t)sizeof(int32_t) >= (int64_t(1) << 31)) {
+    const int seqs = c->H, pps = c->pages_per_slot;
     delete c;
-    return fail(nullptr, INFS_E_ARG, "page table of %d sequences x %d pages exceeds 2 GiB", c->H, c->pages_per_slot);
+    return fail(nullptr, INFS_E_ARG, "page table of %d sequences x %d pages exceeds 2 GiB", seqs, pps);
   }
   {
     const int64_t pages = k.num_pages ? (int64_t)k.num_pages

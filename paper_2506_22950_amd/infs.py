@@ -14,7 +14,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libinfs.so")
+# The library to load: libinfs.so next to this file, or the build named by
+# INFS_LIBRARY (for instance the host-sanitizer build, see build.py).
+LIB_PATH = os.environ.get("INFS_LIBRARY") or os.path.join(HERE, "libinfs.so")
 
 OK, E_ARG, E_STATE, E_CAPACITY, E_DUP, E_NOMEM, E_DEVICE = 0, -1, -2, -3, -4, -5, -6
 STATUS_NAMES = {0: "OK", -1: "E_ARG", -2: "E_STATE", -3: "E_CAPACITY", -4: "E_DUP", -5: "E_NOMEM", -6: "E_DEVICE"}
