@@ -40,10 +40,12 @@
 // still has this layer's partial stores or merges to do puts those behind
 // the whole stream.  So a response work-group issues its next layer's loads
 // only once its CU mate is past its part of the layer (or after a short
-// bound), and a prefix work-group -- whose chunk is small and whose partial
-// is needed early -- loads its next layer's chunk only when that layer may
-// start.  Which work-groups share a CU is read from the hardware (see
-// mate_gate); none of this affects results.
+// bound), a prefix work-group -- whose chunk is small and whose partial is
+// needed early -- loads its next layer's chunk only when that layer may
+// start, and the host places the merge work-groups on the CUs of prefix
+// work-groups, whose queues are then empty while the merges run.  Which
+// work-groups share a CU is read from the hardware (see mate_gate); none of
+// this affects results.
 #pragma once
 #include <type_traits>
 
@@ -727,6 +729,21 @@ __device__ void merge_wave(const StepArgs& a, const LayerView& V, int s, int g, 
   }
 }
 
+// Role of work-group index j of a KV head (see StepArgs::merge_j0): 0 prefix,
+// 1 response, 2 merge, with its index among the work-groups of that role.
+__device__ __forceinline__ int wg_role(const StepArgs& a, int j, int& idx) {
+  if (j < a.n_pre_wg) {
+    idx = j;
+    return 0;
+  }
+  if (j >= a.merge_j0 && j < a.merge_j0 + a.n_merge_wg) {
+    idx = j - a.merge_j0;
+    return 2;
+  }
+  idx = j - a.n_pre_wg - (j >= a.merge_j0 + a.n_merge_wg ? a.n_merge_wg : 0);
+  return 1;
+}
+
 // Hardware id of the CU running this work-group (XCD, shader engine, array, CU).
 __device__ __forceinline__ int32_t cu_id() {
   const int32_t hw = __builtin_amdgcn_s_getreg(4 | (31 << 11));  // HW_REG_HW_ID: CU id in bits 8..15
@@ -750,13 +767,11 @@ __device__ void mate_gate(const StepArgs& a, int l) {
     const int g = blockIdx.x % a.Hkv, j = blockIdx.x / a.Hkv;
     const int jm = j < nj / 2 ? j + nj / 2 : j - nj / 2;
     const int w = threadIdx.x;
-    bool need;
-    if (jm < a.n_pre_wg)
-      need = w == 0 && jm < a.n_prefix_items;
-    else if (jm < a.n_pre_wg + a.n_suf_wg)
-      need = w == 0 && jm - a.n_pre_wg < a.n_suffix_items;
-    else
-      need = (jm - a.n_pre_wg - a.n_suf_wg) * kWaves + w < a.n_merge_items + a.n_zero_items;
+    // a merge mate is not waited for: its part of the layer comes last (the host places merges
+    // opposite prefix work-groups, which load their next layer only when it may start)
+    int im;
+    const int rm = wg_role(a, jm, im);
+    const bool need = w == 0 && (rm == 0 ? im < a.n_prefix_items : rm == 1 ? im < a.n_suffix_items : false);
     const int32_t* line = peer_line(a, jm * a.Hkv + g);
     if (need && __hip_atomic_load(line + 4, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == cu_id() + 1) {
       const int32_t target = (int32_t)((uint32_t)a.peer_base + (uint32_t)l + 1u);
@@ -903,12 +918,14 @@ __global__ __launch_bounds__(kBlockThreads, SH::MIN_WAVES) void layers_kernel(co
       (__builtin_amdgcn_s_getreg(kXccIdReg) & 15) != (int)((blockIdx.x + a.l2_check_shift) % a.l2_xcds))
     __hip_atomic_store(a.status, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   const int g = blockIdx.x % a.Hkv, j = blockIdx.x / a.Hkv;
-  if (j < a.n_pre_wg)
-    prefix_loop<SH, L2>(a, g, j, smem);
-  else if (j < a.n_pre_wg + a.n_suf_wg)
-    suffix_loop<SH, L2>(a, g, j - a.n_pre_wg, smem);
-  else if (j < a.n_pre_wg + a.n_suf_wg + a.n_merge_wg)
-    merge_loop<SH, L2>(a, g, j - a.n_pre_wg - a.n_suf_wg);
+  int idx;
+  const int role = wg_role(a, j, idx);
+  if (role == 0)
+    prefix_loop<SH, L2>(a, g, idx, smem);
+  else if (role == 1)
+    suffix_loop<SH, L2>(a, g, idx, smem);
+  else
+    merge_loop<SH, L2>(a, g, idx);
   if (a.clock_start) {
     __syncthreads();
     if (threadIdx.x == 0)

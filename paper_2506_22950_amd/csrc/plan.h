@@ -101,11 +101,12 @@ struct StepArgs {
   // Step launch through every layer (infs_decode_step_layers); unused by per-layer launches.
   // Layer l reads q + l * q_layer_stride (knew, vnew alike) and writes o + l * o_layer_stride; the
   // prefix store and page pool of layer l are prefix + l * prefix_layer_bytes and pool + l *
-  // pool_layer_bytes.  Per KV head, the first n_pre_wg work-groups take the prefix items round
-  // robin, the next n_suf_wg the response items, and the next n_merge_wg work-groups do one slot's
-  // merge (or zeroing) per wavefront.
+  // pool_layer_bytes.  Per KV head (work-groups j = 0 .. n_pre_wg + n_suf_wg + n_merge_wg - 1), the
+  // first n_pre_wg take the prefix items round robin, j = merge_j0 .. merge_j0 + n_merge_wg - 1 do
+  // one slot's merge (or zeroing) per wavefront, and the others, in order, the response items.
   int32_t num_layers;
   int32_t n_pre_wg, n_suf_wg, n_merge_wg;
+  int32_t merge_j0;                    // first merge work-group of a KV head (>= n_pre_wg)
   int64_t q_layer_stride, kv_layer_stride, o_layer_stride;
   int64_t prefix_layer_bytes, pool_layer_bytes;
   int32_t* merged;                     // per prompt, kCounterStride apart: merges completed (they only grow);

@@ -960,6 +960,9 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     }
     a.n_pre_wg = std::max(pre, 0);
     a.n_suf_wg = prod - a.n_pre_wg;
+    // Merges go opposite the prefix work-groups (index j shares its CU with j + nj/2, see
+    // mate_gate), else after the response work-groups.
+    a.merge_j0 = (nj % 2 == 0 && a.n_pre_wg <= nj / 2 && a.n_merge_wg <= nj / 2) ? nj / 2 : a.n_pre_wg + a.n_suf_wg;
     if ((npi > 0 && a.n_pre_wg < 1) || (nsi > 0 && a.n_suf_wg < 1))
       return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
                   "chunks, response chunks and merges", nj);
