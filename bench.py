@@ -437,7 +437,7 @@ ENTRIES = {"step": "decode_step_layers", "layer": "decode_step"}
 
 
 class Bench:
-    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False, entry="step"):
+    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False, entry="step", overrides=None):
         import numpy as np
         import torch
 
@@ -449,7 +449,7 @@ class Bench:
         self.np, self.torch = np, torch
         self.entry = ENTRIES[entry]
         infs.load()
-        cfg = get_config(cfg_name)
+        cfg = get_config(cfg_name, **(overrides or {}))
         self.cfg = cfg
         t0 = time.time()
         self.wl = wl = Workload(cfg)
@@ -533,6 +533,27 @@ class Bench:
         assert steps == len(self.log), (steps, len(self.log))
         for p in range(self.cfg.num_prompts):
             assert np.array_equal(self.ctx.sample_tokens(p), self.wl.L[p]), "token counters"
+
+    def host_cost(self):
+        """Host time per decode call of the entry: the whole group replayed on a
+        dry-run context (the Python step loop, ctypes and the library's host
+        planning and bookkeeping; no device work, no launch).  Returns
+        (us per call, calls per group decode)."""
+        from paper_2506_22950_amd.group import context_for, decode_group, schedulers_for
+
+        cfg = self.cfg
+        ctx = context_for(cfg, dry_run=True, probe_tokens=self.reuse)
+        for p in range(cfg.num_prompts):
+            for layer in range(cfg.layers):
+                ctx.prefill_shared(p, layer, cfg.prompt_lens[p], None, None)
+        nothing = (None, None, None, None)
+        t0 = time.perf_counter()
+        steps = decode_group(ctx, schedulers_for(cfg, cfg.policy, self.wl.L_hat), self.wl.L, cfg.layers,
+                             lambda k, layer: nothing, reuse=self.reuse, entry=self.entry)
+        dt = time.perf_counter() - t0
+        ctx.destroy()
+        calls = steps * (1 if self.entry == "decode_step_layers" else cfg.layers)
+        return dt * 1e6 / calls, calls
 
     def event_timing(self):
         """One more whole group decode: HIP events on the library's stream (the
@@ -666,6 +687,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="qwen3_1p7b_g64")
     ap.add_argument("--split", type=int, default=0)
+    ap.add_argument("--G", type=int, help="samples per prompt (overrides the workload's)")
+    ap.add_argument("--m", type=int, help="slots per prompt")
+    ap.add_argument("--prompt-len", help="prompt lengths, comma separated (one per prompt)")
+    ap.add_argument("--policy", choices=("naive", "fixed_row", "fifo", "sjf", "fptas", "fptas_sjf", "lpt"),
+                    help="refill policy")
+    ap.add_argument("--seed", type=int, help="seed of the length, prediction and Q/K/V draws")
+    ap.add_argument("--dtype", choices=("bf16", "f32"), help="storage type of Q, K, V")
+    ap.add_argument("--layers", type=int, help="number of layers")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--reuse", type=int, default=0, metavar="K",
@@ -715,7 +744,13 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         copy_calibration(torch)
-    b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8, entry=args.entry)
+    overrides = {k: v for k, v in (("samples_per_prompt", args.G), ("slots_per_prompt", args.m),
+                                    ("policy", args.policy), ("seed", args.seed), ("dtype", args.dtype),
+                                    ("layers", args.layers)) if v is not None}
+    if args.prompt_len:
+        overrides["prompt_lens"] = tuple(int(x) for x in args.prompt_len.split(","))
+    b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8, entry=args.entry,
+              overrides=overrides)
     if args.exchange is not None:
         b.ctx.set_exchange(args.exchange)
 
@@ -751,7 +786,7 @@ def main():
         achieved = per_launch / (avg_us * 1e-6) / 1e9
         kernel = KERNELS[b.entry]
         traffic = (read_traffic(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.exchange is not None
-                                                               or args.split) else None)
+                                                               or args.split or overrides) else None)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": kernel,
@@ -764,7 +799,7 @@ def main():
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}
-        mf = read_mfma(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.split) else None
+        mf = read_mfma(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.split or overrides) else None
         if mf is not None:
             fl = float(mf["mfma_flops_per_launch"])
             roof["mfma"] = {"kernel": f"{kernel} (prefix and response contractions)", "flops_per_launch": round(fl),
@@ -795,6 +830,8 @@ def main():
                      "frac": round(pach / PEAK_HBM_GBS, 4), "phase_ms": round(pregion, 2)}
             log(f"probe: {pn} launches, avg {pavg:.2f} us, {pper / 1e6:.2f} MB/launch -> {pach:.0f} GB/s")
 
+    host_us, host_calls = b.host_cost()
+    log(f"host: {host_us:.1f} us per {b.entry} call (dry-run replay), {host_calls} calls per group decode")
     cpu = None if args.no_cpu_baseline else cpu_baseline(b)
     cfg = b.cfg
     out = {
@@ -823,9 +860,14 @@ def main():
             "kv_cache": "e4m3" if args.kv_fp8 else cfg.dtype,
             "staged_steps": b.window,
             "exchange": {0: "coherence point", 1: "xcd l2"}[b.ctx.exchange_mode()],
+            "entry": b.entry,
+            "overrides": {k: (list(v) if isinstance(v, tuple) else v) for k, v in overrides.items()},
         },
         "roofline": roof,
         "probe": probe,
+        "host": {"us_per_call": round(host_us, 2), "calls_per_group_decode": host_calls,
+                 "timing": "the group replayed on a dry-run context: Python step loop, ctypes and the library's "
+                           "host planning, no device work"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
