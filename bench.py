@@ -312,6 +312,16 @@ def summarize_mfma(workload, pmc_dir, entry="decode_step_layers"):
     return "\n".join(lines)
 
 
+def summarize_counter(counter, pmc_dir, entry="decode_step_layers"):
+    """Mean of one --pmc counter per launch of the entry's kernel (summed over
+    its hardware instances), with the number of launches it covers."""
+    kernel = KERNELS[entry]
+    vals = [float(r["Counter_Value"]) for r in _pmc_rows(pmc_dir, counter) if kernel in r["Kernel_Name"]]
+    if not vals:
+        raise SystemExit(f"{counter}: no {kernel} rows under {pmc_dir}")
+    return f"{kernel} {counter}: {sum(vals) / len(vals):.1f} per launch over {len(vals)} launches"
+
+
 def summarize_stats(workload, stats_dir, bench_out, entry="decode_step_layers", command=""):
     """Kernel statistics table of a `rocprofv3 --kernel-trace --stats` run of
     `bench.py --steps K --warmup W` (without --no-kernel-timing): the run decodes
@@ -714,6 +724,8 @@ def main():
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_DIR", "BENCH_OUT"),
                     help="print the kernel statistics of a rocprofv3 --kernel-trace --stats run of bench.py "
                          "(BENCH_OUT: the JSON line that run printed)")
+    ap.add_argument("--summarize-counter", nargs=2, metavar=("COUNTER", "PMC_DIR"),
+                    help="print the mean per launch of one counter of a rocprofv3 --pmc run")
     ap.add_argument("--profile-command", default="",
                     help="the profiled command line, quoted in the --summarize-stats header")
     ap.add_argument("--summarize-mfma", metavar="PMC_DIR",
@@ -721,6 +733,9 @@ def main():
     ap.add_argument("--schedules", action="store_true",
                     help="print the running steps of the refill policies (host only, no GPU) and exit")
     args = ap.parse_args()
+    if args.summarize_counter:
+        print(summarize_counter(args.summarize_counter[0], args.summarize_counter[1], entry=ENTRIES[args.entry]))
+        return
     if args.summarize_stats:
         print(summarize_stats(args.workload, *args.summarize_stats, entry=ENTRIES[args.entry],
                               command=args.profile_command))
