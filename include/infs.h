@@ -254,9 +254,10 @@ infs_status infs_decode_step_static(infs_ctx* ctx, int32_t layer, const void* q_
    The launch keeps as many work-groups as the GPU holds resident at once (infs_step_launch_workgroups)
    and walks the layers in order: the queries and new K/V rows of layer l are read only after every
    merge of layer l-1 of the same prompt has written its O rows (as a model's layer l would need), while
-   the cached prefix and response K/V of layer l may be loaded earlier.  Split-K partials always go
-   through the device coherence point here (the exchange mode of infs_set_exchange applies to
-   infs_decode_step).  Every device wait is bounded (infs_set_merge_wait); a wait that gives up makes the
+   the cached prefix and response K/V of layer l may be loaded earlier.  Split-K partials follow the
+   exchange mode of infs_set_exchange, as in infs_decode_step (in mode 1 the merges load them past the
+   CU's L1: the launch rewrites them in every layer).  Every device wait is bounded
+   (infs_set_merge_wait); a wait that gives up makes the
    next synchronising call return E_DEVICE.  The launch needs all its work-groups on the GPU at once: other
    work running on the same GPU at the same time can delay it until its waits give up.
    E_STATE: a layer of this step was already decoded, a probe step is open, a live slot's prompt lacks
@@ -302,7 +303,8 @@ infs_status infs_sync(infs_ctx* ctx);
    that error path from the host.  E_STATE while a step is open. */
 infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
 
-/* How work-groups of one decode launch hand their split-K partials to the merging work-group.
+/* How work-groups of one decode or step launch hand their split-K partials to the merging
+   work-group.
    mode 0: stores written through to the device coherence point, loads from it: correct wherever
            work-groups run.
    mode 1: through the L2 of the XCD that runs a KV head's work-groups (fewer trips to the
