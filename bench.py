@@ -101,16 +101,19 @@ def read_mfma(workload, kernel):
     return _read_summary(MFMA_FILE.format(kernel=kernel, workload=workload))
 
 
-def mfma_flops(cfg, steplog, split=256):
+def mfma_flops(cfg, steplog, split=256, nj=None):
     """MFMA flops issued by all launches of a group decode (2 flops per
     multiply-add of every 16x16x32 tile issued), every KV head, every layer:
     (prefix) per prompt with a live slot, S^T = K Q^T and O^T = V^T P^T over
     the padded row tile (m * hpk rows padded to 16/32/64/128) and 32-token
     blocks; (responses, bf16 and E4M3 pages) per live slot, per wavefront of
-    each split-K chunk, per 32-token page pair of its stored tokens (the newest
+    each split-K item, per 32-token page pair of its stored tokens (the newest
     token is folded in apart): two S^T tiles of head_dim / 32 steps, then
     head_dim / 16 O^T tiles and one row-sum tile, each 16 columns wide with hpk
-    of them carrying query rows.  fp32 contexts issue no MFMA."""
+    of them carrying query rows.  The items are the per-layer launch's chunks
+    of `split` tokens, or, with nj (work-groups per KV head of a step launch),
+    the items the library's step-launch plan gives each step
+    (infs_step_split_plan).  fp32 contexts issue no MFMA."""
     if cfg.dtype != "bf16":
         return 0.0
     rows = cfg.slots_per_prompt * cfg.hpk
@@ -135,10 +138,48 @@ def mfma_flops(cfg, steplog, split=256):
             pairs_memo[length] = n
         return pairs_memo[length]
 
+    def wave_pairs(length, ranges):  # ranges: each wavefront's [w0, w1) token range
+        last = length - 1
+        n = 0
+        for w0, w1 in ranges:
+            te = last if w0 <= last < w1 else w1
+            n += -(-(te - w0) // 32) if te > w0 else 0
+        return n
+
+    def piece_pairs(length, n):  # near-equal page ranges, as the step launch cuts them
+        pages = -(-length // 16)
+        ranges = []
+        for c in range(n):
+            pg0, pg1 = c * pages // n, (c + 1) * pages // n
+            ppw = -(-(pg1 - pg0) // 4)
+            t1 = min(pg1 * 16, length)
+            for w in range(4):
+                w0 = min((pg0 + w * ppw) * 16, t1)
+                ranges.append((w0, min(w0 + ppw * 16, t1)))
+        return wave_pairs(length, ranges)
+
+    plan = None
+    if nj is not None:
+        from paper_2506_22950_amd import infs
+
+        scmax = -(-cfg.max_suffix_len // split)
+        chunks = [-(-plen // 128) for plen in cfg.prompt_lens]
+
+        def plan(row):
+            lens = [e[2] if e is not None else 0 for e in row]
+            npi = sum(chunks[p] for p in {e[0] for e in row if e is not None})
+            roles, pieces = infs.step_split_plan(nj, lens, npi, 128, split, scmax)
+            return roles["cut"], pieces
+
     total = 0
     for row in steplog:
         total += sum(per_prompt[p] for p in {e[0] for e in row if e is not None})
-        total += sum(pairs(e[2]) for e in row if e is not None) * per_pair * cfg.num_kv_heads
+        cut, pieces = plan(row) if plan is not None else (0, None)
+        if cut:
+            n = sum(piece_pairs(e[2], int(pieces[s])) for s, e in enumerate(row) if e is not None)
+        else:
+            n = sum(pairs(e[2]) for e in row if e is not None)
+        total += n * per_pair * cfg.num_kv_heads
     return total * cfg.layers
 
 
@@ -294,7 +335,14 @@ def summarize_mfma(workload, pmc_dir, entry="decode_step_layers"):
     busy = per["SQ_VALU_MFMA_BUSY_CYCLES"][1]
     cu_busy_quads = per["SQ_BUSY_CU_CYCLES"][1]
     gui = per["GRBM_GUI_ACTIVE"][1] / XCDS
-    expect = mfma_flops(cfg, steplog) / launches
+    nj = None
+    if entry == "decode_step_layers":  # the step launch's plan depends on the device's work-group count
+        from paper_2506_22950_amd.group import context_for
+
+        ctx = context_for(cfg)
+        nj = ctx.step_launch_workgroups // cfg.num_kv_heads
+        ctx.destroy()
+    expect = mfma_flops(cfg, steplog, nj=nj) / launches
     lines = [
         f"kernel_source_sha256 = {kernel_source_hash()}",
         f"workload = {workload}",
@@ -714,6 +762,9 @@ def main():
     ap.add_argument("--exchange", type=int, choices=(0, 1), default=None,
                     help="partial exchange: 0 through the coherence point, 1 through the XCD's L2 "
                          "(default: the library's choice)")
+    ap.add_argument("--step-split", type=int, choices=(0, 1), default=None,
+                    help="work split of step launches: 1 near-equal response pieces (the library's default), "
+                         "0 the per-layer launch's chunks")
     ap.add_argument("--entry", choices=tuple(ENTRIES), default="step",
                     help="step: one launch per running step through every layer (infs_decode_step_layers); "
                          "layer: one launch per layer (infs_decode_step)")
@@ -768,6 +819,8 @@ def main():
               overrides=overrides)
     if args.exchange is not None:
         b.ctx.set_exchange(args.exchange)
+    if args.step_split is not None:
+        b.ctx.set_step_split(args.step_split)
 
     for w in range(args.warmup):
         t0 = time.time()
@@ -801,7 +854,8 @@ def main():
         achieved = per_launch / (avg_us * 1e-6) / 1e9
         kernel = KERNELS[b.entry]
         traffic = (read_traffic(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.exchange is not None
-                                                               or args.split or overrides) else None)
+                                                               or args.step_split is not None or args.split
+                                                               or overrides) else None)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": kernel,
@@ -876,6 +930,8 @@ def main():
             "staged_steps": b.window,
             "exchange": {0: "coherence point", 1: "xcd l2"}[b.ctx.exchange_mode()],
             "entry": b.entry,
+            "step_split": {0: "per-layer chunks", 1: "response pieces"}[1 if args.step_split is None
+                                                                          else args.step_split],
             "overrides": {k: (list(v) if isinstance(v, tuple) else v) for k, v in overrides.items()},
         },
         "roofline": roof,

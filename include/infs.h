@@ -316,6 +316,31 @@ infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
    E_STATE while a step is open or when mode 1/2 is unavailable (always on dry-run contexts). */
 infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
 
+/* How an infs_decode_step_layers launch divides a step's work among its producer work-groups.
+   mode 1 (default): each live response is cut into near-equal page ranges, at most one per response
+           work-group when the live slots allow, and the number of prefix work-groups is chosen with
+           the cuts so that the most tokens any one work-group reads is as small as it can be (a layer
+           waits for the work-group that reads the most after its queries arrive).
+   mode 0: responses in chunks of split_tokens and work-groups divided in proportion to the chunk
+           counts, the partition of infs_decode_step: outputs then differ from a per-layer decode only
+           in the order the merges add partials.
+   Both give the same results up to rounding (mode 1 moves the split-K boundaries).  E_ARG for another
+   mode; E_STATE while a step is open. */
+infs_status infs_set_step_split(infs_ctx* ctx, int32_t mode);
+
+/* The work split a step launch in `mode` (as infs_set_step_split) uses for one step, with nj
+   work-groups per KV head (infs_step_launch_workgroups / num_kv_heads), S slots of which slot s holds
+   len[s] tokens (0 = idle), n_prefix_items prefix chunks of prefix_split tokens, response chunks of
+   `split` tokens (split_tokens of the context, 256 for 0) and at most scmax of them per slot
+   (ceil(max_suffix_len / split)).  Writes pieces[0..S) (response items per slot) and roles[0..5) =
+   {prefix work-groups, response work-groups, merge work-groups, response items, 1 if the responses
+   are cut into near-equal page ranges else 0 for chunks of `split` tokens}.  A pure function for
+   diagnostics and tests.  E_ARG: nj < 2, S outside [1, 64], split not a multiple of 16 in [16, 4096],
+   scmax < 1, a len outside [0, scmax * split], mode not 0 or 1, null arrays. */
+infs_status infs_step_split_plan(int32_t nj, int32_t S, int32_t n_prefix_items, int32_t prefix_split,
+                                 const int32_t* len, int32_t split, int32_t scmax, int32_t mode, int32_t* pieces,
+                                 int32_t* roles);
+
 /* The current exchange mode (0, 1 or 2); -1 for a NULL context. */
 int32_t infs_exchange_mode(const infs_ctx* ctx);
 

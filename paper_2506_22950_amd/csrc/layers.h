@@ -3,12 +3,13 @@
 //
 // The grid holds as many work-groups as the GPU keeps resident at once, so
 // every work-group runs from the start and none waits for a slot.  Per KV
-// head g, the first n_pre_wg work-groups take the step's prefix chunks and the
-// next n_suf_wg its response chunks, round robin, for every layer in turn (the
-// same items every layer).  The following n_merge_wg work-groups of the head
-// merge: wavefront k of them handles slots
-// k, k + 4 * n_merge_wg, ... of every layer, one (slot, KV head) merge per
-// wavefront at a time (an idle slot only gets its O rows zeroed).
+// head g, n_pre_wg work-groups take the step's prefix chunks and n_suf_wg its
+// response pieces (each live response cut into near-equal page ranges, see
+// step_plan.h), round robin, for every layer in turn (the same items every
+// layer).  Of the n_merge_wg merge work-groups of the head, wavefront k
+// handles slots k, k + 4 * n_merge_wg, ... of every layer, one (slot, KV
+// head) merge per wavefront at a time (an idle slot only gets its O rows
+// zeroed).
 //
 // Layer order.  In a real model the queries and the new K/V rows of layer l
 // come from layer l-1's outputs, so a producer of layer l > 0 reads them only
@@ -50,6 +51,7 @@
 #include <type_traits>
 
 #include "decode.h"
+#include "step_plan.h"
 
 namespace infs {
 namespace {
@@ -507,7 +509,8 @@ struct PrefixMfma {
 // ---- Response chunk, fp32 pages on wavefront dot products (see suffix_chunk) -
 struct RespItem {
   int s, c, len, wt0, wt1, last;
-  bool has_new;
+  bool has_new;  // this wavefront's range holds the newest token
+  bool tail;     // the item is the slot's last piece
 };
 __device__ __forceinline__ RespItem resp_item(const StepArgs& a, int it) {
   // The slot of response item `it`: slots' first items never decrease and an
@@ -526,10 +529,23 @@ __device__ __forceinline__ RespItem resp_item(const StepArgs& a, int it) {
   r.s = s;
   r.c = it - a.slot[s].item_begin;
   r.len = a.slot[s].len;
-  const int w = threadIdx.x >> 6, sub = a.split / 4;
-  const int t0 = r.c * a.split, t1 = min(t0 + a.split, r.len);
-  r.wt0 = min(t0 + w * sub, t1);
-  r.wt1 = min(r.wt0 + sub, t1);
+  const int n = a.slot[s].pieces, w = threadIdx.x >> 6;
+  if (a.resp_cut) {
+    // piece c of n near-equal page ranges; wavefront w takes the w-th run of
+    // ppw pages of it
+    const int pages = (r.len + kPageTokens - 1) / kPageTokens;
+    const int pg0 = piece_first_page(r.c, pages, n), pg1 = piece_first_page(r.c + 1, pages, n);
+    const int ppw = piece_wave_pages(pg1 - pg0);
+    const int t1 = min(pg1 * kPageTokens, r.len);
+    r.wt0 = min((pg0 + w * ppw) * kPageTokens, t1);
+    r.wt1 = min(r.wt0 + ppw * kPageTokens, t1);
+  } else {
+    // chunk c of `split` tokens, a quarter per wavefront
+    const int sub = a.split / kWaves, t0 = r.c * a.split, t1 = min(t0 + a.split, r.len);
+    r.wt0 = min(t0 + w * sub, t1);
+    r.wt1 = min(r.wt0 + sub, t1);
+  }
+  r.tail = r.c == n - 1;
   r.last = r.len - 1;
   r.has_new = r.last >= r.wt0 && r.last < r.wt1;
   return r;
@@ -582,7 +598,7 @@ struct Resp {
       }
     }
     wave_combine_groups<SH, HPK>(m, l, o);
-    if (V.layer == 0 && r.c * a.split + a.split >= r.len && g == 0 && threadIdx.x == 0) {
+    if (V.layer == 0 && r.tail && g == 0 && threadIdx.x == 0) {
       // bookkeeping of this step's token, once per step (its K/V are stored above)
       a.page_table[(int64_t)sp.seq * a.pages_per_slot + (r.last >> 4)] = sp.cur_page;
       __hip_atomic_fetch_add(&a.tokens[(r.s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -632,7 +648,7 @@ struct RespTiles {
       if (base != r.wt0) RM::load_round(V.pool, pages, a.Hkv, g, (base - r.wt0) >> 4, R);
       RM::round(R, bq, base, te, a.scale_log2, A);
     }
-    if (V.layer == 0 && r.c * a.split + a.split >= r.len && g == 0 && threadIdx.x == 0) {
+    if (V.layer == 0 && r.tail && g == 0 && threadIdx.x == 0) {
       // bookkeeping of this step's token, once per step (its K/V are stored above)
       a.page_table[(int64_t)sp.seq * a.pages_per_slot + (r.last >> 4)] = sp.cur_page;
       __hip_atomic_fetch_add(&a.tokens[(r.s / a.m) * a.G + sp.sample], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -677,7 +693,7 @@ __device__ void merge_wave(const StepArgs& a, const LayerView& V, int s, int g, 
     return;
   }
   const int nP = a.prompt[p].nchunks;
-  const int n = nP + (a.slot[s].len + a.split - 1) / a.split;
+  const int n = nP + a.slot[s].pieces;
   const int64_t pbase = ((int64_t)p * a.Hkv + g) * a.prefix_chunks_max * SH::PR + si * HPK;
   const int64_t sbase = prefix_records(a, SH::PR) + ((int64_t)s * a.Hkv + g) * a.suffix_chunks_max * HPK;
   auto rec = [&](int c, int j) -> int64_t { return (c < nP ? pbase + (int64_t)c * SH::PR : sbase + (int64_t)(c - nP) * HPK) + j; };
@@ -878,7 +894,7 @@ __device__ void merge_loop(const StepArgs& a, int g, int mj) {
       if (e < a.n_merge_items) {
         const int s = a.live_slot[e];
         const int p = s / a.m;
-        const uint32_t per = (uint32_t)((a.slot[s].len + a.split - 1) / a.split + a.prompt[p].nchunks);
+        const uint32_t per = (uint32_t)(a.slot[s].pieces + a.prompt[p].nchunks);
         const int32_t target = (int32_t)((uint32_t)a.slot[s].target + (uint32_t)(l + 1) * per);
         merge_wave<SH, L2>(a, V, s, g, target);
         // Counted once this wavefront's partial loads and O stores have completed;

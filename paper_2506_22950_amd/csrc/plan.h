@@ -47,7 +47,9 @@ struct SlotPlan {
                        // through every layer, the value before the launch (each layer adds the
                        // slot's producer count)
   int32_t seq;         // page-table row of the sample's response (a sequence handle)
-  int32_t pad_[2];
+  int32_t pieces;      // response items of the slot: ceil(len / split) chunks in a per-layer launch; in a
+                       // step launch, near-equal page ranges (see step_plan.h), item_begin counting them
+  int32_t pad_;
 };
 
 struct PromptPlan {
@@ -106,6 +108,8 @@ struct StepArgs {
   // one slot's merge (or zeroing) per wavefront, and the others, in order, the response items.
   int32_t num_layers;
   int32_t n_pre_wg, n_suf_wg, n_merge_wg;
+  int32_t resp_cut;                    // 1: slot s's response items are its slot[s].pieces near-equal page
+                                       // ranges (step_plan.h); 0: chunks of `split` tokens
   int32_t merge_j0;                    // first merge work-group of a KV head (>= n_pre_wg)
   int64_t q_layer_stride, kv_layer_stride, o_layer_stride;
   int64_t prefix_layer_bytes, pool_layer_bytes;

@@ -16,6 +16,7 @@
 
 #include "infs.h"
 #include "kernels.h"
+#include "step_plan.h"
 #include "plan.h"
 
 using infs::KernelKey;
@@ -89,6 +90,7 @@ struct infs_ctx {
   uint32_t peer_progress = 0;  // peer-line progress value reached by the step launches so far
   bool step_open = false;
   // Probe phase of prefix reuse.
+  int step_split = 1;                              // infs_set_step_split: 1 planned pieces, 0 per-layer chunks
   int probe_k = 0;                                 // probe tokens per sample (0: no prefix reuse)
   int probe_batch = 0;                             // most samples per probe launch
   KernelKey pkey{};                                // kernel of probe launches
@@ -277,6 +279,7 @@ infs_status open_step(infs_ctx* c) {
     sp.cur_page = c->seq_pages[h][pos / infs::kPageTokens];
     sp.sample = (int32_t)c->slot_sample[s];
     const int nch = ceil_div(len, c->split);
+    sp.pieces = nch;
     items += nch;
     const int P = a.prompt[s / c->m].plen;
     bytes += 2.0 * (len - 1) * kvrow + 2.0 * kvrow_in + 2.0 * kvrow + (double)c->Hq * c->D * (c->es + 4);
@@ -946,32 +949,36 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     a.merged = merged_counters(c);
     a.peer = peer_lines(c);
     a.peer_base = (int32_t)c->peer_progress;
-    // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix and
-    // response chunks in proportion to their counts (at least one each when there are any).
+    // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix chunks
+    // and response pieces so that no producer reads many more tokens than the others.
     const int nj = c->layers_resident / c->Hkv;
-    a.n_merge_wg = std::min(ceil_div(c->S, infs::kWaves), nj - 1);
-    const int prod = nj - a.n_merge_wg;
-    const int npi = a.n_prefix_items, nsi = a.n_suffix_items;
-    int pre = 0;
-    if (npi > 0) {
-      pre = (int)((int64_t)prod * npi / std::max(1, npi + nsi));
-      pre = std::max(1, std::min(pre, npi));
-      if (nsi > 0) pre = std::min(pre, prod - 1);
+    int32_t lens[infs::kMaxSlots], pieces[infs::kMaxSlots];
+    for (int s = 0; s < c->S; ++s) lens[s] = a.slot[s].len;
+    const infs::StepRoles roles =
+        c->step_split ? infs::plan_step_roles(nj, c->S, a.n_prefix_items, c->prefix_split, lens, c->split, c->scmax,
+                                              pieces)
+                      : infs::plan_step_roles_chunks(nj, c->S, a.n_prefix_items, lens, c->split, pieces);
+    if ((a.n_prefix_items > 0 && roles.n_pre < 1) || (roles.n_suffix_items > 0 && roles.n_suf < 1))
+      return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
+                  "chunks, response chunks and merges", nj);
+    a.n_merge_wg = roles.n_merge;
+    a.n_pre_wg = roles.n_pre;
+    a.n_suf_wg = roles.n_suf;
+    for (int s = 0, items = 0; s < c->S; ++s) {
+      a.slot[s].pieces = pieces[s];
+      a.slot[s].item_begin = items;
+      items += pieces[s];
     }
-    a.n_pre_wg = std::max(pre, 0);
-    a.n_suf_wg = prod - a.n_pre_wg;
+    a.n_suffix_items = roles.n_suffix_items;
+    a.resp_cut = roles.cut ? 1 : 0;
     // Merges go opposite the prefix work-groups (index j shares its CU with j + nj/2, see
     // mate_gate), else after the response work-groups.
     a.merge_j0 = (nj % 2 == 0 && a.n_pre_wg <= nj / 2 && a.n_merge_wg <= nj / 2) ? nj / 2 : a.n_pre_wg + a.n_suf_wg;
-    if ((npi > 0 && a.n_pre_wg < 1) || (nsi > 0 && a.n_suf_wg < 1))
-      return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
-                  "chunks, response chunks and merges", nj);
     // counter targets: each slot counts its producers once per layer, each prompt its merges
     for (int s = 0; s < c->S; ++s) {
       a.slot[s].target = (int32_t)c->slot_arrivals[s];
       if (a.slot[s].len > 0)
-        c->slot_arrivals[s] +=
-            (uint32_t)c->L * (uint32_t)(ceil_div(a.slot[s].len, c->split) + a.prompt[s / c->m].nchunks);
+        c->slot_arrivals[s] += (uint32_t)c->L * (uint32_t)(a.slot[s].pieces + a.prompt[s / c->m].nchunks);
     }
     for (int p = 0; p < c->NP; ++p) {
       int live = 0;
@@ -1098,6 +1105,35 @@ infs_status infs_set_exchange(infs_ctx* c, int32_t mode) {
                 c->dry ? "dry-run context" : "work-groups of one KV head do not share an XCD on this device");
   c->plan.l2_xcds = mode > 0 ? c->l2_xcds : 0;
   c->plan.l2_check_shift = mode == 2 ? 1 : 0;
+  return INFS_OK;
+}
+
+infs_status infs_step_split_plan(int32_t nj, int32_t S, int32_t n_prefix_items, int32_t prefix_split,
+                                 const int32_t* len, int32_t split, int32_t scmax, int32_t mode, int32_t* pieces,
+                                 int32_t* roles) {
+  if (nj < 2 || S < 1 || S > infs::kMaxSlots || n_prefix_items < 0 || prefix_split < 1 || split < infs::kWaves ||
+      split > infs::kMaxSplit || split % infs::kPageTokens || scmax < 1 || mode < 0 || mode > 1)
+    return fail(nullptr, INFS_E_ARG, "step_split_plan: nj >= 2, S in [1, %d], split a page multiple up to %d, "
+                "scmax >= 1 and mode 0 or 1", infs::kMaxSlots, infs::kMaxSplit);
+  if (!len || !pieces || !roles) return fail(nullptr, INFS_E_ARG, "step_split_plan: null array");
+  for (int s = 0; s < S; ++s)
+    if (len[s] < 0 || len[s] > scmax * split)
+      return fail(nullptr, INFS_E_ARG, "step_split_plan: len[%d] = %d outside [0, scmax * split]", s, len[s]);
+  const infs::StepRoles r = mode ? infs::plan_step_roles(nj, S, n_prefix_items, prefix_split, len, split, scmax, pieces)
+                                 : infs::plan_step_roles_chunks(nj, S, n_prefix_items, len, split, pieces);
+  roles[0] = r.n_pre;
+  roles[1] = r.n_suf;
+  roles[2] = r.n_merge;
+  roles[3] = r.n_suffix_items;
+  roles[4] = r.cut ? 1 : 0;
+  return INFS_OK;
+}
+
+infs_status infs_set_step_split(infs_ctx* c, int32_t mode) {
+  CHECK_CTX(c);
+  if (mode < 0 || mode > 1) return fail(c, INFS_E_ARG, "step split mode must be 0 or 1");
+  if (c->step_open || c->probe_open) return fail(c, INFS_E_STATE, "set_step_split while a step is open");
+  c->step_split = mode;
   return INFS_OK;
 }
 

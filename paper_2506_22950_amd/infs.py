@@ -38,7 +38,8 @@ EXPORTS = (
     "infs_sched_destroy", "infs_fptas_assign", "infs_probe_step", "infs_end_probe_step", "infs_probe_batch",
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
     "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode", "infs_decode_step_static",
-    "infs_sched_optimum", "infs_decode_step_layers", "infs_step_launch_workgroups",
+    "infs_sched_optimum", "infs_decode_step_layers", "infs_step_launch_workgroups", "infs_set_step_split",
+    "infs_step_split_plan",
 )
 
 
@@ -101,6 +102,9 @@ def load():
         "infs_get_kernel_info": (I32, [P, ctypes.POINTER(KernelInfo)]),
         "infs_set_exchange": (I32, [P, I32]),
         "infs_exchange_mode": (I32, [P]),
+        "infs_set_step_split": (I32, [P, I32]),
+        "infs_step_split_plan": (I32, [I32, I32, I32, I32, ctypes.POINTER(I32), I32, I32, I32, ctypes.POINTER(I32),
+                                       ctypes.POINTER(I32)]),
         "infs_timing_begin": (I32, [P]),
         "infs_timing_end": (I32, [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
                                   ctypes.POINTER(I64)]),
@@ -290,6 +294,11 @@ class Context:
     def exchange_mode(self) -> int:
         return load().infs_exchange_mode(self._h)
 
+    def set_step_split(self, mode: int):
+        """Work split of step launches: 1 near-equal response pieces (default), 0 the
+        per-layer launch's chunks."""
+        self._call(load().infs_set_step_split, mode)
+
     def kernel_info(self) -> dict:
         """The decode (and probe) kernel instantiation this context runs."""
         k = KernelInfo()
@@ -377,3 +386,17 @@ def sched_optimum(lengths, m, max_nodes=20_000_000):
     if st != OK:
         raise InfsError(st, "infs_sched_optimum")
     return best.value, lower.value, slot
+
+
+def step_split_plan(nj, lens, n_prefix_items, prefix_split, split, scmax, mode=1):
+    """infs_step_split_plan: (roles, pieces) of one step launch, roles = dict(n_pre, n_suf, n_merge,
+    items, cut) and pieces[s] the response items of slot s."""
+    L = np.ascontiguousarray(lens, dtype=np.int32)
+    pieces = np.zeros(len(L), dtype=np.int32)
+    roles = np.zeros(5, dtype=np.int32)
+    I32P = ctypes.POINTER(ctypes.c_int32)
+    st = load().infs_step_split_plan(nj, len(L), n_prefix_items, prefix_split, L.ctypes.data_as(I32P), split, scmax,
+                                     mode, pieces.ctypes.data_as(I32P), roles.ctypes.data_as(I32P))
+    if st != OK:
+        raise InfsError(st, "infs_step_split_plan")
+    return dict(zip(("n_pre", "n_suf", "n_merge", "items", "cut"), (int(x) for x in roles))), pieces

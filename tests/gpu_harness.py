@@ -22,14 +22,16 @@ def say(*a):
 
 
 def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
-                  probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step", scale=0.0):
+                  probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step", scale=0.0,
+                  step_split=None):
     """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
     reuse first; if `probe` is a dict it receives 'log' (probe step log) and
     'captured' (the O buffer [L, batch, Hq, d] after every probe step).
     inspect(ctx, step, log) is called after every decode step; kv_fp8 stores the
     KV cache as E4M3; exchange sets the partial exchange mode (default: the
     library's); entry names the C call that decodes each layer; scale is the
-    context's softmax scale (0: 1/sqrt(head_dim))."""
+    context's softmax scale (0: 1/sqrt(head_dim)); step_split sets the work
+    split of step launches (default: the library's)."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
@@ -41,6 +43,8 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
     ctx = context_for(cfg, stream=stream, split_tokens=split, probe_tokens=reuse, kv_fp8=kv_fp8, scale=scale)
     if exchange is not None:
         ctx.set_exchange(exchange)
+    if step_split is not None:
+        ctx.set_step_split(step_split)
     keep = []
     for p in range(cfg.num_prompts):
         for layer in range(cfg.layers):

@@ -389,6 +389,23 @@ def test_exchange_mode_on_dry_run():
     ctx.destroy()
 
 
+def test_step_split_mode_on_dry_run():
+    # The step launch's work split: 0 or 1, not changed while a step is open.
+    cfg, ctx = _dry()
+    none4 = (None, None, None, None)
+    assert _code(ctx.set_step_split, 2) == infs.E_ARG
+    assert _code(ctx.set_step_split, -1) == infs.E_ARG
+    ctx.set_step_split(0)
+    ctx.set_step_split(1)
+    ctx.prefill_shared(0, 0, 32, None, None)
+    ctx.refill_slot(0, 0, 3)
+    ctx.decode_step(0, *none4)
+    assert _code(ctx.set_step_split, 0) == infs.E_STATE
+    ctx.end_step()
+    ctx.set_step_split(0)
+    ctx.destroy()
+
+
 def test_static_entry_point_workspace_limit():
     # infs_decode_step_static keeps the split-K workspace and counters in a
     # static array of INFS_STATIC_SCRATCH_BYTES: the benchmark and long-tail

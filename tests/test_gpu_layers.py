@@ -3,9 +3,12 @@
 Each case decodes a whole group with one launch per running step and checks,
 against the float64 oracle: the step log and the device token counters bit
 for bit, every captured output within the tolerance (1e-2 bf16, 1e-5 fp32),
-idle rows exactly 0.  Each case is also decoded with one launch per layer
-(infs_decode_step): the two differ only in the order in which a merge folds
-the split-K partials, so their outputs agree to float rounding.
+idle rows exactly 0.  The default work split cuts responses into near-equal
+pieces; each case is decoded again with the per-layer launch's chunks
+(infs_set_step_split(ctx, 0)), checked against the oracle too, and with one
+launch per layer (infs_decode_step): those two differ only in the order in
+which a merge folds the split-K partials, so their outputs agree to float
+rounding.
 """
 
 import numpy as np
@@ -33,13 +36,19 @@ def _layers_case(cfg, policy, split=128, every=2, layers=None, kv_fp8=False, win
                                     scale=scale if scale > 0 else None)
     diff = 0.0
     if against_layer_path:
+        _, log0, _, chunked, _, _ = run_gpu_group(cfg, policy, wl=wl, split=split, capture=cap, kv_fp8=kv_fp8,
+                                                  window=window, entry=entry, scale=scale, step_split=0)
+        assert log0 == want
+        worst0, _ = check_against_oracle(cfg, wl, want, chunked, layers=layers, kv_fp8=kv_fp8,
+                                         scale=scale if scale > 0 else None)
+        worst = max(worst, worst0)
         _, _, _, per_layer, _, _ = run_gpu_group(cfg, policy, wl=wl, split=split, capture=cap, kv_fp8=kv_fp8,
                                                  window=window, scale=scale)
-        for k in captured:
-            diff = max(diff, float(np.abs(captured[k].astype(np.float64) - per_layer[k]).max()))
-        assert diff <= 1e-5, f"step launch and per-layer launches differ by {diff:.3g}"
-    say(f"  [{cfg.name} {policy} step launch] {steps} steps, {n} outputs vs oracle max err {worst:.3g}; "
-        f"vs per-layer launches {diff:.3g}")
+        for k in chunked:
+            diff = max(diff, float(np.abs(chunked[k].astype(np.float64) - per_layer[k]).max()))
+        assert diff <= 1e-5, f"step launch (per-layer chunks) and per-layer launches differ by {diff:.3g}"
+    say(f"  [{cfg.name} {policy} step launch] {steps} steps, {n} outputs vs oracle max err {worst:.3g} "
+        f"(both work splits); per-layer chunks vs per-layer launches {diff:.3g}")
 
 
 _BF16_SMALL = dict(prompt_lens=(700,), samples_per_prompt=24, length_dist=("lognormal", 4.0, 1.0, 1, 300),
