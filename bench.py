@@ -492,10 +492,11 @@ STAGE_BUDGET_BYTES = 160 << 30  # staged per-step inputs beyond this are cycled 
 
 
 ENTRIES = {"step": "decode_step_layers", "layer": "decode_step"}
+PROBE_ENTRIES = {"step": "probe_step_layers", "layer": "probe_step"}
 
 
 class Bench:
-    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False, entry="step", overrides=None):
+    def __init__(self, cfg_name, split=0, reuse=0, kv_fp8=False, entry="step", overrides=None, probe_entry="layer"):
         import numpy as np
         import torch
 
@@ -506,6 +507,7 @@ class Bench:
 
         self.np, self.torch = np, torch
         self.entry = ENTRIES[entry]
+        self.probe_entry = PROBE_ENTRIES[probe_entry]
         infs.load()
         cfg = get_config(cfg_name, **(overrides or {}))
         self.cfg = cfg
@@ -570,7 +572,7 @@ class Bench:
         from paper_2506_22950_amd.group import probe_group
 
         if self.reuse:
-            probe_group(self.ctx, self.wl.L, self.reuse, self.cfg.layers, self.provide_probe)
+            probe_group(self.ctx, self.wl.L, self.reuse, self.cfg.layers, self.provide_probe, entry=self.probe_entry)
 
     def decode(self):
         from paper_2506_22950_amd.group import decode_group, schedulers_for
@@ -762,6 +764,9 @@ def main():
     ap.add_argument("--exchange", type=int, choices=(0, 1), default=None,
                     help="partial exchange: 0 through the coherence point, 1 through the XCD's L2 "
                          "(default: the library's choice)")
+    ap.add_argument("--probe-entry", choices=tuple(PROBE_ENTRIES), default="layer",
+                    help="probe phase of --reuse: layer = one launch per layer (infs_probe_step, the default: "
+                         "faster for a 64-sample batch), step = one launch per probe step (infs_probe_step_layers)")
     ap.add_argument("--step-split", type=int, choices=(0, 1), default=None,
                     help="work split of step launches: 1 near-equal response pieces (the library's default), "
                          "0 the per-layer launch's chunks")
@@ -816,7 +821,7 @@ def main():
     if args.prompt_len:
         overrides["prompt_lens"] = tuple(int(x) for x in args.prompt_len.split(","))
     b = Bench(args.workload, split=args.split, reuse=args.reuse, kv_fp8=args.kv_fp8, entry=args.entry,
-              overrides=overrides)
+              overrides=overrides, probe_entry=args.probe_entry)
     if args.exchange is not None:
         b.ctx.set_exchange(args.exchange)
     if args.step_split is not None:
@@ -892,8 +897,10 @@ def main():
             pavg = pms * 1000.0 / pn
             pper = palg / pn
             pach = pper / (pavg * 1e-6) / 1e9
-            probe = {"kernel": "decode_kernel (probe launches, %d rows per KV head)" % (b.ctx.probe_batch *
-                                                                                      b.cfg.hpk),
+            rows = b.ctx.probe_batch * b.cfg.hpk
+            probe = {"kernel": ("layers_kernel (probe step launches through every layer, %d rows per KV head)" % rows
+                                if b.probe_entry == "probe_step_layers" else
+                                "decode_kernel (probe launches, one per layer, %d rows per KV head)" % rows),
                      "probe_tokens": args.reuse, "launches": pn, "avg_launch_us": round(pavg, 3),
                      "alg_bytes_per_launch": round(pper), "achieved": round(pach, 1), "unit": "GB/s",
                      "frac": round(pach / PEAK_HBM_GBS, 4), "phase_ms": round(pregion, 2)}

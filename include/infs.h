@@ -202,6 +202,20 @@ infs_status infs_probe_step(infs_ctx* ctx, int32_t layer, int32_t prompt, int32_
                             const uint8_t* live_host, const void* q_dev, const void* k_new_dev,
                             const void* v_new_dev, float* o_dev);
 
+/* Every layer of one probe step in a single launch: the same results as infs_probe_step for layers
+   0 .. num_layers-1 with the same batch, with the layer order, strides (in bytes; 0 = one layer's n
+   rows), bounded waits and residency of infs_decode_step_layers (Section 2.1; Section 4 for the probe
+   phase).  Layer l reads q_dev + l * q_layer_stride ([n, Hq, d]), k_new_dev / v_new_dev + l *
+   kv_layer_stride ([n, Hkv, d]) and writes o_dev + l * o_layer_stride ([n, Hq, d] fp32).  E_STATE: a
+   layer of this probe step was already probed, a decode step is open, the prompt lacks a prefilled
+   layer, or the device cannot hold the launch; E_ARG and E_CAPACITY as infs_probe_step, and for
+   strides below one layer's rows or not multiples of 16.  Close with infs_end_probe_step;
+   infs_get_stats counts the call as one launch. */
+infs_status infs_probe_step_layers(infs_ctx* ctx, int32_t prompt, int32_t first_sample, int32_t n,
+                                   const uint8_t* live_host, const void* q_dev, const void* k_new_dev,
+                                   const void* v_new_dev, float* o_dev, int64_t q_layer_stride,
+                                   int64_t kv_layer_stride, int64_t o_layer_stride);
+
 /* Close the probe step: every live sample's probe length grows by one.  E_STATE unless every layer
    was probed exactly once. */
 infs_status infs_end_probe_step(infs_ctx* ctx);

@@ -68,6 +68,7 @@ struct infs_ctx {
   int32_t* status = nullptr;
   void* scratch = nullptr;  // this device's static scratch array (infs_decode_step_static)
   int layers_resident = 0;  // work-groups of the step-launch kernel resident at once (0: no step launch)
+  int players_resident = 0; // the same for the probe kernel's step launch (0: none)
   // host state
   std::vector<int32_t> plen;                       // per prompt, -1 before its first prefill
   std::vector<std::vector<uint8_t>> prefilled;     // [prompt][layer]
@@ -88,6 +89,7 @@ struct infs_ctx {
   // Merges each prompt's "merged" counter has counted so far (step launches only).
   std::vector<uint32_t> merged_arrivals;
   uint32_t peer_progress = 0;  // peer-line progress value reached by the step launches so far
+  uint32_t probe_merged_arrivals = 0;  // merges counted by probe step launches so far
   bool step_open = false;
   // Probe phase of prefix reuse.
   int step_split = 1;                              // infs_set_step_split: 1 planned pieces, 0 per-layer chunks
@@ -171,16 +173,20 @@ void free_device(infs_ctx* c) {
 // probe launches' own [kMaxSlots][Hkv], then for step launches one "merged"
 // counter per prompt, one layer-done flag per (prompt, KV head) and one peer
 // line per work-group; each on a 128-byte line of its own.
+size_t probe_merged_lines(const infs_ctx* c) { return c->probe_k > 0 ? 1 + (size_t)c->Hkv : 0; }
 size_t counter_lines(const infs_ctx* c) {
-  return (size_t)(c->S + infs::kMaxSlots) * c->Hkv + c->NP + (size_t)c->NP * c->Hkv + (size_t)c->layers_resident;
+  return (size_t)(c->S + infs::kMaxSlots) * c->Hkv + c->NP + (size_t)c->NP * c->Hkv + probe_merged_lines(c) +
+         (size_t)std::max(c->layers_resident, c->players_resident);
 }
 size_t counter_bytes(const infs_ctx* c) { return sizeof(int32_t) * infs::kCounterStride * counter_lines(c); }
 int32_t* merged_counters(const infs_ctx* c) {
   return c->counters + (size_t)(c->S + infs::kMaxSlots) * c->Hkv * infs::kCounterStride;
 }
-int32_t* peer_lines(const infs_ctx* c) {
+// The merged counter and layer flags of probe step launches (one prompt's layout).
+int32_t* probe_merged_counters(const infs_ctx* c) {
   return merged_counters(c) + ((size_t)c->NP + (size_t)c->NP * c->Hkv) * infs::kCounterStride;
 }
+int32_t* peer_lines(const infs_ctx* c) { return probe_merged_counters(c) + probe_merged_lines(c) * infs::kCounterStride; }
 
 // Split-K record capacities.  Records are numbered (prompt, KV head)-major for
 // prefix chunks and (slot, KV head)-major for response chunks, so padding the
@@ -210,6 +216,7 @@ void reset_host(infs_ctx* c) {
   c->slot_arrivals.assign(c->S, 0);
   c->merged_arrivals.assign(c->NP, 0);
   c->peer_progress = 0;
+  c->probe_merged_arrivals = 0;
   c->step_open = false;
   c->probe_len.assign(c->probe_k > 0 ? c->NP : 0, std::vector<int32_t>(c->G, 0));
   c->probe_open = false;
@@ -671,6 +678,14 @@ infs_status infs_create(const infs_config* cfg, void* hip_stream, infs_ctx** out
     }
     // a step launch needs at least one producer and one merge work-group per KV head
     if (c->layers_resident / c->Hkv < 2) c->layers_resident = 0;
+    if (c->probe_k > 0) {
+      const hipError_t pe = infs::layers_resident(c->pkey, &c->players_resident);
+      if (pe != hipSuccess) {
+        delete c;
+        return device_fail(nullptr, pe, "occupancy query of the probe step launch");
+      }
+      if (c->players_resident / c->Hkv < 2) c->players_resident = 0;
+    }
     infs_status st = INFS_OK;
     if (st == INFS_OK) st = alloc((void**)&c->prefix, c->prefix_layer_bytes * c->L, "prefix store");
     if (st == INFS_OK) st = alloc((void**)&c->pool, c->pool_layer_bytes * c->L, "page pool");
@@ -811,6 +826,58 @@ infs_status infs_release_sample(infs_ctx* c, int32_t prompt, int64_t sample_id) 
 
 namespace {
 
+// Roles, counter targets and launch of a step launch through every layer of
+// plan `a` (a decode step or a probe step) with nj work-groups per KV head.
+// slot_arrivals[s] and merged_arrivals[p] are the host's running values of the
+// plan's slot counters and per-prompt merged counters (a.merged); both advance
+// by the launch's layers.
+infs_status launch_step_layers(infs_ctx* c, const KernelKey& key, StepArgs& a, int nj, uint32_t* slot_arrivals,
+                               uint32_t* merged_arrivals) {
+  a.peer = peer_lines(c);
+  a.peer_base = (int32_t)c->peer_progress;
+  // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix chunks
+  // and response pieces so that no producer reads many more tokens than the others.
+  int32_t lens[infs::kMaxSlots], pieces[infs::kMaxSlots];
+  for (int s = 0; s < a.S; ++s) lens[s] = a.slot[s].len;
+  const infs::StepRoles roles =
+      c->step_split ? infs::plan_step_roles(nj, a.S, a.n_prefix_items, c->prefix_split, lens, c->split, c->scmax,
+                                            pieces)
+                    : infs::plan_step_roles_chunks(nj, a.S, a.n_prefix_items, lens, c->split, pieces);
+  if ((a.n_prefix_items > 0 && roles.n_pre < 1) || (roles.n_suffix_items > 0 && roles.n_suf < 1))
+    return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
+                "chunks, response chunks and merges", nj);
+  a.n_merge_wg = roles.n_merge;
+  a.n_pre_wg = roles.n_pre;
+  a.n_suf_wg = roles.n_suf;
+  for (int s = 0, items = 0; s < a.S; ++s) {
+    a.slot[s].pieces = pieces[s];
+    a.slot[s].item_begin = items;
+    items += pieces[s];
+  }
+  a.n_suffix_items = roles.n_suffix_items;
+  a.resp_cut = roles.cut ? 1 : 0;
+  // Merges go opposite the prefix work-groups (index j shares its CU with j + nj/2, see
+  // mate_gate), else after the response work-groups.
+  a.merge_j0 = (nj % 2 == 0 && a.n_pre_wg <= nj / 2 && a.n_merge_wg <= nj / 2) ? nj / 2 : a.n_pre_wg + a.n_suf_wg;
+  // counter targets: each slot counts its producers once per layer, each prompt its merges
+  for (int s = 0; s < a.S; ++s) {
+    a.slot[s].target = (int32_t)slot_arrivals[s];
+    if (a.slot[s].len > 0)
+      slot_arrivals[s] += (uint32_t)c->L * (uint32_t)(a.slot[s].pieces + a.prompt[s / a.m].nchunks);
+  }
+  for (int p = 0; p < a.num_prompts; ++p) {
+    int live = 0;
+    for (int s = p * a.m; s < (p + 1) * a.m; ++s) live += a.slot[s].len > 0;
+    a.merged_base[p] = (int32_t)merged_arrivals[p];
+    a.merged_per_layer[p] = live * c->Hkv;
+    merged_arrivals[p] += (uint32_t)c->L * (uint32_t)(live * c->Hkv);
+  }
+  infs_status st = timed_launch(c, key, a, c->Hkv * (a.n_pre_wg + a.n_suf_wg + a.n_merge_wg), true);
+  if (st != INFS_OK) return st;
+  c->peer_progress += (uint32_t)c->L;
+  return INFS_OK;
+}
+
 // One layer of the open (or opening) step; with `static_ws` the split-K
 // workspace and arrival counters are taken from the static scratch array.
 infs_status decode_layer(infs_ctx* c, int32_t layer, const void* q_dev, const void* k_new_dev, const void* v_new_dev,
@@ -947,49 +1014,9 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     a.prefix_layer_bytes = (int64_t)c->prefix_layer_bytes;
     a.pool_layer_bytes = (int64_t)c->pool_layer_bytes;
     a.merged = merged_counters(c);
-    a.peer = peer_lines(c);
-    a.peer_base = (int32_t)c->peer_progress;
-    // Work-groups per KV head: one merge wavefront per slot, the rest split between prefix chunks
-    // and response pieces so that no producer reads many more tokens than the others.
-    const int nj = c->layers_resident / c->Hkv;
-    int32_t lens[infs::kMaxSlots], pieces[infs::kMaxSlots];
-    for (int s = 0; s < c->S; ++s) lens[s] = a.slot[s].len;
-    const infs::StepRoles roles =
-        c->step_split ? infs::plan_step_roles(nj, c->S, a.n_prefix_items, c->prefix_split, lens, c->split, c->scmax,
-                                              pieces)
-                      : infs::plan_step_roles_chunks(nj, c->S, a.n_prefix_items, lens, c->split, pieces);
-    if ((a.n_prefix_items > 0 && roles.n_pre < 1) || (roles.n_suffix_items > 0 && roles.n_suf < 1))
-      return fail(c, INFS_E_STATE, "no step launch on this device: %d work-groups per KV head cannot take prefix "
-                  "chunks, response chunks and merges", nj);
-    a.n_merge_wg = roles.n_merge;
-    a.n_pre_wg = roles.n_pre;
-    a.n_suf_wg = roles.n_suf;
-    for (int s = 0, items = 0; s < c->S; ++s) {
-      a.slot[s].pieces = pieces[s];
-      a.slot[s].item_begin = items;
-      items += pieces[s];
-    }
-    a.n_suffix_items = roles.n_suffix_items;
-    a.resp_cut = roles.cut ? 1 : 0;
-    // Merges go opposite the prefix work-groups (index j shares its CU with j + nj/2, see
-    // mate_gate), else after the response work-groups.
-    a.merge_j0 = (nj % 2 == 0 && a.n_pre_wg <= nj / 2 && a.n_merge_wg <= nj / 2) ? nj / 2 : a.n_pre_wg + a.n_suf_wg;
-    // counter targets: each slot counts its producers once per layer, each prompt its merges
-    for (int s = 0; s < c->S; ++s) {
-      a.slot[s].target = (int32_t)c->slot_arrivals[s];
-      if (a.slot[s].len > 0)
-        c->slot_arrivals[s] += (uint32_t)c->L * (uint32_t)(a.slot[s].pieces + a.prompt[s / c->m].nchunks);
-    }
-    for (int p = 0; p < c->NP; ++p) {
-      int live = 0;
-      for (int s = p * c->m; s < (p + 1) * c->m; ++s) live += a.slot[s].len > 0;
-      a.merged_base[p] = (int32_t)c->merged_arrivals[p];
-      a.merged_per_layer[p] = live * c->Hkv;
-      c->merged_arrivals[p] += (uint32_t)c->L * (uint32_t)(live * c->Hkv);
-    }
-    infs_status st = timed_launch(c, c->key, a, c->Hkv * (a.n_pre_wg + a.n_suf_wg + a.n_merge_wg), true);
+    infs_status st = launch_step_layers(c, c->key, a, c->layers_resident / c->Hkv, c->slot_arrivals.data(),
+                                        c->merged_arrivals.data());
     if (st != INFS_OK) return st;
-    c->peer_progress += (uint32_t)c->L;
   }
   std::fill(c->layer_done.begin(), c->layer_done.end(), 1);
   c->layers_done = c->L;
@@ -1070,6 +1097,77 @@ infs_status infs_probe_step(infs_ctx* c, int32_t layer, int32_t prompt, int32_t 
   ++c->stats.launches;
   c->stats.alg_bytes += c->pstep_bytes;
   c->stats.alg_flops += c->pstep_flops;
+  return INFS_OK;
+}
+
+infs_status infs_probe_step_layers(infs_ctx* c, int32_t prompt, int32_t first_sample, int32_t n,
+                                   const uint8_t* live_host, const void* q_dev, const void* k_new_dev,
+                                   const void* v_new_dev, float* o_dev, int64_t q_layer_stride,
+                                   int64_t kv_layer_stride, int64_t o_layer_stride) {
+  CHECK_CTX(c);
+  if (c->probe_k == 0) return fail(c, INFS_E_STATE, "probe_step_layers needs a context with probe_tokens > 0");
+  if (prompt < 0 || prompt >= c->NP) return fail(c, INFS_E_ARG, "prompt %d out of range [0, %d)", prompt, c->NP);
+  if (n < 1 || n > c->probe_batch) return fail(c, INFS_E_ARG, "n=%d out of range [1, %d]", n, c->probe_batch);
+  if (first_sample < 0 || first_sample > c->G - n)
+    return fail(c, INFS_E_ARG, "samples %d..%d out of range [0, %d)", first_sample, first_sample + n - 1, c->G);
+  const int64_t q_bytes = (int64_t)n * c->Hq * c->D * (int64_t)c->es;
+  const int64_t kv_bytes = (int64_t)n * c->Hkv * c->D * (int64_t)c->es;
+  const int64_t o_bytes = (int64_t)n * c->Hq * c->D * (int64_t)sizeof(float);
+  if (q_layer_stride == 0) q_layer_stride = q_bytes;
+  if (kv_layer_stride == 0) kv_layer_stride = kv_bytes;
+  if (o_layer_stride == 0) o_layer_stride = o_bytes;
+  if (q_layer_stride < q_bytes || kv_layer_stride < kv_bytes || o_layer_stride < o_bytes)
+    return fail(c, INFS_E_ARG, "layer strides must be 0 or at least one layer's rows (%lld, %lld, %lld bytes)",
+                (long long)q_bytes, (long long)kv_bytes, (long long)o_bytes);
+  if ((q_layer_stride | kv_layer_stride | o_layer_stride) & 15)
+    return fail(c, INFS_E_ARG, "layer strides must be multiples of 16 bytes");
+  if (!c->dry && (!q_dev || !k_new_dev || !v_new_dev || !o_dev)) return fail(c, INFS_E_ARG, "null buffer");
+  if (!c->dry && (((uintptr_t)q_dev | (uintptr_t)k_new_dev | (uintptr_t)v_new_dev | (uintptr_t)o_dev) & 15))
+    return fail(c, INFS_E_ARG, "q, k_new, v_new and o must be 16-byte aligned");
+  if (c->step_open) return fail(c, INFS_E_STATE, "probe_step_layers while a decode step is open");
+  if (c->probe_open)
+    return fail(c, INFS_E_STATE, "probe_step_layers needs a probe step with no layer probed yet (%d probed)",
+                c->probe_layers_done);
+  if (!c->dry && c->players_resident == 0)
+    return fail(c, INFS_E_STATE, "no probe step launch on this device: too few work-groups resident per KV head");
+  uint8_t live[infs::kMaxSlots];
+  bool any = false;
+  for (int j = 0; j < n; ++j) {
+    live[j] = live_host ? (live_host[j] != 0) : 1;
+    any |= live[j] != 0;
+  }
+  for (int layer = 0; any && layer < c->L; ++layer)
+    if (!c->prefilled[prompt][layer])
+      return fail(c, INFS_E_STATE, "prompt %d has no prefix for layer %d", prompt, layer);
+  infs_status st = open_probe(c, prompt, first_sample, n, live);
+  if (st != INFS_OK) return st;
+  if (!c->dry) {
+    StepArgs& a = c->pplan;
+    a.q = q_dev;
+    a.knew = k_new_dev;
+    a.vnew = v_new_dev;
+    a.o = o_dev;
+    a.prefix = c->prefix + (size_t)prompt * c->Hkv * infs::prefix_elems_per_head(c->key, c->pmax_pad) * c->kv_es;
+    a.pool = c->pool;
+    a.tokens = c->tokens + (size_t)prompt * c->G;
+    a.counters = c->counters + (size_t)c->S * c->Hkv * infs::kCounterStride;
+    a.count_tokens = 1;
+    a.num_layers = c->L;
+    a.q_layer_stride = q_layer_stride;
+    a.kv_layer_stride = kv_layer_stride;
+    a.o_layer_stride = o_layer_stride;
+    a.prefix_layer_bytes = (int64_t)c->prefix_layer_bytes;
+    a.pool_layer_bytes = (int64_t)c->pool_layer_bytes;
+    a.merged = probe_merged_counters(c);
+    st = launch_step_layers(c, c->pkey, a, c->players_resident / c->Hkv, c->probe_slot_arrivals.data(),
+                            &c->probe_merged_arrivals);
+    if (st != INFS_OK) return st;
+  }
+  std::fill(c->probe_layer_done.begin(), c->probe_layer_done.end(), 1);
+  c->probe_layers_done = c->L;
+  ++c->stats.launches;
+  c->stats.alg_bytes += c->pstep_bytes * c->L;
+  c->stats.alg_flops += c->pstep_flops * c->L;
   return INFS_OK;
 }
 

@@ -38,7 +38,7 @@ def schedulers_for(cfg, policy: str, pred=None) -> List[infs.Sched]:
 
 
 def probe_group(ctx: infs.Context, lengths, k: int, num_layers: int, provide: Callable,
-                log: Optional[list] = None, after_step: Optional[Callable] = None) -> int:
+                log: Optional[list] = None, after_step: Optional[Callable] = None, entry: str = "probe_step") -> int:
     """Probe phase of prefix reuse (Section 4): every sample decodes its first
     min(L_i, k) tokens against the shared prompt, in batches of up to
     ctx.probe_batch samples of one prompt; samples that finish within their
@@ -49,6 +49,9 @@ def probe_group(ctx: infs.Context, lengths, k: int, num_layers: int, provide: Ca
     log, if given, receives one row per probe step: per batch position
     (prompt, sample, t) with t the probe length after this step, or None.
     after_step(step) is called after each end_probe_step.
+    entry: "probe_step" (one launch per layer) or "probe_step_layers" (every
+    layer of a probe step in one launch; the layer strides are read off the
+    pointers provide returns for layers 0 and 1).
     """
     nb = ctx.probe_batch
     steps = 0
@@ -60,8 +63,18 @@ def probe_group(ctx: infs.Context, lengths, k: int, num_layers: int, provide: Ca
                 live = [int(row[first + j]) >= t for j in range(n)]
                 if not any(live):
                     continue
-                for layer in range(num_layers):
-                    ctx.probe_step(layer, p, first, n, live, *provide(steps, p, first, n, layer))
+                if entry == "probe_step_layers":
+                    b0 = provide(steps, p, first, n, 0)
+                    strides = [0, 0, 0]
+                    if num_layers > 1 and b0[0] is not None:  # dry-run contexts take no buffers
+                        b1 = provide(steps, p, first, n, 1)
+                        strides = [b1[0] - b0[0], b1[1] - b0[1], b1[3] - b0[3]]
+                        if b1[2] - b0[2] != strides[1]:
+                            raise ValueError("k_new and v_new need the same layer stride")
+                    ctx.probe_step_layers(p, first, n, live, *b0, *strides)
+                else:
+                    for layer in range(num_layers):
+                        ctx.probe_step(layer, p, first, n, live, *provide(steps, p, first, n, layer))
                 ctx.end_probe_step()
                 if after_step is not None:
                     after_step(steps)

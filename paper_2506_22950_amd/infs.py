@@ -39,7 +39,7 @@ EXPORTS = (
     "infs_probe_state", "infs_release_sample", "infs_read_prefix", "infs_read_response", "infs_set_merge_wait",
     "infs_get_kernel_info", "infs_set_exchange", "infs_exchange_mode", "infs_decode_step_static",
     "infs_sched_optimum", "infs_decode_step_layers", "infs_step_launch_workgroups", "infs_set_step_split",
-    "infs_step_split_plan",
+    "infs_step_split_plan", "infs_probe_step_layers",
 )
 
 
@@ -119,6 +119,8 @@ def load():
         "infs_sched_optimum": (I32, [I32, I32, ctypes.POINTER(I32), I64, ctypes.POINTER(I64), ctypes.POINTER(I64),
                                      ctypes.POINTER(I32)]),
         "infs_probe_step": (I32, [P, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_uint8), P, P, P, P]),
+        "infs_probe_step_layers": (I32, [P, I32, I32, I32, ctypes.POINTER(ctypes.c_uint8), P, P, P, P, I64, I64,
+                                         I64]),
         "infs_end_probe_step": (I32, [P]),
         "infs_probe_batch": (I32, [P]),
         "infs_probe_state": (I32, [P, I32, I64, ctypes.POINTER(I32)]),
@@ -245,6 +247,15 @@ class Context:
             buf = (ctypes.c_uint8 * n)(*[1 if x else 0 for x in live])
         self._call(load().infs_probe_step, layer, prompt, first_sample, n, buf, _ptr(q), _ptr(k_new), _ptr(v_new),
                    _ptr(o))
+
+    def probe_step_layers(self, prompt, first_sample, n, live, q, k_new, v_new, o, q_layer_stride=0,
+                          kv_layer_stride=0, o_layer_stride=0):
+        """Every layer of one probe step in one launch; strides in bytes (0: n rows)."""
+        buf = None
+        if live is not None:
+            buf = (ctypes.c_uint8 * n)(*[1 if x else 0 for x in live])
+        self._call(load().infs_probe_step_layers, prompt, first_sample, n, buf, _ptr(q), _ptr(k_new), _ptr(v_new),
+                   _ptr(o), q_layer_stride, kv_layer_stride, o_layer_stride)
 
     def end_probe_step(self):
         self._call(load().infs_end_probe_step)

@@ -23,7 +23,7 @@ def say(*a):
 
 def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, wl=None, stop_after=None, reuse=0,
                   probe=None, inspect=None, kv_fp8=False, exchange=None, entry="decode_step", scale=0.0,
-                  step_split=None):
+                  step_split=None, probe_entry="probe_step"):
     """Group decode through the C ABI.  reuse = k runs the probe phase of prefix
     reuse first; if `probe` is a dict it receives 'log' (probe step log) and
     'captured' (the O buffer [L, batch, Hq, d] after every probe step).
@@ -31,7 +31,8 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
     KV cache as E4M3; exchange sets the partial exchange mode (default: the
     library's); entry names the C call that decodes each layer; scale is the
     context's softmax scale (0: 1/sqrt(head_dim)); step_split sets the work
-    split of step launches (default: the library's)."""
+    split of step launches (default: the library's); probe_entry is the C call
+    of the probe phase (infs_probe_step per layer, or infs_probe_step_layers)."""
     import torch
 
     assert torch.cuda.is_available(), "GPU test needs a GPU"
@@ -91,7 +92,7 @@ def run_gpu_group(cfg, policy, capture=lambda step: True, split=0, window=1024, 
         def pafter(j):
             pcap[j] = po.cpu().numpy()
 
-        nprobe = probe_group(ctx, wl.L, reuse, L, pprovide, after_step=pafter)
+        nprobe = probe_group(ctx, wl.L, reuse, L, pprovide, after_step=pafter, entry=probe_entry)
         assert nprobe == len(plog)
         if probe is not None:
             probe["log"], probe["captured"] = plog, pcap

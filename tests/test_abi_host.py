@@ -353,6 +353,44 @@ def test_probe_state_machine_errors():
 
 
 
+def test_probe_step_launch_state_machine():
+    # infs_probe_step_layers on a dry-run context: the whole probe step in one call, the same
+    # bookkeeping as one infs_probe_step per layer, and its own argument and state errors.
+    cfg = get_config("tiny_f32").with_(layers=3, samples_per_prompt=6, slots_per_prompt=2, max_suffix_len=16)
+    nothing = (None, None, None, None)
+    a = context_for(cfg, dry_run=True, probe_tokens=2)
+    b = context_for(cfg, dry_run=True, probe_tokens=2)
+    assert _code(a.probe_step_layers, 0, 0, 6, None, *nothing) == infs.E_STATE    # prompt not prefilled
+    for ctx in (a, b):
+        for layer in range(cfg.layers):
+            ctx.prefill_shared(0, layer, cfg.prompt_lens[0], None, None)
+    live = [1, 0, 1, 1, 1, 1]
+    a.probe_step_layers(0, 0, 6, live, *nothing)
+    for layer in range(cfg.layers):
+        b.probe_step(layer, 0, 0, 6, live, *nothing)
+    assert _code(a.probe_step_layers, 0, 0, 6, live, *nothing) == infs.E_STATE   # the step is probed
+    assert _code(a.probe_step, 0, 0, 0, 6, live, *nothing) == infs.E_STATE
+    a.end_probe_step()
+    b.end_probe_step()
+    assert [a.probe_state(0, i) for i in range(6)] == [b.probe_state(0, i) for i in range(6)] == live
+    assert _code(a.probe_step_layers, 0, 0, 7, None, *nothing) == infs.E_ARG      # batch too large
+    assert _code(a.probe_step_layers, 1, 0, 1, None, *nothing) == infs.E_ARG      # no prompt 1
+    assert _code(a.probe_step_layers, 0, 0, 6, None, *nothing, 8, 0, 0) == infs.E_ARG  # stride below a layer
+    a.probe_step(0, 0, 0, 6, None, *nothing)                                     # per-layer step open
+    assert _code(a.probe_step_layers, 0, 0, 6, None, *nothing) == infs.E_STATE
+    for layer in range(1, cfg.layers):
+        a.probe_step(layer, 0, 0, 6, None, *nothing)
+    a.end_probe_step()
+    assert _code(a.probe_step_layers, 0, 0, 1, None, *nothing) == infs.E_CAPACITY  # sample 0 has its k tokens
+    sa, sb = a.get_stats(), b.get_stats()
+    assert (sa.launches, sb.launches) == (1 + cfg.layers, cfg.layers)  # a: one step launch, then per layer
+    assert sa.tokens == sb.tokens + 6 and sa.alg_bytes > sb.alg_bytes
+    plain = context_for(cfg, dry_run=True)
+    assert _code(plain.probe_step_layers, 0, 0, 1, None, *nothing) == infs.E_STATE
+    for ctx in (a, b, plain):
+        ctx.destroy()
+
+
 def test_fp8_kv_validation():
     # The FP8 cache needs bf16, head_dim 128 and the MFMA prefix path.
     for name, over in (("tiny_f32", {}),                                           # fp32

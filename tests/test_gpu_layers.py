@@ -212,3 +212,51 @@ def test_step_launch_exchange_placement_check():
         ctx.sync()
     assert ei.value.status == infs.E_DEVICE
     ctx.destroy()
+
+
+def _probe_case(cfg, policy, k, split=128):
+    # The probe phase with one launch per probe step (infs_probe_step_layers) against the
+    # oracle, and against one launch per layer: with the per-layer chunks the two differ only
+    # in the order the merges add partials.
+    wl = Workload(cfg)
+    want = oracle_log(cfg, wl, policy, reuse=k)
+    runs = {}
+    for entry, step_split in (("probe_step_layers", None), ("probe_step_layers", 0), ("probe_step", None)):
+        probe = {}
+        _, log, steps, _, tokens, stats = run_gpu_group(cfg, policy, wl=wl, split=split, reuse=k, probe=probe,
+                                                        capture=lambda j: False, probe_entry=entry,
+                                                        step_split=step_split)
+        assert log == want and steps == len(want)
+        assert np.array_equal(tokens, wl.L), "device token counters (probe + decode) differ from the lengths"
+        runs[(entry, step_split)] = probe
+    worst = 0.0
+    for key in (("probe_step_layers", None), ("probe_step_layers", 0)):
+        w, n = check_against_oracle(cfg, wl, runs[key]["log"], runs[key]["captured"])
+        worst = max(worst, w)
+    a, b = runs[("probe_step_layers", 0)]["captured"], runs[("probe_step", None)]["captured"]
+    assert a.keys() == b.keys()
+    diff = max(float(np.abs(a[j].astype(np.float64) - b[j]).max()) for j in a)
+    assert diff <= 1e-5, f"probe step launch and per-layer probe launches differ by {diff:.3g}"
+    say(f"  [{cfg.name} probe step launch k={k}] {len(runs[('probe_step', None)]['log'])} probe steps, "
+        f"{n} outputs vs oracle max err {worst:.3g}; vs per-layer probe launches {diff:.3g}")
+
+
+def test_probe_step_launch_bf16_128_row_tiles():
+    # 40 samples x hpk 2 = 80 rows per KV head on 128-row MFMA tiles, three layers.
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=3, prompt_lens=(300,), samples_per_prompt=40,
+                                             slots_per_prompt=8, length_dist=("lognormal", 3.5, 1.0, 1, 200),
+                                             max_suffix_len=200, pool_rows=None)
+    _probe_case(cfg, "sjf", 16)
+
+
+def test_probe_step_launch_hpk4_two_prompts():
+    # 32Q/8KV: batches of 32 samples = 128 rows per KV head; two prompts, each probed in turn.
+    cfg = get_config("qwen3_8b_4prompts").with_(layers=2, prompt_lens=(200, 450), samples_per_prompt=36,
+                                                length_dist=("lognormal", 3.5, 1.0, 1, 160), max_suffix_len=160,
+                                                pool_rows=None)
+    _probe_case(cfg, "fptas_sjf", 8)
+
+
+def test_probe_step_launch_f32_wave():
+    # fp32 wavefront path: batches of 8 samples (16 rows), three layers.
+    _probe_case(get_config("tiny_f32").with_(layers=3), "fifo", 5, split=0)
