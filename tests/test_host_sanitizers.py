@@ -3,8 +3,9 @@
 runtime.cpp and sched.cpp are rebuilt with host-only sanitizers
 (build.build_sanitized: every -fsanitize= applies to host code only) and the
 host-side suites -- the C ABI from Python (test_abi_host.py), the dry-run
-state machine (test_state_machine.py) and the plain C consumer
-(test_c_consumer.py) -- run again against that build in a child process with
+state machine (test_state_machine.py), the plain C consumer
+(test_c_consumer.py) and the step-launch plan through the ABI
+(test_step_plan.py) -- run again against that build in a child process with
 the sanitizer runtime preloaded.  Any report (an out-of-bounds access, a use
 after free, undefined behaviour) fails the run.  No GPU is used: these suites
 run dry-run contexts.  Leak checking is off: the Python interpreter keeps its
@@ -19,7 +20,8 @@ import pytest
 pytestmark = pytest.mark.sanitize
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SUITES = ["tests/test_abi_host.py", "tests/test_state_machine.py", "tests/test_c_consumer.py"]
+SUITES = ["tests/test_abi_host.py", "tests/test_state_machine.py", "tests/test_c_consumer.py",
+          "tests/test_step_plan.py::test_step_split_plan_hand_cases"]
 
 
 def test_host_runtime_under_asan_and_ubsan():

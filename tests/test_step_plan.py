@@ -16,14 +16,20 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(os.path.dirname(HERE), "paper_2506_22950_amd", "csrc")
 
 
-def test_step_plan_host_check(tmp_path):
+@pytest.mark.parametrize("sanitize", [False, True], ids=["plain", "asan_ubsan"])
+def test_step_plan_host_check(tmp_path, sanitize):
+    # Also built with AddressSanitizer and UndefinedBehaviorSanitizer (g++, host code only):
+    # any out-of-bounds access or undefined behaviour in the planner fails the run.
     if shutil.which("g++") is None:
         pytest.skip("g++ not available")
     exe = str(tmp_path / "step_plan_check")
-    r = subprocess.run(["g++", "-std=c++17", "-O2", "-Wall", "-Wextra", "-Werror", "-I" + CSRC,
+    flags = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=all"] if sanitize else ["-O2"]
+    r = subprocess.run(["g++", "-std=c++17", *flags, "-Wall", "-Wextra", "-Werror", "-I" + CSRC,
                         os.path.join(HERE, "step_plan_check.cpp"), "-o", exe], capture_output=True, text=True)
+    if sanitize and r.returncode != 0 and "asan" in r.stderr.lower():
+        pytest.skip("g++ sanitizer runtime not available")
     assert r.returncode == 0, r.stderr
-    r = subprocess.run([exe, "20000"], capture_output=True, text=True, timeout=120)
+    r = subprocess.run([exe, "20000"], capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "failures 0" in r.stdout
 
