@@ -33,7 +33,8 @@ SIMDS = 1024  # 256 compute units x 4 SIMDs
 XCDS = 8
 MFMA_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE")
 KERNEL_SOURCES = tuple("paper_2506_22950_amd/csrc/" + f for f in (
-    "decode.h", "layers.h", "kernels.h", "plan.h", "kernels.hip", "inst_wave_f32_d64.hip", "inst_wave_f32_d128.hip",
+    "decode.h", "layers.h", "step_plan.h", "kernels.h", "plan.h", "kernels.hip", "inst_wave_f32_d64.hip",
+    "inst_wave_f32_d128.hip",
     "inst_wave_bf16_d64.hip", "inst_wave_bf16_d128.hip", "inst_mfma_d64.hip", "inst_mfma_d128a.hip",
     "inst_mfma_d128b.hip", "inst_kv8a.hip", "inst_kv8b.hip"))
 METRIC = "generated tokens/sec per group decode + achieved HBM TB/s vs peak, 1 MI355X"

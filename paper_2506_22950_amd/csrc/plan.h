@@ -39,7 +39,7 @@ constexpr size_t kStaticScratchBytes = size_t(16) << 20;
 
 struct SlotPlan {
   int32_t len;         // response length after this step's append; 0 = idle
-  int32_t item_begin;  // first response-chunk item of this slot
+  int32_t item_begin;  // first response item of this slot
   int32_t cur_page;    // page holding position len-1 (where this step's K/V go)
   int32_t sample;      // sample id (token counters)
   int32_t target;      // slot counter value once this launch's producers for the slot (its response

@@ -1209,7 +1209,7 @@ infs_status infs_set_exchange(infs_ctx* c, int32_t mode) {
 infs_status infs_step_split_plan(int32_t nj, int32_t S, int32_t n_prefix_items, int32_t prefix_split,
                                  const int32_t* len, int32_t split, int32_t scmax, int32_t mode, int32_t* pieces,
                                  int32_t* roles) {
-  if (nj < 2 || S < 1 || S > infs::kMaxSlots || n_prefix_items < 0 || prefix_split < 1 || split < infs::kWaves ||
+  if (nj < 2 || S < 1 || S > infs::kMaxSlots || n_prefix_items < 0 || prefix_split < 1 || split < infs::kPageTokens ||
       split > infs::kMaxSplit || split % infs::kPageTokens || scmax < 1 || mode < 0 || mode > 1)
     return fail(nullptr, INFS_E_ARG, "step_split_plan: nj >= 2, S in [1, %d], split a page multiple up to %d, "
                 "scmax >= 1 and mode 0 or 1", infs::kMaxSlots, infs::kMaxSplit);

@@ -39,9 +39,8 @@ constexpr int piece_wave_pages(int piece_pages) { return (piece_pages + kWaves -
 
 struct StepRoles {
   int n_pre, n_suf, n_merge;  // work-groups per KV head taking prefix chunks, response pieces, merges
-  int n_suffix_items;         // response pieces of the step (sum of pieces[])
-  int max_tokens;             // planned largest token count of one producer (prefix or response)
-  bool cut;                   // pieces chosen by the plan (else the per-layer launch's chunks)
+  int n_suffix_items;         // response items of the step (sum of pieces[])
+  bool cut;                   // near-equal pieces chosen by the plan (else the per-layer launch's chunks)
 };
 
 namespace step_plan_detail {
@@ -124,18 +123,17 @@ inline StepRoles plan_step_roles_chunks(int nj, int S, int n_prefix_items, const
 // While the per-layer chunks leave every response work-group at most one
 // chunk, they are kept: all of a producer's tokens are then in registers when
 // its layer starts, and cutting finer only spreads the same bytes over more
-// work-groups and partials (which measured slower).  Otherwise the responses
-// are cut into pieces, at most one per response work-group, and the number of
-// prefix work-groups k-fold loaded (k = 1, 2, ...) is chosen to minimise the
-// largest per-producer token count, prefix tokens counted twice: every slot's
-// merge waits for all prefix chunks, so a prefix work-group's second chunk
-// delays the whole layer.  When the live slots outnumber the response
-// work-groups the chunks stay, dealt round robin.
+// work-groups and partials (which measured slower).  Otherwise the number of
+// prefix work-groups is chosen among the fewest that take k chunks each
+// (k = 1, 2, ...) to minimise the largest per-producer token count, prefix
+// tokens counted twice (every slot's merge waits for all prefix chunks, so a
+// prefix work-group's second chunk delays the whole layer), and the responses
+// are cut into pieces, at most one per remaining work-group; when the live
+// slots outnumber those work-groups the chunks stay, dealt round robin.
 inline StepRoles plan_step_roles(int nj, int S, int n_prefix_items, int prefix_split, const int32_t* len, int split,
                                  int scmax, int32_t* pieces) {
   using namespace step_plan_detail;
   StepRoles r = plan_step_roles_chunks(nj, S, n_prefix_items, len, split, pieces);
-  r.max_tokens = r.n_suf > 0 ? cdiv(r.n_suffix_items, r.n_suf) * split : 0;
   if (r.n_suffix_items <= r.n_suf) return r;
   const int prod = nj - r.n_merge, chunks = r.n_suffix_items;
   int best = -1, best_pre = r.n_pre;
@@ -166,7 +164,6 @@ inline StepRoles plan_step_roles(int nj, int S, int n_prefix_items, int prefix_s
     for (int s = 0; s < S; ++s) pieces[s] = len[s] > 0 ? cdiv(len[s], split) : 0;
   r.n_suffix_items = 0;
   for (int s = 0; s < S; ++s) r.n_suffix_items += pieces[s];
-  r.max_tokens = r.cut ? big * kPageTokens : cdiv(r.n_suffix_items, r.n_suf) * split;
   return r;
 }
 
