@@ -10,7 +10,8 @@
  *   - a fixed pool holds the response KV of the m live slots; every running
  *     step decodes one token for each live slot, through every layer
  *     (Section 2.1; Section 5.1, definition of a running step)
- *                                                          -> infs_decode_step, infs_end_step
+ *                                                          -> infs_decode_step, infs_decode_step_layers,
+ *                                                             infs_end_step
  *   - a finished sample releases its slot and buffer, and the slot is refilled
  *     at once with a pending sample that starts at the next step
  *     (Section 3.2; Algorithm 1, phase 2)                  -> infs_retire_slot, infs_refill_slot
@@ -20,8 +21,8 @@
  *     (Algorithm 1), longest-first                          -> infs_sched_*, infs_fptas_assign
  *   - prefix reuse: every sample first decodes k probe tokens, whose KV is
  *     kept; a dispatched sample resumes at token k+1 (Section 4)
- *                                                          -> infs_probe_step, infs_end_probe_step,
- *                                                             infs_release_sample
+ *                                                          -> infs_probe_step, infs_probe_step_layers,
+ *                                                             infs_end_probe_step, infs_release_sample
  *   - optionally an FP8 (E4M3) KV cache, in the direction of the KV-cache
  *     compression the paper leaves as future work           -> INFS_FLAG_KV_FP8
  *
@@ -331,10 +332,12 @@ infs_status infs_set_merge_wait(infs_ctx* ctx, int32_t max_polls);
 infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
 
 /* How an infs_decode_step_layers launch divides a step's work among its producer work-groups.
-   mode 1 (default): each live response is cut into near-equal page ranges, at most one per response
-           work-group when the live slots allow, and the number of prefix work-groups is chosen with
-           the cuts so that the most tokens any one work-group reads is as small as it can be (a layer
-           waits for the work-group that reads the most after its queries arrive).
+   mode 1 (default): the chunks of mode 0 while every response work-group takes at most one;
+           otherwise each live response is cut into near-equal page ranges (at most one per response
+           work-group when the live slots allow) and the number of prefix work-groups is chosen with
+           the cuts, so that the most tokens one work-group reads after its layer's queries arrive is
+           as small as it can be (a work-group holds one round of 256 tokens in registers before
+           then).
    mode 0: responses in chunks of split_tokens and work-groups divided in proportion to the chunk
            counts, the partition of infs_decode_step: outputs then differ from a per-layer decode only
            in the order the merges add partials.
