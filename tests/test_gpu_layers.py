@@ -260,3 +260,54 @@ def test_probe_step_launch_hpk4_two_prompts():
 def test_probe_step_launch_f32_wave():
     # fp32 wavefront path: batches of 8 samples (16 rows), three layers.
     _probe_case(get_config("tiny_f32").with_(layers=3), "fifo", 5, split=0)
+
+
+def _count_cut_steps(cfg, log, nj, split, mfma):
+    # Steps whose work split cuts the responses into near-equal pieces (the library's own plan).
+    split = split or 256
+    psplit = 128 if mfma else split
+    scmax = -(-cfg.max_suffix_len // split)
+    chunks = [-(-plen // psplit) for plen in cfg.prompt_lens]
+    cut = 0
+    for row in log:
+        lens = [e[2] if e is not None else 0 for e in row]
+        npi = sum(chunks[p] for p in {e[0] for e in row if e is not None})
+        roles, _ = infs.step_split_plan(nj, lens, npi, psplit, split, scmax)
+        cut += roles["cut"]
+    return cut
+
+
+@pytest.mark.parametrize("name", ["bf16_mfma", "f32_wave"])
+def test_step_launch_cut_pieces_multi_round(name):
+    # Long responses on few slots: the per-layer chunks outnumber the response work-groups, so
+    # the step launch cuts the responses into pieces of several load rounds per wavefront
+    # (MFMA tiles, and the fp32 wavefront path); checked against the oracle, and the test
+    # asserts that the cut path ran.
+    if name == "bf16_mfma":
+        cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(256,), samples_per_prompt=16,
+                                                 slots_per_prompt=16, length_dist=("uniform", 900, 1400),
+                                                 max_suffix_len=1400, pool_rows=None)
+        split, every = 0, 37
+    else:
+        cfg = get_config("tiny_f32").with_(layers=2, num_q_heads=16, num_kv_heads=8, samples_per_prompt=12,
+                                           slots_per_prompt=8, length_dist=("uniform", 1500, 2000),
+                                           max_suffix_len=2000)
+        split, every = 128, 61
+    seen = {}
+
+    def grab(ctx, step, log):
+        if not seen:
+            seen["nj"] = ctx.step_launch_workgroups // cfg.num_kv_heads
+            seen["mfma"] = ctx.kernel_info()["mfma"]
+            seen["log"] = log
+
+    wl = Workload(cfg)
+    want = oracle_log(cfg, wl, cfg.policy)
+    cap = sample_steps(want, every=every, edge=2, refills=4).__contains__
+    _, log, steps, captured, tokens, _ = run_gpu_group(cfg, cfg.policy, wl=wl, split=split, capture=cap,
+                                                       entry="decode_step_layers", inspect=grab)
+    assert log == want and np.array_equal(tokens, wl.L)
+    ncut = _count_cut_steps(cfg, want, seen["nj"], split, seen["mfma"])
+    assert ncut > 0, "no step took the cut path"
+    worst, n = check_against_oracle(cfg, wl, want, captured)
+    say(f"  [{name} cut pieces] {steps} steps ({ncut} cut), {n} outputs vs oracle max err {worst:.3g}")
