@@ -164,12 +164,13 @@ def mfma_flops(cfg, steplog, split=256, nj=None):
         from paper_2506_22950_amd import infs
 
         scmax = -(-cfg.max_suffix_len // split)
-        chunks = [-(-plen // 128) for plen in cfg.prompt_lens]
+        psplit = 256  # the step launch's MFMA prefix chunks
+        chunks = [-(-plen // psplit) for plen in cfg.prompt_lens]
 
         def plan(row):
             lens = [e[2] if e is not None else 0 for e in row]
             npi = sum(chunks[p] for p in {e[0] for e in row if e is not None})
-            roles, pieces = infs.step_split_plan(nj, lens, npi, 128, split, scmax)
+            roles, pieces = infs.step_split_plan(nj, lens, npi, psplit, split, scmax)
             return roles["cut"], pieces
 
     total = 0

@@ -338,16 +338,20 @@ infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
            the cuts, so that the most tokens one work-group reads after its layer's queries arrive is
            as small as it can be (a work-group holds one round of 256 tokens in registers before
            then).
-   mode 0: responses in chunks of split_tokens and work-groups divided in proportion to the chunk
-           counts, the partition of infs_decode_step: outputs then differ from a per-layer decode only
-           in the order the merges add partials.
+   Mode 1 also takes the prefix in chunks of 256 tokens on MFMA tiles with a bf16 cache (two
+   per-layer chunks, walked by the same work-group), which leaves more work-groups for the responses.
+   mode 0: responses in chunks of split_tokens, the prefix in the per-layer launch's chunks, and
+           work-groups divided in proportion to the chunk counts, the partition of infs_decode_step:
+           outputs then differ from a per-layer decode only in the order the merges add partials.
    Both give the same results up to rounding (mode 1 moves the split-K boundaries).  E_ARG for another
    mode; E_STATE while a step is open. */
 infs_status infs_set_step_split(infs_ctx* ctx, int32_t mode);
 
 /* The work split a step launch in `mode` (as infs_set_step_split) uses for one step, with nj
    work-groups per KV head (infs_step_launch_workgroups / num_kv_heads), S slots of which slot s holds
-   len[s] tokens (0 = idle), n_prefix_items prefix chunks of prefix_split tokens, response chunks of
+   len[s] tokens (0 = idle), n_prefix_items prefix chunks of prefix_split tokens (a step launch in mode 1
+   cuts the prefix into chunks of 256 tokens on MFMA tiles with a bf16 cache, 128 with an E4M3 cache,
+   split_tokens on the wavefront path), response chunks of
    `split` tokens (split_tokens of the context, 256 for 0) and at most scmax of them per slot
    (ceil(max_suffix_len / split)).  Writes pieces[0..S) (response items per slot) and roles[0..5) =
    {prefix work-groups, response work-groups, merge work-groups, response items, 1 if the responses

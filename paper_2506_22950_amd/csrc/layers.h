@@ -265,6 +265,7 @@ __device__ __forceinline__ void load_prefix_q(const StepArgs& a, const LayerView
 // Prefix item k of the step (prompt p, chunk c) and this wavefront's range.
 struct PrefixItem {
   int p, c, t0, t1;
+  int nbc;  // 32-token blocks of a whole chunk (the MFMA tiles split them over their token groups)
 };
 __device__ __forceinline__ PrefixItem prefix_item(const StepArgs& a, int k) {
   int p = 0;
@@ -274,6 +275,7 @@ __device__ __forceinline__ PrefixItem prefix_item(const StepArgs& a, int k) {
   it.c = k - a.prompt[p].item_begin;
   it.t0 = it.c * a.prefix_split;
   it.t1 = min(it.t0 + a.prefix_split, a.prompt[p].plen);
+  it.nbc = a.prefix_split / kMfmaBlock;
   return it;
 }
 
@@ -327,12 +329,14 @@ struct PrefixMfma {
     bf16x8 ka[2][KB], va[DB], kn[2][KB], vn[DB];
   };
   static constexpr int kBlockLoads = 2 * KB + DB;  // load instructions of one block
-  // This wavefront's blocks [b0, b1) of the chunk.
+  // This wavefront's blocks [b0, b1) of the chunk: its token group's share of
+  // the chunk's blocks (a step launch's chunks hold twice the per-layer
+  // launch's, see kStepPrefixSplit).
   __device__ __forceinline__ static void blocks(const PrefixItem& it, int& nblk, int& b0, int& b1) {
-    const int tg = (threadIdx.x >> 6) / SH::RG;
+    const int tg = (threadIdx.x >> 6) / SH::RG, bpw = it.nbc / SH::TG;
     nblk = (it.t1 - it.t0 + kMfmaBlock - 1) / kMfmaBlock;
-    b0 = tg * SH::BPW;
-    b1 = min(b0 + SH::BPW, nblk);
+    b0 = tg * bpw;
+    b1 = min(b0 + bpw, nblk);
   }
   __device__ __forceinline__ static const char* head(const StepArgs& a, const LayerView& V, const PrefixItem& it, int g) {
     return V.prefix + ((int64_t)(it.p * a.Hkv + g) * (a.max_prompt_len / kMfmaBlock)) * (2 * kMfmaBlock * D * SH::KES);

@@ -16,6 +16,7 @@ constexpr int kBlockThreads = 256; // 4 wavefronts of 64
 constexpr int kWaves = kBlockThreads / 64;
 constexpr int kMfmaBlock = 32;     // prefix tokens per MFMA block
 constexpr int kMfmaPrefixSplit = 4 * kMfmaBlock;  // MFMA prefix chunk: one block per wavefront
+constexpr int kStepPrefixSplit = 2 * kMfmaPrefixSplit;  // MFMA prefix chunk of a step launch (step_plan.h)
 constexpr int kMaxPartials = 128;  // prefix + response chunks merged for one slot
 constexpr int kMaxSplit = 4096;    // split-K chunk length limit (a wavefront covers <= 64 pages)
 

@@ -242,6 +242,7 @@ infs_status open_step(infs_ctx* c) {
     return fail(c, INFS_E_CAPACITY, "page pool exhausted: need %d pages, %zu free", need_pages, c->free_pages.size());
 
   StepArgs& a = c->plan;
+  a.prefix_split = c->prefix_split;  // a step launch may have lengthened the chunks of the last step
   int items = 0;
   std::vector<int> live(c->NP, 0);
   for (int s = 0; s < c->S; ++s)
@@ -330,6 +331,7 @@ infs_status open_probe(infs_ctx* c, int p, int first, int n, const uint8_t* live
   if (nlive > 0 && c->plen[p] < 0) return fail(c, INFS_E_STATE, "prompt %d has no prefilled prefix", p);
   StepArgs& a = c->pplan;
   a = c->plan;
+  a.prefix_split = c->prefix_split;
   a.S = n;
   a.m = n;
   a.num_prompts = 1;
@@ -840,7 +842,7 @@ infs_status launch_step_layers(infs_ctx* c, const KernelKey& key, StepArgs& a, i
   int32_t lens[infs::kMaxSlots], pieces[infs::kMaxSlots];
   for (int s = 0; s < a.S; ++s) lens[s] = a.slot[s].len;
   const infs::StepRoles roles =
-      c->step_split ? infs::plan_step_roles(nj, a.S, a.n_prefix_items, c->prefix_split, lens, c->split, c->scmax,
+      c->step_split ? infs::plan_step_roles(nj, a.S, a.n_prefix_items, a.prefix_split, lens, c->split, c->scmax,
                                             pieces)
                     : infs::plan_step_roles_chunks(nj, a.S, a.n_prefix_items, lens, c->split, pieces);
   if ((a.n_prefix_items > 0 && roles.n_pre < 1) || (roles.n_suffix_items > 0 && roles.n_suf < 1))
@@ -1014,6 +1016,21 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     a.prefix_layer_bytes = (int64_t)c->prefix_layer_bytes;
     a.pool_layer_bytes = (int64_t)c->pool_layer_bytes;
     a.merged = merged_counters(c);
+    if (c->step_split && c->key.mfma && !c->key.kv8) {
+      // MFMA prefix chunks of kStepPrefixSplit tokens: half as many prefix work-groups, each
+      // walking twice the blocks with the next block in flight, leave more work-groups to the
+      // responses (the records of 128-token chunks have room for them).  An E4M3 cache, with
+      // half the bytes per work-group, keeps the shorter chunks.
+      a.prefix_split = infs::kStepPrefixSplit;
+      int items = 0;
+      for (int p = 0; p < c->NP; ++p) {
+        infs::PromptPlan& pp = a.prompt[p];
+        pp.nchunks = pp.nchunks > 0 ? ceil_div(pp.plen, a.prefix_split) : 0;
+        pp.item_begin = items;
+        items += pp.nchunks;
+      }
+      a.n_prefix_items = items;
+    }
     infs_status st = launch_step_layers(c, c->key, a, c->layers_resident / c->Hkv, c->slot_arrivals.data(),
                                         c->merged_arrivals.data());
     if (st != INFS_OK) return st;

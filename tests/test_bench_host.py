@@ -52,14 +52,15 @@ def test_mfma_flops_closed_form():
     long = [[(0, 0, 300)] + [None] * 15]
     assert bench.mfma_flops(big, long) - bench.mfma_flops(big, one) == 28 * 10 * pair
     assert bench.mfma_flops(get_config("tiny_f32"), log) == 0  # fp32 contexts issue no MFMA
-    # Step launch with 64 work-groups per KV head: one 300-token response fits the chunks, so the
-    # count is the same.  Sixteen of 900 tokens (57 pages) are 64 chunks for 48 response
-    # work-groups, so the plan cuts each into 2 pieces for 44 (pages [0, 28) and [28, 57)):
-    # wavefronts of 7 pages (112 tokens, 4 pairs each) and of 8 pages (4, 4, 4 pairs, then 67
-    # stored tokens: 3) -- 31 pairs against the chunks' 8 + 8 + 8 + 5 = 29.
+    # Step launch with 64 work-groups per KV head (8 prefix chunks of 256 tokens): one 300-token
+    # response fits the chunks, so the count is the same.  Sixteen of 900 tokens (57 pages) are 64
+    # chunks for the chunk plan's 54 response work-groups, so the plan keeps 8 prefix work-groups
+    # and cuts each response into 3 pieces of 19 pages for the other 52: wavefronts of 5 pages
+    # (80 tokens, 3 pairs) and a last one of 4 pages (2 pairs; in the last piece 51 stored tokens,
+    # the newest apart: 2) -- 33 pairs against the chunks' 8 + 8 + 8 + 5 = 29.
     assert bench.mfma_flops(big, long, nj=64) == bench.mfma_flops(big, long)
     many = [[(0, i, 900) for i in range(16)]]
-    assert bench.mfma_flops(big, many, nj=64) - bench.mfma_flops(big, many) == 28 * 16 * 2 * pair
+    assert bench.mfma_flops(big, many, nj=64) - bench.mfma_flops(big, many) == 28 * 16 * 4 * pair
 
 
 def test_launches_per_entry():

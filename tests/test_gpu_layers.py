@@ -265,7 +265,7 @@ def test_probe_step_launch_f32_wave():
 def _count_cut_steps(cfg, log, nj, split, mfma):
     # Steps whose work split cuts the responses into near-equal pieces (the library's own plan).
     split = split or 256
-    psplit = 128 if mfma else split
+    psplit = 256 if mfma else split  # the step launch's MFMA prefix chunks hold 256 tokens
     scmax = -(-cfg.max_suffix_len // split)
     chunks = [-(-plen // psplit) for plen in cfg.prompt_lens]
     cut = 0
