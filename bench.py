@@ -875,7 +875,8 @@ def main():
                 "kernel_body_us": round(body_us, 3),
                 "kernel_body_timing": "device wall clock, first block start to last block end, averaged per launch",
                 "body_achieved": round(per_launch / (body_us * 1e-6) / 1e9, 1)}
-        mf = read_mfma(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.split or overrides) else None
+        mf = (read_mfma(args.workload, kernel) if not (args.reuse or args.kv_fp8 or args.split or overrides
+                                                       or args.step_split is not None) else None)
         if mf is not None:
             fl = float(mf["mfma_flops_per_launch"])
             roof["mfma"] = {"kernel": f"{kernel} (prefix and response contractions)", "flops_per_launch": round(fl),
