@@ -311,3 +311,17 @@ def test_step_launch_cut_pieces_multi_round(name):
     assert ncut > 0, "no step took the cut path"
     worst, n = check_against_oracle(cfg, wl, want, captured)
     say(f"  [{name} cut pieces] {steps} steps ({ncut} cut), {n} outputs vs oracle max err {worst:.3g}")
+
+
+@pytest.mark.parametrize("rows", [16, 128])
+def test_step_launch_prefix_tile_shapes(rows):
+    # The step launch's 256-token prefix chunks on the 16-row tile (four token groups, two
+    # blocks each; two prompts of 700 and 300 tokens) and the 128-row tile (one token group
+    # walking eight blocks; one prompt of 700 tokens), with partial last chunks; against the
+    # oracle and, with the per-layer partition, against per-layer launches.
+    m = rows // 2  # hpk = 2
+    prompts = (700, 300) if rows == 16 else (700,)
+    cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=prompts, samples_per_prompt=m + 4,
+                                             slots_per_prompt=m, length_dist=("lognormal", 3.5, 1.0, 1, 200),
+                                             max_suffix_len=200, pool_rows=None)
+    _layers_case(cfg, "sjf", every=5)
