@@ -164,12 +164,16 @@ def mfma_flops(cfg, steplog, split=256, nj=None):
         from paper_2506_22950_amd import infs
 
         scmax = -(-cfg.max_suffix_len // split)
-        psplit = 256  # the step launch's MFMA prefix chunks
-        chunks = [-(-plen // psplit) for plen in cfg.prompt_lens]
 
         def plan(row):
+            # the library's rule: the per-layer launch's 128-token prefix chunks unless they would
+            # give some producer two items, then 256-token chunks (bf16 MFMA tiles)
             lens = [e[2] if e is not None else 0 for e in row]
-            npi = sum(chunks[p] for p in {e[0] for e in row if e is not None})
+            live = {e[0] for e in row if e is not None}
+            npi = sum(-(-cfg.prompt_lens[p] // 128) for p in live)
+            r0, _ = infs.step_split_plan(nj, lens, npi, 128, split, scmax, mode=0)
+            psplit = 256 if (r0["items"] > r0["n_suf"] or r0["n_pre"] < npi) else 128
+            npi = sum(-(-cfg.prompt_lens[p] // psplit) for p in live)
             roles, pieces = infs.step_split_plan(nj, lens, npi, psplit, split, scmax)
             return roles["cut"], pieces
 

@@ -338,8 +338,9 @@ infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
            the cuts, so that the most tokens one work-group reads after its layer's queries arrive is
            as small as it can be (a work-group holds one round of 256 tokens in registers before
            then).
-   Mode 1 also takes the prefix in chunks of 256 tokens on MFMA tiles with a bf16 cache (two
-   per-layer chunks, walked by the same work-group), which leaves more work-groups for the responses.
+   Where the per-layer prefix chunks would give some work-group two items, mode 1 also takes the
+   prefix in chunks of 256 tokens on MFMA tiles with a bf16 cache (two per-layer chunks, walked by
+   the same work-group), which leaves more work-groups for the responses.
    mode 0: responses in chunks of split_tokens, the prefix in the per-layer launch's chunks, and
            work-groups divided in proportion to the chunk counts, the partition of infs_decode_step:
            outputs then differ from a per-layer decode only in the order the merges add partials.
@@ -350,8 +351,9 @@ infs_status infs_set_step_split(infs_ctx* ctx, int32_t mode);
 /* The work split a step launch in `mode` (as infs_set_step_split) uses for one step, with nj
    work-groups per KV head (infs_step_launch_workgroups / num_kv_heads), S slots of which slot s holds
    len[s] tokens (0 = idle), n_prefix_items prefix chunks of prefix_split tokens (a step launch in mode 1
-   cuts the prefix into chunks of 256 tokens on MFMA tiles with a bf16 cache, 128 with an E4M3 cache,
-   split_tokens on the wavefront path), response chunks of
+   takes the prefix in chunks of 128 tokens on MFMA tiles, or of 256 with a bf16 cache where the
+   128-token ones would give some work-group two items, and of split_tokens on the wavefront path),
+   response chunks of
    `split` tokens (split_tokens of the context, 256 for 0) and at most scmax of them per slot
    (ceil(max_suffix_len / split)).  Writes pieces[0..S) (response items per slot) and roles[0..5) =
    {prefix work-groups, response work-groups, merge work-groups, response items, 1 if the responses

@@ -115,6 +115,18 @@ inline StepRoles plan_step_roles_chunks(int nj, int S, int n_prefix_items, const
   return r;
 }
 
+// Whether a step launch takes the prefix in chunks of kStepPrefixSplit tokens
+// rather than the per-layer launch's (n_prefix_items of them): when the
+// per-layer chunks would leave some producer two items.  Longer chunks free
+// work-groups for the responses, but each prefix work-group then walks twice
+// the blocks after its layer's queries arrive, which lengthens a layer that
+// had room to spare.
+inline bool longer_prefix_chunks(int nj, int S, int n_prefix_items, const int32_t* len, int split) {
+  int32_t pieces[kMaxSlots];
+  const StepRoles r = plan_step_roles_chunks(nj, S, n_prefix_items, len, split, pieces);
+  return r.n_suffix_items > r.n_suf || r.n_pre < n_prefix_items;
+}
+
 // Roles of the nj work-groups per KV head and the response pieces of a step.
 // n_prefix_items prefix chunks of prefix_split tokens; live slot s has len[s]
 // tokens; the per-layer launch cuts responses into chunks of `split` tokens,

@@ -263,15 +263,22 @@ def test_probe_step_launch_f32_wave():
 
 
 def _count_cut_steps(cfg, log, nj, split, mfma):
-    # Steps whose work split cuts the responses into near-equal pieces (the library's own plan).
+    # Steps whose work split cuts the responses into near-equal pieces (the library's own plan;
+    # on MFMA tiles the prefix comes in 128-token chunks unless those would give some producer
+    # two items, then in 256-token chunks).
     split = split or 256
-    psplit = 256 if mfma else split  # the step launch's MFMA prefix chunks hold 256 tokens
     scmax = -(-cfg.max_suffix_len // split)
-    chunks = [-(-plen // psplit) for plen in cfg.prompt_lens]
     cut = 0
     for row in log:
         lens = [e[2] if e is not None else 0 for e in row]
-        npi = sum(chunks[p] for p in {e[0] for e in row if e is not None})
+        live = {e[0] for e in row if e is not None}
+        psplit = 128 if mfma else split
+        npi = sum(-(-cfg.prompt_lens[p] // psplit) for p in live)
+        if mfma:
+            r0, _ = infs.step_split_plan(nj, lens, npi, psplit, split, scmax, mode=0)
+            if r0["items"] > r0["n_suf"] or r0["n_pre"] < npi:
+                psplit = 256
+                npi = sum(-(-cfg.prompt_lens[p] // psplit) for p in live)
         roles, _ = infs.step_split_plan(nj, lens, npi, psplit, split, scmax)
         cut += roles["cut"]
     return cut
@@ -315,10 +322,11 @@ def test_step_launch_cut_pieces_multi_round(name):
 
 @pytest.mark.parametrize("rows", [16, 128])
 def test_step_launch_prefix_tile_shapes(rows):
-    # The step launch's 256-token prefix chunks on the 16-row tile (four token groups, two
-    # blocks each; two prompts of 700 and 300 tokens) and the 128-row tile (one token group
-    # walking eight blocks; one prompt of 700 tokens), with partial last chunks; against the
-    # oracle and, with the per-layer partition, against per-layer launches.
+    # The step launch's prefix chunks on the 16-row tile (four token groups; two prompts of
+    # 700 and 300 tokens) and the 128-row tile (one token group walking the chunk; one prompt of
+    # 700 tokens), with partial last chunks: 256-token chunks wherever the 128-token ones would
+    # give some producer two items; against the oracle and, with the per-layer partition,
+    # against per-layer launches.
     m = rows // 2  # hpk = 2
     prompts = (700, 300) if rows == 16 else (700,)
     cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=prompts, samples_per_prompt=m + 4,
