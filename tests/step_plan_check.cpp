@@ -3,7 +3,9 @@
 // checks the roles add up, that every live response's pieces are whole page
 // ranges covering it exactly (also per wavefront, as the kernel cuts them),
 // the bounds on pieces per slot and pages per piece, and that the cut is the
-// smallest largest piece a brute force over all piece counts finds.
+// smallest largest piece a brute force over all piece counts finds; and that
+// the step launch takes longer prefix chunks exactly when the per-layer chunks
+// would give some producer two items.
 #include <cstdio>
 #include <cstdlib>
 #include <random>
@@ -100,6 +102,21 @@ int main(int argc, char** argv) {
         ++live;
       }
     const int npi = live > 0 ? uni(0, 64) : 0;
+    // Longer prefix chunks exactly when dealing the per-layer chunks round robin over the
+    // chunk plan's work-groups would give some producer a second item (with two producers
+    // or more: with one, the runtime refuses the step launch).
+    if (nj - std::min(cdiv(S, kWaves), nj - 1) >= 2) {
+      std::vector<int32_t> chunk_pieces(S, -1);
+      const StepRoles c = plan_step_roles_chunks(nj, S, npi, len.data(), split, chunk_pieces.data());
+      int most = 0;
+      for (int i = 0; i < npi; ++i) most = std::max(most, i / std::max(c.n_pre, 1) + 1);
+      for (int i = 0; i < c.n_suffix_items; ++i) most = std::max(most, i / std::max(c.n_suf, 1) + 1);
+      CHECK(longer_prefix_chunks(nj, S, npi, len.data(), split) == (most > 1),
+            "case %d: longer prefix chunks %d with at most %d items per producer", cs,
+            (int)longer_prefix_chunks(nj, S, npi, len.data(), split), most);
+      if (npi > 0) CHECK(c.n_pre >= 1, "case %d: prefix chunks but no prefix work-group", cs);
+      if (c.n_suffix_items > 0) CHECK(c.n_suf >= 1, "case %d: response chunks but no response work-group", cs);
+    }
     const StepRoles r = plan_step_roles(nj, S, npi, prefix_split, len.data(), split, scmax, pieces.data());
     const int merge = std::min(cdiv(S, kWaves), nj - 1);
     CHECK(r.n_merge == merge, "case %d: %d merge work-groups, expected %d", cs, r.n_merge, merge);
