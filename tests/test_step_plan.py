@@ -3,8 +3,9 @@ tests/step_plan_check.cpp is built with g++ against the header alone and
 checks, over random slot lengths and launch shapes, that the roles add up,
 that the pieces of every live response are whole page ranges that tile it
 (per wavefront too, as the kernel cuts them) within the bounds on pieces per
-slot and pages per wavefront, and that the cut matches an exhaustive search
-for the smallest largest piece."""
+slot and pages per wavefront, that the cut matches an exhaustive search
+for the smallest largest piece, and that longer prefix chunks are chosen
+exactly when the per-layer chunks would give some producer two items."""
 
 import os
 import shutil
