@@ -658,7 +658,7 @@ class Bench:
         return (ms, region_ms, n, st.alg_bytes - before.alg_bytes, st.launches - before.launches), probe
 
 
-CPU_POOL_MAX = 16  # worker processes at most (the host share of one GPU machine)
+CPU_POOL_MAX = 16  # worker processes at most (a host's CPU share per GPU)
 
 
 def _oracle_worker_init(cfg_name, overrides):

@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol():
 
 
 def _oracle_log(cfg, L, policy, pred):
-    """Oracle step log in the driver's format: per step, per slot (p, i, t) or None."""
+    """Oracle step log in the format of group.plan_steps: per step, per slot (p, i, t) or None."""
     total, res = simulate_group(L, cfg.slots_per_prompt, policy, pred)
     m = cfg.slots_per_prompt
     log = []
