@@ -167,7 +167,7 @@ def mfma_flops(cfg, steplog, split=256, nj=None):
 
         def plan(row):
             # the library's rule: the per-layer launch's 128-token prefix chunks unless they would
-            # give some producer two items, then 256-token chunks (bf16 MFMA tiles)
+            # give some producer two items, then 256-token chunks (MFMA tiles, bf16 or E4M3 cache)
             lens = [e[2] if e is not None else 0 for e in row]
             live = {e[0] for e in row if e is not None}
             npi = sum(-(-cfg.prompt_lens[p] // 128) for p in live)

@@ -339,7 +339,7 @@ infs_status infs_set_exchange(infs_ctx* ctx, int32_t mode);
            as small as it can be (a work-group holds one round of 256 tokens in registers before
            then).
    Where the per-layer prefix chunks would give some work-group two items, mode 1 also takes the
-   prefix in chunks of 256 tokens on MFMA tiles with a bf16 cache (two per-layer chunks, walked by
+   prefix in chunks of 256 tokens on MFMA tiles, bf16 or E4M3 cache (two per-layer chunks, walked by
    the same work-group), which leaves more work-groups for the responses.
    mode 0: responses in chunks of split_tokens, the prefix in the per-layer launch's chunks, and
            work-groups divided in proportion to the chunk counts, the partition of infs_decode_step:
@@ -351,7 +351,7 @@ infs_status infs_set_step_split(infs_ctx* ctx, int32_t mode);
 /* The work split a step launch in `mode` (as infs_set_step_split) uses for one step, with nj
    work-groups per KV head (infs_step_launch_workgroups / num_kv_heads), S slots of which slot s holds
    len[s] tokens (0 = idle), n_prefix_items prefix chunks of prefix_split tokens (a step launch in mode 1
-   takes the prefix in chunks of 128 tokens on MFMA tiles, or of 256 with a bf16 cache where the
+   takes the prefix in chunks of 128 tokens on MFMA tiles, or of 256 where the
    128-token ones would give some work-group two items, and of split_tokens on the wavefront path),
    response chunks of
    `split` tokens (split_tokens of the context, 256 for 0) and at most scmax of them per slot

@@ -1018,13 +1018,12 @@ infs_status infs_decode_step_layers(infs_ctx* c, const void* q_dev, const void* 
     a.merged = merged_counters(c);
     int32_t lens[infs::kMaxSlots];
     for (int s = 0; s < c->S; ++s) lens[s] = a.slot[s].len;
-    if (c->step_split && c->key.mfma && !c->key.kv8 &&
+    if (c->step_split && c->key.mfma &&
         infs::longer_prefix_chunks(c->layers_resident / c->Hkv, c->S, a.n_prefix_items, lens, c->split)) {
-      // MFMA prefix chunks of kStepPrefixSplit tokens when the per-layer chunks would give some
-      // producer two items: half as many prefix work-groups, each walking twice the blocks with
-      // the next block in flight, leave more work-groups to the responses (the records of
-      // 128-token chunks have room for them).  An E4M3 cache, with half the bytes per
-      // work-group, keeps the shorter chunks.
+      // MFMA prefix chunks of kStepPrefixSplit tokens (bf16 or E4M3 cache) when the per-layer
+      // chunks would give some producer two items: half as many prefix work-groups, each walking
+      // twice the blocks with the next block in flight, leave more work-groups to the responses
+      // (the records of 128-token chunks have room for them).
       a.prefix_split = infs::kStepPrefixSplit;
       int items = 0;
       for (int p = 0; p < c->NP; ++p) {

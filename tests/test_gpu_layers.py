@@ -320,16 +320,42 @@ def test_step_launch_cut_pieces_multi_round(name):
     say(f"  [{name} cut pieces] {steps} steps ({ncut} cut), {n} outputs vs oracle max err {worst:.3g}")
 
 
-@pytest.mark.parametrize("rows", [16, 128])
-def test_step_launch_prefix_tile_shapes(rows):
-    # The step launch's prefix chunks on the 16-row tile (four token groups; two prompts of
-    # 700 and 300 tokens) and the 128-row tile (one token group walking the chunk; one prompt of
-    # 700 tokens), with partial last chunks: 256-token chunks wherever the 128-token ones would
-    # give some producer two items; against the oracle and, with the per-layer partition,
-    # against per-layer launches.
+@pytest.mark.parametrize("rows,kv_fp8", [(16, False), (128, False), (16, True), (128, True)],
+                         ids=["16_bf16", "128_bf16", "16_fp8", "128_fp8"])
+def test_step_launch_prefix_tile_shapes(rows, kv_fp8):
+    # The step launch's prefix chunks on the 16-row tile (four token groups; four prompts of
+    # 700, 300, 500 and 400 tokens, responses of about 300 tokens, so that the chunks outnumber
+    # the producers) and the 128-row tile (one token group walking the chunk; one prompt of 700
+    # tokens), with partial last chunks, bf16 and E4M3 caches: 256-token chunks wherever the
+    # 128-token ones would give some producer two items; against the oracle and, with the
+    # per-layer partition, against per-layer launches.  The test asserts that some step took the
+    # longer chunks.
     m = rows // 2  # hpk = 2
-    prompts = (700, 300) if rows == 16 else (700,)
+    if rows == 16:
+        prompts, dist, longest, every = (700, 300, 500, 400), ("lognormal", 5.7, 0.2, 1, 400), 400, 15
+    else:
+        prompts, dist, longest, every = (700,), ("lognormal", 3.5, 1.0, 1, 200), 200, 5
     cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=prompts, samples_per_prompt=m + 4,
-                                             slots_per_prompt=m, length_dist=("lognormal", 3.5, 1.0, 1, 200),
-                                             max_suffix_len=200, pool_rows=None)
-    _layers_case(cfg, "sjf", every=5)
+                                             slots_per_prompt=m, length_dist=dist, max_suffix_len=longest,
+                                             pool_rows=None)
+    seen = {}
+
+    def grab(ctx, step, log):
+        if not seen:
+            seen["nj"] = ctx.step_launch_workgroups // cfg.num_kv_heads
+
+    wl = Workload(cfg)
+    want = oracle_log(cfg, wl, "sjf")
+    run_gpu_group(cfg, "sjf", wl=wl, split=128, capture=lambda k: False, kv_fp8=kv_fp8, stop_after=1,
+                  entry="decode_step_layers", inspect=grab)
+    nj = seen["nj"]
+    longer = 0
+    for row in want:
+        lens = [e[2] if e is not None else 0 for e in row]
+        live = {e[0] for e in row if e is not None}
+        npi = sum(-(-cfg.prompt_lens[p] // 128) for p in live)
+        r0, _ = infs.step_split_plan(nj, lens, npi, 128, 128, -(-cfg.max_suffix_len // 128), mode=0)
+        longer += r0["items"] > r0["n_suf"] or r0["n_pre"] < npi
+    assert longer > 0, "no step took the longer prefix chunks"
+    say(f"  [{rows}-row prefix tile] {longer} of {len(want)} steps take 256-token prefix chunks")
+    _layers_case(cfg, "sjf", every=every, kv_fp8=kv_fp8)
