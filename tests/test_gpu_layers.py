@@ -104,17 +104,19 @@ def test_step_launch_alternating_with_layer_launches():
     _layers_case(cfg, "sjf", every=2, entry=lambda step: "decode_step_layers" if step % 2 else "decode_step")
 
 
-@pytest.mark.parametrize("name,every,window", [
-    ("qwen3_1p7b_g64", 397, 512),
-    ("longtail_g128", 997, 256),
-    ("qwen3_8b_4prompts", 1201, 128),
-])
-def test_step_launch_full_size_sampled(name, every, window):
+@pytest.mark.parametrize("name,every,window,kv_fp8", [
+    ("qwen3_1p7b_g64", 397, 512, False),
+    ("qwen3_1p7b_g64", 397, 512, True),
+    ("longtail_g128", 997, 256, False),
+    ("qwen3_8b_4prompts", 1201, 128, False),
+], ids=["qwen3_1p7b_g64", "qwen3_1p7b_g64_e4m3", "longtail_g128", "qwen3_8b_4prompts"])
+def test_step_launch_full_size_sampled(name, every, window, kv_fp8):
     # Whole workload, one step launch per running step (the benchmark's
-    # configuration); sampled steps on the first, middle and last layer.
+    # configuration, with the bf16 cache and, for the benchmark workload, the
+    # E4M3 cache); sampled steps on the first, middle and last layer.
     cfg = get_config(name)
     _layers_case(cfg, cfg.policy, split=0, every=every, layers=(0, cfg.layers // 2, cfg.layers - 1),
-                 window=window, against_layer_path=False)
+                 window=window, against_layer_path=False, kv_fp8=kv_fp8)
 
 
 def test_step_launch_wait_give_up_is_reported():
@@ -284,13 +286,14 @@ def _count_cut_steps(cfg, log, nj, split, mfma):
     return cut
 
 
-@pytest.mark.parametrize("name", ["bf16_mfma", "f32_wave"])
+@pytest.mark.parametrize("name", ["bf16_mfma", "e4m3_mfma", "f32_wave"])
 def test_step_launch_cut_pieces_multi_round(name):
     # Long responses on few slots: the per-layer chunks outnumber the response work-groups, so
     # the step launch cuts the responses into pieces of several load rounds per wavefront
-    # (MFMA tiles, and the fp32 wavefront path); checked against the oracle, and the test
-    # asserts that the cut path ran.
-    if name == "bf16_mfma":
+    # (MFMA tiles on bf16 and E4M3 pages, and the fp32 wavefront path); checked against the
+    # oracle, and the test asserts that the cut path ran.
+    kv_fp8 = name == "e4m3_mfma"
+    if name in ("bf16_mfma", "e4m3_mfma"):
         cfg = get_config("qwen3_1p7b_g64").with_(layers=2, prompt_lens=(256,), samples_per_prompt=16,
                                                  slots_per_prompt=16, length_dist=("uniform", 900, 1400),
                                                  max_suffix_len=1400, pool_rows=None)
@@ -312,11 +315,11 @@ def test_step_launch_cut_pieces_multi_round(name):
     want = oracle_log(cfg, wl, cfg.policy)
     cap = sample_steps(want, every=every, edge=2, refills=4).__contains__
     _, log, steps, captured, tokens, _ = run_gpu_group(cfg, cfg.policy, wl=wl, split=split, capture=cap,
-                                                       entry="decode_step_layers", inspect=grab)
+                                                       entry="decode_step_layers", inspect=grab, kv_fp8=kv_fp8)
     assert log == want and np.array_equal(tokens, wl.L)
     ncut = _count_cut_steps(cfg, want, seen["nj"], split, seen["mfma"])
     assert ncut > 0, "no step took the cut path"
-    worst, n = check_against_oracle(cfg, wl, want, captured)
+    worst, n = check_against_oracle(cfg, wl, want, captured, kv_fp8=kv_fp8)
     say(f"  [{name} cut pieces] {steps} steps ({ncut} cut), {n} outputs vs oracle max err {worst:.3g}")
 
 
